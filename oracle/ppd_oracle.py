@@ -1,0 +1,423 @@
+"""CPU oracle for the Parallel Prompt Decoding (PPD) tree-verification step.
+
+TEST INFRASTRUCTURE.  Only the test-suite, the smoke check and the benchmark's
+CPU-baseline leg may import this module.  The GPU library never calls it and
+shares no code with it.
+
+Plain, slow, float64 numpy.  Each function restates what the paper computes:
+
+* Section 3 (guess-and-verify in one step): the tree of candidate tokens, with
+  prompt tokens appended, goes through one forward pass of the frozen decoder;
+  candidates are verified by exact matching against the model's greedy token;
+  the accepted candidates enter the sequence and the KV cache.
+* Section 3.1: a prompt token stands at the position of the future token it
+  approximates, so a node at depth k of the tree sits at position L + k.
+* Section 4.1 (customised sparse tree attention, after SpecInfer): every node
+  attends to the cached prefix, to its own ancestors and to itself, and to
+  nothing else, so many candidates are scored without growing the batch.
+* Section 5.4 (memory): a single KV cache is shared by guessing and
+  verification; only accepted tokens are committed to it.
+
+The decoder is Llama-style (the paper's MobileLLaMA / Vicuna family):
+pre-RMSNorm, rotary position embedding with rotate-half pairing, multi-head
+(optionally grouped) attention, SwiGLU MLP, tied nothing.
+
+Precision.  Every sum is taken in float64.  With `store="bf16"` (or "f32") the
+oracle rounds to that storage type exactly where the GPU path stores values in
+it: weights and embeddings (already rounded on input), keys/values/queries after
+RoPE, and the input operand of every matrix product (attention output, SwiGLU
+output, and the RMS-normalised activations, see `normed_rows`).  The residual
+stream, softmax and logits are not rounded.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# storage rounding
+
+
+def round_store(x: np.ndarray, store: Optional[str]) -> np.ndarray:
+    """Round float64 values to the storage type and return them as float64.
+
+    "bf16": round to nearest even on the bfloat16 grid (via float32, whose
+    rounding is also to nearest even).  "f32": float32.  None: unchanged."""
+    if store is None:
+        return x
+    x32 = np.asarray(x, dtype=np.float32)
+    if store == "f32":
+        return x32.astype(np.float64)
+    if store == "bf16":
+        b = x32.view(np.uint32).astype(np.uint64)
+        nan = np.isnan(x32)
+        b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+        out = b.astype(np.uint32).view(np.float32).astype(np.float64)
+        out[nan] = np.nan
+        return out
+    raise ValueError(store)
+
+
+def to_f64(t) -> np.ndarray:
+    """torch tensor (any float dtype, any device) or array -> float64 numpy."""
+    if hasattr(t, "detach"):
+        t = t.detach()
+        if t.dtype.is_floating_point and t.element_size() < 4:
+            t = t.float()
+        return t.cpu().numpy().astype(np.float64)
+    return np.asarray(t, dtype=np.float64)
+
+
+# ----------------------------------------------------------------------------
+# model container
+
+
+class Model:
+    """Weights of one decoder, converted to float64 on access.
+
+    `w` is the dict produced by `synth.model.make_weights` (torch tensors) or
+    an equivalent dict of arrays.  Layers are converted lazily and not kept,
+    so a 7B-shaped model fits in host memory as its bf16 original."""
+
+    def __init__(self, shape, w: Dict, keep_layers: bool = True):
+        self.shape = shape
+        self._w = w
+        self._keep = keep_layers
+        self._cache: Dict[int, Dict[str, np.ndarray]] = {}
+        self.tok_emb_src = w["tok_emb"]
+        self.prompt_emb = to_f64(w["prompt_emb"])
+        self.final_norm = to_f64(w["final_norm"])
+        self._lm_head = None
+
+    @property
+    def lm_head(self) -> np.ndarray:
+        if self._lm_head is None:
+            self._lm_head = to_f64(self._w["lm_head"])
+        return self._lm_head
+
+    def embed_row(self, token: int) -> np.ndarray:
+        return to_f64(self.tok_emb_src[int(token)])
+
+    def layer(self, l: int) -> Dict[str, np.ndarray]:
+        if l in self._cache:
+            return self._cache[l]
+        src = self._w["layers"][l]
+        lay = {k: to_f64(v) for k, v in src.items()}
+        if self._keep:
+            self._cache[l] = lay
+        return lay
+
+
+# ----------------------------------------------------------------------------
+# tree structure (Section 4.1)
+
+
+def validate_tree(parent: Sequence[int]) -> None:
+    """Topologically ordered tree: parent[0] = -1 (root), 0 <= parent[i] < i."""
+    p = np.asarray(parent)
+    if p.ndim != 1 or p.size < 1 or p[0] != -1:
+        raise ValueError("parent[0] must be -1")
+    for i in range(1, p.size):
+        if not (0 <= p[i] < i):
+            raise ValueError(f"parent[{i}]={p[i]} is not an earlier node")
+
+
+def build_mask(parent: Sequence[int]) -> Tuple[np.ndarray, np.ndarray]:
+    """depth[i] (root = 0) and the tree attention mask.
+
+    anc[i, j] is True iff node j lies on the root-to-i path (j == i included):
+    the only tree nodes i may attend to (Section 4.1)."""
+    validate_tree(parent)
+    T = len(parent)
+    depth = np.zeros(T, np.int64)
+    anc = np.zeros((T, T), bool)
+    for i in range(T):
+        j = i
+        while j != -1:
+            anc[i, j] = True
+            j = int(parent[j])
+        depth[i] = anc[i].sum() - 1
+    return depth, anc
+
+
+def pack_mask(anc: np.ndarray, words: int = 2) -> np.ndarray:
+    """Bit-packed mask rows: bit (j mod 64) of word j // 64 is anc[i, j]."""
+    T = anc.shape[0]
+    out = np.zeros((T, words), np.uint64)
+    for i in range(T):
+        for j in range(T):
+            if anc[i, j]:
+                out[i, j // 64] |= np.uint64(1) << np.uint64(j % 64)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# decoder building blocks
+
+
+def rms_scale(x: np.ndarray, eps: float) -> np.ndarray:
+    """Per-row RMSNorm factor 1 / sqrt(mean(x^2) + eps)."""
+    return 1.0 / np.sqrt(np.mean(x * x, axis=-1) + eps)
+
+
+def normed_rows(x: np.ndarray, g: np.ndarray, eps: float, store) -> Tuple[np.ndarray, np.ndarray]:
+    """RMSNorm(x) * g, split as (rounded operand, row scale).
+
+    RMSNorm(x)_k * g_k = r * (x_k * g_k) with r = 1/sqrt(mean(x^2) + eps).  The
+    GPU stores x*g in the storage type and applies r to each output row of the
+    following matrix product, which is the same product up to rounding; the
+    oracle rounds at the same point.  Returns (round(x*g), r)."""
+    return round_store(x * g, store), rms_scale(x, eps)
+
+
+def rope_tables(pos: np.ndarray, d: int, base: float) -> Tuple[np.ndarray, np.ndarray]:
+    """cos/sin of pos * base^(-2i/d), i < d/2 (rotary embedding)."""
+    i = np.arange(d // 2, dtype=np.float64)
+    inv = base ** (-2.0 * i / d)
+    ang = np.asarray(pos, np.float64)[:, None] * inv[None, :]
+    return np.cos(ang), np.sin(ang)
+
+
+def apply_rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    """Rotate-half rotary embedding; x [n, heads, d], cos/sin [n, d/2].
+
+    Pairs (i, i + d/2) rotate by the angle of frequency i."""
+    h = x.shape[-1] // 2
+    a, b = x[..., :h], x[..., h:]
+    c, s = cos[:, None, :], sin[:, None, :]
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    return x / (1.0 + np.exp(-x))
+
+
+def softmax_rows(s: np.ndarray) -> np.ndarray:
+    m = np.max(s, axis=-1, keepdims=True)
+    e = np.exp(s - m)
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def embed(model: Model, ids: Sequence[int]) -> np.ndarray:
+    """Token embedding for ids < vocab; prompt-token embedding ids - vocab else
+    (prompt tokens are trained embeddings appended to the input, Section 3)."""
+    V = model.shape.vocab
+    rows = []
+    for t in ids:
+        t = int(t)
+        if 0 <= t < V:
+            rows.append(model.embed_row(t))
+        elif V <= t < V + model.shape.n_prompt:
+            rows.append(model.prompt_emb[t - V])
+        else:
+            raise ValueError(f"token id {t} out of range")
+    return np.stack(rows)
+
+
+# ----------------------------------------------------------------------------
+# the verification forward pass (Sections 3 and 4.1)
+
+
+def verify_forward(model: Model, k_cache: Sequence[np.ndarray], v_cache: Sequence[np.ndarray],
+                   L: int, ids: Sequence[int], parent: Sequence[int],
+                   store: Optional[str]) -> Dict:
+    """One forward pass over all T tree nodes.
+
+    k_cache[l] / v_cache[l]: [n_kv_heads, >=L, d] float64 keys (after RoPE) and
+    values of the accepted prefix.  Node i sits at position L + depth[i] and
+    attends to cache positions [0, L) and to its tree ancestors and itself.
+
+    Returns logits [T, vocab], the tree keys/values per layer
+    ([n_kv_heads, T, d], rounded to the storage type) and depth."""
+    sh = model.shape
+    T = len(ids)
+    depth, anc = build_mask(parent)
+    pos = L + depth
+    cos, sin = rope_tables(pos, sh.head_dim, sh.rope_base)
+    nh, nkv, d = sh.n_heads, sh.n_kv_heads, sh.head_dim
+    grp = nh // nkv
+    x = embed(model, ids)                                   # residual stream
+    tree_k, tree_v = [], []
+    for l in range(sh.n_layers):
+        lay = model.layer(l)
+        a, r = normed_rows(x, lay["attn_norm"], sh.rms_eps, store)
+        qkv = r[:, None] * (a @ lay["w_qkv"].T)
+        q = qkv[:, :nh * d].reshape(T, nh, d)
+        k = qkv[:, nh * d:(nh + nkv) * d].reshape(T, nkv, d)
+        v = qkv[:, (nh + nkv) * d:].reshape(T, nkv, d)
+        q = round_store(apply_rope(q, cos, sin), store)
+        k = round_store(apply_rope(k, cos, sin), store)
+        v = round_store(v, store)
+        kt = k.transpose(1, 0, 2)                           # [nkv, T, d]
+        vt = v.transpose(1, 0, 2)
+        tree_k.append(kt)
+        tree_v.append(vt)
+        o = np.zeros((T, nh, d))
+        for h in range(nh):
+            kh = np.concatenate([k_cache[l][h // grp][:L], kt[h // grp]], axis=0)
+            vh = np.concatenate([v_cache[l][h // grp][:L], vt[h // grp]], axis=0)
+            s = (q[:, h, :] @ kh.T) / np.sqrt(d)            # [T, L+T]
+            s[:, L:][~anc] = -np.inf                        # tree part: ancestors only
+            o[:, h, :] = softmax_rows(s) @ vh
+        o = round_store(o.reshape(T, nh * d), store)
+        x = x + o @ lay["w_o"].T
+        a, r = normed_rows(x, lay["mlp_norm"], sh.rms_eps, store)
+        gu = r[:, None] * (a @ lay["w_gate_up"].T)
+        act = round_store(silu(gu[:, :sh.ffn]) * gu[:, sh.ffn:], store)
+        x = x + act @ lay["w_down"].T
+    a, r = normed_rows(x, model.final_norm, sh.rms_eps, store)
+    logits = r[:, None] * (a @ model.lm_head.T)
+    return {"logits": logits, "tree_k": tree_k, "tree_v": tree_v, "depth": depth}
+
+
+def argmax_first(logits: np.ndarray) -> np.ndarray:
+    """Greedy token per row: the smallest index attaining the maximum."""
+    return np.argmax(logits, axis=-1).astype(np.int64)
+
+
+# ----------------------------------------------------------------------------
+# verification and acceptance (Section 3: exact matching)
+
+
+def accept(parent: Sequence[int], ids: Sequence[int], pred: Sequence[int], vocab: int):
+    """Exact-matching verification and acceptance.
+
+    A candidate is verified when its token equals the greedy prediction at its
+    parent and its parent is verified (the root always is).  Prompt nodes are
+    never verified.  The accepted path is the deepest verified node's root
+    path (ties: smallest node index).  Tokens emitted this step are the
+    accepted candidates plus the bonus token pred[best]: n_path of them, so a
+    root-only tree emits exactly one token, as vanilla decoding does.
+
+    Returns (path root-first, n_path, next_tok)."""
+    T = len(parent)
+    depth, _ = build_mask(parent)
+    ok = np.zeros(T, bool)
+    ok[0] = True
+    for i in range(1, T):
+        p = int(parent[i])
+        ok[i] = ok[p] and 0 <= int(ids[i]) < vocab and int(ids[i]) == int(pred[p])
+    best = 0
+    for i in range(1, T):
+        if ok[i] and depth[i] > depth[best]:
+            best = i
+    path = []
+    j = best
+    while j != -1:
+        path.append(j)
+        j = int(parent[j])
+    path = path[::-1]
+    return np.asarray(path, np.int64), len(path), int(pred[best])
+
+
+def kv_compact(k_cache: List[np.ndarray], v_cache: List[np.ndarray], tree_k, tree_v,
+               L: int, path: Sequence[int]):
+    """Commit the accepted nodes' keys/values: cache[L + k] = tree[path[k]].
+
+    Prompt-token keys/values are never committed: one shared cache (Section
+    5.4).  Returns the new cache length L + len(path)."""
+    for l in range(len(k_cache)):
+        for kk, node in enumerate(path):
+            k_cache[l][:, L + kk, :] = tree_k[l][:, node, :]
+            v_cache[l][:, L + kk, :] = tree_v[l][:, node, :]
+    return L + len(path)
+
+
+# ----------------------------------------------------------------------------
+# plain causal decoding (the reference behaviour the tree step must reproduce)
+
+
+def decode_token(model: Model, k_cache: List[np.ndarray], v_cache: List[np.ndarray],
+                 L: int, token: int, store: Optional[str]) -> np.ndarray:
+    """Ordinary one-token decode at position L with a growing KV cache.
+
+    Appends the token's keys/values at position L of every layer (caches must
+    have room) and returns its logits.  No tree, no mask: the token sees
+    positions [0, L] only."""
+    sh = model.shape
+    nh, nkv, d = sh.n_heads, sh.n_kv_heads, sh.head_dim
+    grp = nh // nkv
+    cos, sin = rope_tables(np.array([L]), d, sh.rope_base)
+    x = embed(model, [token])
+    for l in range(sh.n_layers):
+        lay = model.layer(l)
+        a, r = normed_rows(x, lay["attn_norm"], sh.rms_eps, store)
+        qkv = r[:, None] * (a @ lay["w_qkv"].T)
+        q = round_store(apply_rope(qkv[:, :nh * d].reshape(1, nh, d), cos, sin), store)
+        k = round_store(apply_rope(qkv[:, nh * d:(nh + nkv) * d].reshape(1, nkv, d), cos, sin), store)
+        v = round_store(qkv[:, (nh + nkv) * d:].reshape(1, nkv, d), store)
+        k_cache[l][:, L, :] = k[0]
+        v_cache[l][:, L, :] = v[0]
+        o = np.zeros((nh, d))
+        for h in range(nh):
+            kh = k_cache[l][h // grp][:L + 1]
+            vh = v_cache[l][h // grp][:L + 1]
+            s = kh @ q[0, h] / np.sqrt(d)
+            p = np.exp(s - s.max())
+            o[h] = (p / p.sum()) @ vh
+        o = round_store(o.reshape(1, nh * d), store)
+        x = x + o @ lay["w_o"].T
+        a, r = normed_rows(x, lay["mlp_norm"], sh.rms_eps, store)
+        gu = r[:, None] * (a @ lay["w_gate_up"].T)
+        act = round_store(silu(gu[:, :sh.ffn]) * gu[:, sh.ffn:], store)
+        x = x + act @ lay["w_down"].T
+    a, r = normed_rows(x, model.final_norm, sh.rms_eps, store)
+    return (r[:, None] * (a @ model.lm_head.T))[0]
+
+
+def new_cache(model: Model, capacity: int):
+    sh = model.shape
+    k = [np.zeros((sh.n_kv_heads, capacity, sh.head_dim)) for _ in range(sh.n_layers)]
+    v = [np.zeros((sh.n_kv_heads, capacity, sh.head_dim)) for _ in range(sh.n_layers)]
+    return k, v
+
+
+def copy_cache(k_cache, v_cache):
+    return [a.copy() for a in k_cache], [a.copy() for a in v_cache]
+
+
+def causal_logits(model: Model, k_cache, v_cache, L: int, tokens: Sequence[int],
+                  store: Optional[str]) -> np.ndarray:
+    """Logits after each of `tokens` fed one by one at positions L, L+1, ...
+
+    Works on copies, so the given caches are unchanged (brute-force check of
+    one tree path)."""
+    kc, vc = copy_cache(k_cache, v_cache)
+    out = []
+    for j, t in enumerate(tokens):
+        out.append(decode_token(model, kc, vc, L + j, t, store))
+    return np.stack(out)
+
+
+def prefill(model: Model, tokens: Sequence[int], capacity: int, store: Optional[str]):
+    """KV cache of a prompt, built by plain one-token decoding."""
+    kc, vc = new_cache(model, capacity)
+    last = None
+    for j, t in enumerate(tokens):
+        last = decode_token(model, kc, vc, j, t, store)
+    return kc, vc, last
+
+
+def greedy_decode(model: Model, k_cache, v_cache, L: int, first_token: int, n: int,
+                  store: Optional[str]) -> List[int]:
+    """Vanilla greedy continuation: feed first_token at L, then n-1 more tokens.
+
+    Returns the n tokens emitted after first_token (works on copies)."""
+    kc, vc = copy_cache(k_cache, v_cache)
+    out, tok = [], int(first_token)
+    for j in range(n):
+        logits = decode_token(model, kc, vc, L + j, tok, store)
+        tok = int(np.argmax(logits))
+        out.append(tok)
+    return out
+
+
+def path_tokens(parent: Sequence[int], ids: Sequence[int], node: int) -> List[int]:
+    """Token ids on the root-to-node path, root first."""
+    seq = []
+    j = int(node)
+    while j != -1:
+        seq.append(int(ids[j]))
+        j = int(parent[j])
+    return seq[::-1]

@@ -1,0 +1,402 @@
+"""Pins of the CPU oracle against things other than itself.
+
+* HuggingFace Llama (a library implementation) driven by a custom 4-D mask and
+  position ids reproduces the oracle's tree logits and prefill cache.
+* Brute force: every tree node's logits equal an ordinary token-by-token
+  causal decode of its root-to-node path (Section 4.1: ancestors-only
+  attention; Section 3.1: prompt tokens at the positions of the tokens they
+  stand for).
+* Special cases: a chain tree is causal multi-token decoding; a one-node tree
+  is vanilla one-token decoding (Table 1: vanilla tau = 1.00).
+* Invariants: non-ancestor nodes do not influence a node; relabelling nodes
+  permutes rows.
+* Closed forms for RMSNorm, rotary embedding, SiLU, softmax, bf16 rounding.
+* Acceptance: brute-force enumeration of root paths; Proposition 1's expected
+  accept length by Monte Carlo; multi-step losslessness (Section 5.1: greedy
+  output is identical to the original model's).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from synth import workload
+from synth.configs import ModelShape
+from synth.model import make_weights, tokens
+from synth.trees import make_tree, tree_from_parents
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+MICRO = ModelShape("micro", 2, 64, 4, 2, 16, 96, 50, "f32")
+
+
+def _setup(w, gain_std=0.1, store="f32", L=None, shape=None):
+    sh = shape or w.shape
+    W = make_weights(sh, w.seeds["weights"], gain_std=gain_std)
+    m = O.Model(sh, W)
+    L = w.cache_len if L is None else L
+    ids = tokens(L + 1, sh.vocab, w.seeds["tokens"]).numpy()
+    kc, vc, _ = O.prefill(m, ids[:-1], L + 160, store)
+    return sh, W, m, kc, vc, L, int(ids[-1])
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return _setup(workload("tiny"))
+
+
+# ---------------------------------------------------------------- library pin
+
+def test_matches_hf_llama_tree_forward():
+    from hf_reference import build_hf_llama, hf_prefill, hf_tree_logits
+    w = workload("tiny", cache_len=48)
+    sh, W, m, kc, vc, L, root = _setup(w, store=None)
+    hf = build_hf_llama(sh, W)
+    ids = tokens(L + 1, sh.vocab, w.seeds["tokens"]).numpy()
+    hf_logits, pkv = hf_prefill(hf, ids[:-1])
+    k_hf = pkv.layers[1].keys[0].numpy()
+    v_hf = pkv.layers[1].values[0].numpy()
+    assert np.abs(k_hf - kc[1][:, :L]).max() < 1e-5
+    assert np.abs(v_hf - vc[1][:, :L]).max() < 1e-5
+    for seed in range(3):
+        tree = make_tree("candidates:10", sh.vocab, 3, 4, 77 + seed, root)
+        res = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, None)
+        depth, anc = O.build_mask(tree.parent)
+        ref = hf_tree_logits(hf, pkv, L, tree.ids, depth, anc, sh.vocab)
+        assert np.abs(ref - res["logits"]).max() < 2e-5
+
+
+def test_matches_hf_llama_gqa():
+    from hf_reference import build_hf_llama, hf_prefill, hf_tree_logits
+    w = workload("small-gqa")
+    sh = MICRO
+    W = make_weights(sh, 5, gain_std=0.2)
+    m = O.Model(sh, W)
+    ids = tokens(21, sh.vocab, 6).numpy()
+    kc, vc, _ = O.prefill(m, ids[:-1], 64, None)
+    hf = build_hf_llama(sh, W)
+    _, pkv = hf_prefill(hf, ids[:-1])
+    tree = make_tree("total:17", sh.vocab, 3, 3, 9, int(ids[-1]))
+    res = O.verify_forward(m, kc, vc, 20, tree.ids, tree.parent, None)
+    depth, anc = O.build_mask(tree.parent)
+    ref = hf_tree_logits(hf, pkv, 20, tree.ids, depth, anc, sh.vocab)
+    assert np.abs(ref - res["logits"]).max() < 1e-5
+
+
+# ---------------------------------------------------------------- brute force
+
+@pytest.mark.parametrize("spec,seed", [("candidates:10", 1), ("candidates:10", 2), ("total:25", 3)])
+def test_tree_nodes_equal_causal_paths(tiny, spec, seed):
+    sh, W, m, kc, vc, L, root = tiny
+    tree = make_tree(spec, sh.vocab, 3, 4, seed, root)
+    res = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, "f32")
+    for i in range(tree.T):
+        seq = O.path_tokens(tree.parent, tree.ids, i)
+        ref = O.causal_logits(m, kc, vc, L, seq, "f32")[-1]
+        assert np.abs(ref - res["logits"][i]).max() < 1e-9
+
+
+def test_tree_nodes_equal_causal_paths_bf16():
+    w = workload("small", n_layers=1, cache_len=40)
+    sh, W, m, kc, vc, L, root = _setup(w, store="bf16")
+    tree = make_tree("total:20", sh.vocab, 3, 4, 5, root)
+    res = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, "bf16")
+    for i in range(tree.T):
+        seq = O.path_tokens(tree.parent, tree.ids, i)
+        ref = O.causal_logits(m, kc, vc, L, seq, "bf16")[-1]
+        assert np.abs(ref - res["logits"][i]).max() < 1e-9
+
+
+def test_chain_tree_is_multitoken_decode(tiny):
+    sh, W, m, kc, vc, L, root = tiny
+    seq = [root] + list(tokens(5, sh.vocab, 99).numpy()) + [sh.vocab + j for j in range(3)]
+    parent = [-1] + list(range(len(seq) - 1))
+    res = O.verify_forward(m, kc, vc, L, seq, parent, "f32")
+    ref = O.causal_logits(m, kc, vc, L, seq, "f32")
+    assert np.abs(ref - res["logits"]).max() < 1e-9
+    # and the tree keys are the keys a causal decode would cache
+    kc2, vc2 = O.copy_cache(kc, vc)
+    for j, t in enumerate(seq):
+        O.decode_token(m, kc2, vc2, L + j, t, "f32")
+    for l in range(sh.n_layers):
+        assert np.abs(kc2[l][:, L:L + len(seq)] - res["tree_k"][l]).max() < 1e-12
+        assert np.abs(vc2[l][:, L:L + len(seq)] - res["tree_v"][l]).max() < 1e-12
+
+
+def test_single_node_tree_is_vanilla_decode(tiny):
+    sh, W, m, kc, vc, L, root = tiny
+    res = O.verify_forward(m, kc, vc, L, [root], [-1], "f32")
+    kc2, vc2 = O.copy_cache(kc, vc)
+    ref = O.decode_token(m, kc2, vc2, L, root, "f32")
+    assert np.abs(ref - res["logits"][0]).max() < 1e-12
+    path, n_path, nxt = O.accept([-1], [root], O.argmax_first(res["logits"]), sh.vocab)
+    assert n_path == 1 and list(path) == [0] and nxt == int(np.argmax(ref))
+
+
+# ---------------------------------------------------------------- invariants
+
+def test_non_ancestors_do_not_matter(tiny):
+    sh, W, m, kc, vc, L, root = tiny
+    tree = make_tree("candidates:10", sh.vocab, 3, 4, 11, root)
+    full = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, "f32")["logits"]
+    # keep only the ancestor closure of one deep node
+    depth, anc = O.build_mask(tree.parent)
+    target = int(np.argmax(depth))
+    keep = [j for j in range(tree.T) if anc[target, j]]
+    remap = {old: new for new, old in enumerate(keep)}
+    sub_parent = [-1 if tree.parent[j] < 0 else remap[int(tree.parent[j])] for j in keep]
+    sub = O.verify_forward(m, kc, vc, L, tree.ids[keep], sub_parent, "f32")["logits"]
+    for new, old in enumerate(keep):
+        assert np.abs(sub[new] - full[old]).max() < 1e-12
+
+
+def test_relabel_permutes_rows(tiny):
+    sh, W, m, kc, vc, L, root = tiny
+    tree = make_tree("candidates:10", sh.vocab, 3, 4, 12, root)
+    res = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, "f32")["logits"]
+    # another topological order: depth-first
+    children = {i: [] for i in range(tree.T)}
+    for i in range(1, tree.T):
+        children[int(tree.parent[i])].append(i)
+    order, stack = [], [0]
+    while stack:
+        j = stack.pop()
+        order.append(j)
+        stack.extend(reversed(children[j]))
+    new_of = {old: new for new, old in enumerate(order)}
+    par2 = [-1] + [new_of[int(tree.parent[o])] for o in order[1:]]
+    res2 = O.verify_forward(m, kc, vc, L, tree.ids[order], par2, "f32")["logits"]
+    assert np.abs(res2 - res[order]).max() < 1e-12
+
+
+# ---------------------------------------------------------------- closed forms
+
+def test_rmsnorm_closed_form():
+    x = np.array([[3.0, -4.0], [1.0, 1.0]])
+    r = O.rms_scale(x, 0.0)
+    assert np.allclose(r, [1 / math.sqrt(12.5), 1.0])
+    c = 0.37
+    r = O.rms_scale(np.full((1, 8), c), 1e-6)
+    assert abs(r[0] - 1 / math.sqrt(c * c + 1e-6)) < 1e-15
+    a, r = O.normed_rows(np.array([[2.0, 0.0, -2.0, 0.0]]), np.array([1.0, 2.0, 3.0, 4.0]), 0.0, None)
+    assert np.allclose(r[:, None] * a, [[math.sqrt(2), 0, -3 * math.sqrt(2), 0]])
+
+
+def test_rope_is_a_rotation_by_pos_times_frequency():
+    d, base = 8, 100.0
+    pos = np.array([0, 1, 5, 1234])
+    cos, sin = O.rope_tables(pos, d, base)
+    x = np.random.default_rng(0).standard_normal((4, 1, d))
+    y = O.apply_rope(x, cos, sin)
+    for n in range(4):
+        for i in range(d // 2):
+            th = pos[n] * base ** (-2 * i / d)
+            R = np.array([[math.cos(th), -math.sin(th)], [math.sin(th), math.cos(th)]])
+            ref = R @ np.array([x[n, 0, i], x[n, 0, i + d // 2]])
+            assert np.allclose([y[n, 0, i], y[n, 0, i + d // 2]], ref, atol=1e-12)
+    assert np.allclose(y[0], x[0])                          # position 0: identity
+    # relative property: <rope(q,m), rope(k,n)> depends on m - n only
+    q = np.random.default_rng(1).standard_normal((1, 1, d))
+    k = np.random.default_rng(2).standard_normal((1, 1, d))
+
+    def dot(m, n):
+        cm, sm = O.rope_tables(np.array([m]), d, base)
+        cn, sn = O.rope_tables(np.array([n]), d, base)
+        return float(np.sum(O.apply_rope(q, cm, sm) * O.apply_rope(k, cn, sn)))
+    assert abs(dot(10, 3) - dot(107, 100)) < 1e-10
+
+
+def test_silu_softmax_library():
+    from scipy.special import expit, softmax
+    x = np.linspace(-30, 30, 101)
+    assert np.allclose(O.silu(x), x * expit(x), rtol=1e-14, atol=1e-300)
+    s = np.random.default_rng(3).standard_normal((4, 9)) * 5
+    s[1, 3] = -np.inf
+    assert np.allclose(O.softmax_rows(s), softmax(s, axis=-1), rtol=1e-14)
+
+
+def test_bf16_rounding_matches_torch_and_ties_to_even():
+    rng = np.random.default_rng(4)
+    x = np.concatenate([rng.standard_normal(10000) * 10.0 ** rng.integers(-20, 20, 10000),
+                        [0.0, -0.0, 1e-40, 3.0e38, -3.4e38]])
+    ref = torch.tensor(x.astype(np.float32)).to(torch.bfloat16).double().numpy()
+    assert np.array_equal(O.round_store(x, "bf16"), ref)
+    # 1 + 2^-8 is halfway between 1 and 1 + 2^-7: ties to even (1.0)
+    assert O.round_store(np.array([1 + 2 ** -8]), "bf16")[0] == 1.0
+    assert O.round_store(np.array([1 + 3 * 2 ** -8]), "bf16")[0] == 1 + 2 ** -6
+    assert O.round_store(np.array([0.1]), "f32")[0] == float(np.float32(0.1))
+
+
+def test_masks():
+    parent = [-1, 0, 0, 1, 3, 2, 4]
+    depth, anc = O.build_mask(parent)
+    assert list(depth) == [0, 1, 1, 2, 3, 2, 4]
+    assert anc[6].tolist() == [True, True, False, True, True, False, True]
+    packed = O.pack_mask(anc)
+    assert int(packed[6, 0]) == (1 << 0) | (1 << 1) | (1 << 3) | (1 << 4) | (1 << 6)
+    chain = [-1] + list(range(99))
+    d2, a2 = O.build_mask(chain)
+    assert list(d2) == list(range(100))
+    p2 = O.pack_mask(a2)
+    assert int(p2[99, 0]) == (1 << 64) - 1 and int(p2[99, 1]) == (1 << 36) - 1
+    for bad in ([0], [-1, 1], [-1, 0, 3], [-1, -1]):
+        with pytest.raises(ValueError):
+            O.build_mask(bad)
+
+
+# ---------------------------------------------------------------- acceptance
+
+def _brute_accept(parent, ids, pred, vocab):
+    """Enumerate every root path; keep the longest whose every candidate
+    matches the greedy token of its predecessor (ties: smallest end node)."""
+    best = (0, [0])
+    for node in range(len(parent)):
+        path, j = [], node
+        while j != -1:
+            path.append(j)
+            j = parent[j]
+        path = path[::-1]
+        good = all(0 <= ids[path[k]] < vocab and ids[path[k]] == pred[path[k - 1]]
+                   for k in range(1, len(path)))
+        if good and len(path) > len(best[1]):
+            best = (node, path)
+    return best[1], pred[best[0]]
+
+
+def test_accept_brute_force():
+    V = 7
+    rng = np.random.default_rng(5)
+    for trial in range(600):
+        spec = ["candidates:6", "total:20", "candidates:12"][trial % 3]
+        tree = make_tree(spec, V, 2, 4, 1000 + trial, int(rng.integers(V)))
+        ids = tree.ids.copy()
+        if trial % 4 == 3:
+            # duplicate sibling tokens (allowed by the interface): equally deep
+            # verified nodes can then exist and the smallest index must win
+            ids[1:tree.n_candidates] = rng.integers(2, size=tree.n_candidates - 1)
+        # predictions may even name prompt ids: prompt nodes still never verify
+        pred = rng.integers(V + 2, size=tree.T)
+        if trial % 2:
+            node = int(rng.integers(tree.n_candidates))
+            p = O.path_tokens(tree.parent, list(range(tree.T)), node)
+            for a, b in zip(p[:-1], p[1:]):
+                pred[a] = ids[b]
+        if trial % 5 == 0:
+            pred[:] = ids[np.maximum(np.arange(tree.T), 1)]   # prompt ids predicted too
+        path, n_path, nxt = O.accept(tree.parent, ids, pred, V)
+        bpath, bnxt = _brute_accept(list(tree.parent), list(ids), list(pred), V)
+        assert list(path) == bpath and n_path == len(bpath) and nxt == bnxt
+
+
+def test_vanilla_tau_is_one_and_table1_accounting():
+    """Table 1: vanilla decoding has tau = 1.00 and throughput ~= tau / L_fp."""
+    g = json.load(open(os.path.join(GOLD, "table1.json")))
+    for row in g["rows"]:
+        assert abs(row["tau"] / row["L_fp"] - row["T"]) / row["T"] < 0.05, row
+        if row["method"] == "vanilla":
+            assert row["tau"] == 1.0
+    # the oracle's accounting reproduces tau = 1 for a root-only tree
+    _, n_path, _ = O.accept([-1], [3], [5], 10)
+    assert n_path == 1
+
+
+def test_prompt_table_share_matches_table1():
+    """P_tr (Table 1): 3 prompt embeddings of size hidden over the model's
+    parameters reproduces 4.50e-4 % (MobileLLaMA) and 1.82e-4 % (Vicuna-7B)."""
+    g = json.load(open(os.path.join(GOLD, "table1.json")))
+    share = {r["model"]: r["P_tr_pct"] for r in g["rows"] if "P_tr_pct" in r}
+    for name, key in (("1.4b", "MobileLLaMA"), ("7b", "Vicuna-7B")):
+        sh = workload(name).shape
+        pct = 100.0 * g["prompt_tokens"] * g["ept"] * sh.hidden / sh.total_params()
+        assert abs(pct - share[key]) / share[key] < 0.01, (name, pct)
+
+
+def test_proposition1_expected_accept_length():
+    """Proposition 1: with independent acceptance probability p_d at depth d,
+    the expected number of accepted candidates is the sum over candidates v of
+    the product of p along the root path of v."""
+    V = 4
+    tree = make_tree("candidates:9", V, 3, 3, 21, 0)
+    depth, anc = O.build_mask(tree.parent)
+    p = {1: 0.6, 2: 0.45, 3: 0.3}
+    rng = np.random.default_rng(6)
+    n = 20000
+    acc = 0
+    cand = range(1, tree.n_candidates)
+    # each node's children hold distinct tokens; the true next token after node
+    # u is child c's token with prob q(c) = p_depth(c) / n_children(u), else a
+    # token no child holds.
+    kids = {u: [c for c in cand if tree.parent[c] == u] for u in range(tree.n_candidates)}
+    q = {c: p[int(depth[c])] / len(kids[int(tree.parent[c])]) for c in cand}
+    expected = sum(np.prod([q[u] for u in range(1, tree.n_candidates) if anc[v, u]]) for v in cand)
+    for _ in range(n):
+        pred = np.full(tree.T, V + 100)  # "no child" token (never a candidate id)
+        for u in range(tree.n_candidates):
+            if kids[u]:
+                r = rng.random()
+                c0 = 0.0
+                for c in kids[u]:
+                    c0 += q[c]
+                    if r < c0:
+                        pred[u] = tree.ids[c]
+                        break
+        _, n_path, _ = O.accept(tree.parent, tree.ids, pred, V)
+        acc += n_path - 1
+    mc = acc / n
+    se = math.sqrt(expected * 4 / n) + 1e-3
+    assert abs(mc - expected) < 4 * se, (mc, expected)
+
+
+# ---------------------------------------------------------------- whole loop
+
+def test_multistep_ppd_is_lossless(tiny):
+    """Section 5.1 / Figure 5: with exact matching the generated text is that of
+    the original model.  Trees carry the true greedy continuation along a random
+    path (random depth) and random tokens elsewhere."""
+    sh, W, m, kc0, vc0, L0, root = tiny
+    kc, vc = O.copy_cache(kc0, vc0)
+    steps, L, tok = 6, L0, root
+    n_total = 0
+    emitted = []
+    rng = np.random.default_rng(7)
+    for s in range(steps):
+        tree = make_tree("candidates:10", sh.vocab, 3, 4, 500 + s, tok)
+        truth = O.greedy_decode(m, kc, vc, L, tok, 6, "f32")
+        node = int(rng.integers(tree.n_candidates))
+        path_nodes = O.path_tokens(tree.parent, list(range(tree.T)), node)
+        ids = tree.ids.copy()
+        for k, nd in enumerate(path_nodes[1:]):
+            ids[nd] = truth[k]
+        res = O.verify_forward(m, kc, vc, L, ids, tree.parent, "f32")
+        pred = O.argmax_first(res["logits"])
+        path, n_path, nxt = O.accept(tree.parent, ids, pred, sh.vocab)
+        assert n_path >= len(path_nodes)           # at least the planted path
+        L = O.kv_compact(kc, vc, res["tree_k"], res["tree_v"], L, path)
+        emitted += [int(ids[j]) for j in path[1:]] + [nxt]
+        tok = nxt
+        n_total += n_path
+    ref = O.greedy_decode(m, kc0, vc0, L0, root, len(emitted), "f32")
+    assert emitted == ref
+    assert L == L0 + n_total
+
+
+def test_kv_compact_commits_path_rows(tiny):
+    sh, W, m, kc0, vc0, L, root = tiny
+    tree = make_tree("candidates:10", sh.vocab, 3, 4, 31, root)
+    res = O.verify_forward(m, kc0, vc0, L, tree.ids, tree.parent, "f32")
+    depth, _ = O.build_mask(tree.parent)
+    node = int(np.argmax(depth[:tree.n_candidates]))
+    path = O.path_tokens(tree.parent, list(range(tree.T)), node)
+    kc, vc = O.copy_cache(kc0, vc0)
+    L2 = O.kv_compact(kc, vc, res["tree_k"], res["tree_v"], L, path)
+    kr, vr = O.copy_cache(kc0, vc0)
+    for j, nd in enumerate(path):
+        O.decode_token(m, kr, vr, L + j, int(tree.ids[nd]), "f32")
+    assert L2 == L + len(path)
+    for l in range(sh.n_layers):
+        assert np.abs(kc[l][:, :L2] - kr[l][:, :L2]).max() < 1e-12
+        assert np.abs(vc[l][:, :L2] - vr[l][:, :L2]).max() < 1e-12
