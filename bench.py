@@ -1,0 +1,251 @@
+"""Benchmark of the PPD tree-verification step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload 7b] [--T 64] [--graph]
+
+A step is one pass of the whole hot path on one synthetic batch:
+ppd_verify_step (forward over the T tree nodes, fp32 logits, greedy tokens)
+-> ppd_accept -> ppd_kv_compact, enqueued on one stream.  The cache length L is
+the same every step (the compaction writes past L, the next step overwrites).
+Inputs are resident in HBM before timing starts.  Prints one JSON line.
+
+The default workload is the Vicuna-7B-shaped decoder (32 layers, hidden 4096,
+32 heads x 128, ffn 11008, vocab 32000, bf16, random weights) with a
+2048-token KV prefix and a 64-node candidate tree (3 prompt tokens per leaf).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def step_bytes(sh, L, T, n_path):
+    """Algorithmic HBM bytes of one step: every weight matrix, norm gain and
+    the LM head once, the KV prefix once, the tree K/V write, the T embedding
+    rows, the fp32 logits write and the compaction's read + write."""
+    H, F, nh, nkv, d, V, nl = (sh.hidden, sh.ffn, sh.n_heads, sh.n_kv_heads, sh.head_dim,
+                               sh.vocab, sh.n_layers)
+    es = 2 if sh.dtype == "bf16" else 4
+    w = nl * (sh.qkv_rows * H + H * nh * d + 2 * F * H + H * F + 2 * H) + V * H + H
+    kv_prefix = nl * nkv * L * d * 2
+    tree_kv = nl * nkv * T * d * 2
+    emb = T * H
+    return (w + kv_prefix + tree_kv + emb) * es + T * V * 4 + 2 * n_path * nl * nkv * d * 2 * es
+
+
+def step_flops(sh, L, T):
+    per_tok = 2 * (sh.n_layers * (sh.qkv_rows * sh.hidden + sh.hidden * sh.n_heads * sh.head_dim
+                                  + 3 * sh.ffn * sh.hidden) + sh.vocab * sh.hidden)
+    attn = 4 * T * (L + T) * sh.n_heads * sh.head_dim * sh.n_layers
+    return T * per_tok + attn
+
+
+def gate_up_bytes(sh, T):
+    """Algorithmic bytes of one gate/up launch: the [2F, H] weight, the
+    [T, H] normalised operand and the [T, F] SwiGLU output."""
+    return (2 * sh.ffn * sh.hidden + T * sh.hidden + T * sh.ffn) * 2
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="7b")
+    ap.add_argument("--T", type=int, default=None)
+    ap.add_argument("--L", type=int, default=None)
+    ap.add_argument("--graph", action="store_true", help="replay the step as a HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=4,
+                    help="decoder layers in the CPU oracle's timed sample")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the step is a single-GPU kernel path); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2405_18628_amd as ppd
+    from synth import workload
+    from synth.model import empty_kv, fill_kv_normal, make_weights
+    from synth.trees import make_tree
+
+    wl = workload(args.workload)
+    sh = wl.shape
+    L = wl.cache_len if args.L is None else args.L
+    spec = wl.tree if args.T is None else f"total:{args.T}"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t0 = time.time()
+    W = make_weights(sh, wl.seeds["weights"], device=dev)
+    cap = ((L + 128 + 63) // 64) * 64
+    k, v = empty_kv(sh, cap, device=dev)
+    fill_kv_normal(k, v, L, wl.seeds["kv"])
+    torch.cuda.synchronize()
+    print(f"[bench] {wl.name}: inputs ready in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    tree = make_tree(spec, sh.vocab, sh.n_prompt, wl.max_depth, wl.seeds["tree"], 1, wl.max_fanout)
+    T = tree.T
+    depth, mask = ppd.ppd_build_tree_mask(tree.parent)
+    todev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    ids_d, par_d, dep_d, mask_d = (todev(tree.ids), todev(tree.parent), todev(depth),
+                                   todev(mask.view(np.int64)))
+    model = ppd.Model(sh, W)
+    kv = ppd.KVCache(k, v)
+    ws = torch.empty(ppd.ppd_workspace_bytes(model, T, cap), dtype=torch.uint8, device=dev)
+    ppd.ppd_workspace_init(ws)
+    logits = torch.empty((T, sh.vocab), device=dev)
+    pred = torch.empty(T, dtype=torch.int32, device=dev)
+    path = torch.empty(T, dtype=torch.int32, device=dev)
+    n_path = torch.empty(1, dtype=torch.int32, device=dev)
+    nxt = torch.empty(1, dtype=torch.int32, device=dev)
+
+    def step():
+        ppd.ppd_verify_step(model, kv, L, T, ids_d, dep_d, mask_d, ws, logits, pred)
+        ppd.ppd_accept(T, par_d, ids_d, pred, sh.vocab, path, n_path, nxt, ws)
+        ppd.ppd_kv_compact(model, kv, L, path, n_path)
+
+    run = step
+    if args.graph:
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(2):
+                step()
+        torch.cuda.current_stream().wait_stream(s)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        run = g.replay
+
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    n_acc = int(n_path.item())
+    status = ppd.ppd_device_status(ws)
+
+    # forward-only latency (verify without accept / compact)
+    e0.record()
+    for _ in range(args.steps):
+        ppd.ppd_verify_step(model, kv, L, T, ids_d, dep_d, mask_d, ws, logits, pred)
+    e1.record()
+    torch.cuda.synchronize()
+    fwd_ms = e0.elapsed_time(e1) / args.steps
+
+    # per-kernel durations with HIP events on the step's stream (eager steps)
+    kernels = {}
+    for kind in ("qkv", "attention", "o_proj", "gate_up", "down", "lm_head"):
+        n = 1 if kind == "lm_head" else sh.n_layers
+        st = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        sp = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        keep = ppd.ppd_set_kernel_timer(kind, st, sp)
+        tot, cnt = 0.0, 0
+        for _ in range(args.steps):
+            step()
+            torch.cuda.synchronize()
+            tot += sum(a.elapsed_time(b) for a, b in zip(st, sp))
+            cnt += n
+        ppd.ppd_set_kernel_timer(kind)
+        del keep
+        kernels[kind] = tot / cnt * 1e3  # us per launch
+
+    alg = step_bytes(sh, L, T, n_acc)
+    flops = step_flops(sh, L, T)
+    gu_us = kernels["gate_up"]
+    gu_bytes = gate_up_bytes(sh, T)
+    achieved = gu_bytes / (gu_us * 1e-6) / 1e9
+    out = {
+        "metric": "verify-step latency (us) + achieved HBM GB/s, 7B shape, 64-token tree, 2k ctx",
+        "value": round(ms * 1e3, 1),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": sh.dtype,
+        "data": "synthetic (seeded random weights N(0,0.02), KV prefix N(0,1), random tree)",
+        "config": {"workload": f"{sh.name} verify step", "layers": sh.n_layers,
+                   "hidden": sh.hidden, "heads": sh.n_heads, "ffn": sh.ffn, "vocab": sh.vocab,
+                   "tree_tokens": T, "cache_len": L, "graph": bool(args.graph)},
+        "step_hbm_gbs": round(alg / (ms * 1e-3) / 1e9, 1),
+        "step_roofline_frac": round(alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "step_alg_bytes": alg,
+        "step_alg_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+        "forward_us": round(fwd_ms * 1e3, 1),
+        "tree_tokens_per_s": round(T / (ms * 1e-3), 1),
+        "emitted_tokens_per_s": round(n_acc / (ms * 1e-3), 1),
+        "kernel_us": {k2: round(v2, 2) for k2, v2 in kernels.items()},
+        "device_status": status,
+        "roofline": {"bound": "hbm", "kernel": "gate_up GEMM + SwiGLU",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "alg_bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_us, 2)},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(sh, W, k, v, L, tree, args.cpu_layers)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(sh, W, k, v, L, tree, n_sample):
+    """The oracle (float64 numpy, BLAS threads = host cores) on a bounded
+    sample of the same step: forward + acceptance over the same tree with
+    n_sample/2 and n_sample of the model's decoder layers (plus embedding and
+    LM head); the per-layer cost is scaled to the full layer count.  Weights
+    and caches are copied from the device and converted to float64 before
+    timing.  Returns the estimated full-step latency in us."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=os.cpu_count())
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    half = max(1, n_sample // 2)
+    times = {}
+    for n in (half, n_sample):
+        Wn = {key: W[key] for key in ("tok_emb", "prompt_emb", "final_norm", "lm_head")}
+        Wn["layers"] = W["layers"][:n]
+        m = O.Model(sh.with_layers(n), Wn, keep_layers=True)
+        for l in range(n):
+            m.layer(l)
+        _ = m.lm_head
+        kc = [O.to_f64(k[l, :, :L, :]) for l in range(n)]
+        vc = [O.to_f64(v[l, :, :, :L]).transpose(0, 2, 1) for l in range(n)]
+        t0 = time.perf_counter()
+        res = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, sh.dtype)
+        pred = O.argmax_first(res["logits"])
+        O.accept(tree.parent, tree.ids, pred, sh.vocab)
+        times[n] = time.perf_counter() - t0
+        del m, kc, vc, res
+    per_layer = (times[n_sample] - times[half]) / (n_sample - half)
+    fixed = max(0.0, times[half] - half * per_layer)
+    est = fixed + sh.n_layers * per_layer
+    return {"value": round(est * 1e6, 1), "unit": "us", "cores": int(cores), "kind": "oracle",
+            "sample": (f"oracle forward+accept over the same {tree.T}-node tree and {L}-token "
+                       f"cache with {half} and {n_sample} of the {sh.n_layers} decoder layers "
+                       f"(+ embedding, LM head): {times[half]:.2f} s and {times[n_sample]:.2f} s; "
+                       f"per-layer cost scaled to {sh.n_layers} layers")}
+
+
+if __name__ == "__main__":
+    main()

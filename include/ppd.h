@@ -1,0 +1,204 @@
+/*
+ * ppd.h -- C ABI of the Parallel Prompt Decoding (PPD) tree-verification step
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * One decode step of PPD (Section 3 of the paper: candidate generation,
+ * verification and acceptance merged into a single forward pass) is, on the
+ * verification side:
+ *
+ *   ppd_build_tree_mask  host: depths and ancestor bitmask of the candidate
+ *                        tree with its prompt-token chains (Section 4.1)
+ *   ppd_verify_step      device: one forward pass of the frozen decoder over
+ *                        all T tree nodes against the KV cache under the tree
+ *                        mask; per-node logits and greedy tokens
+ *   ppd_accept           device: exact-matching verification, longest
+ *                        accepted root path, bonus token (Section 3)
+ *   ppd_kv_compact       device: commit the accepted nodes' keys/values to
+ *                        the single shared KV cache (Section 5.4)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Tree.  Nodes 0..T-1 in topological order: parent[0] = -1 (node 0 is the
+ *   root: the last verified token, whose keys/values are not cached yet) and
+ *   0 <= parent[i] < i.  ids[i] < vocab is a vocabulary token; ids[i] >= vocab
+ *   is prompt token ids[i] - vocab (< n_prompt).  Node i sits at position
+ *   L + depth[i] (Section 3.1: a prompt token takes the position of the token
+ *   it predicts) and attends to cache positions [0, L), to its tree ancestors
+ *   and to itself (Section 4.1).  1 <= T <= PPD_T_MAX.
+ * Mask.  uint64 mask[T][PPD_MASK_WORDS]; bit (j % 64) of word j / 64 of row i
+ *   is set iff node j is node i or one of its ancestors.
+ * Memory.  Every pointer marked "device" is HIP device memory owned by the
+ *   caller and must stay valid until the enqueued work completes.  The
+ *   library allocates nothing and keeps no state besides the thread-local
+ *   error string and the optional thread-local kernel timer.  Weights, caches and activations of PPD_BF16 models are
+ *   bfloat16 (raw 16-bit words); PPD_F32 models use float32 throughout.
+ * Streams.  Device calls enqueue on `stream` (a hipStream_t; NULL = default
+ *   stream) and return without waiting.  verify -> accept -> compact must be
+ *   enqueued in that order on one stream; no host synchronisation is needed
+ *   between them.  Calls never allocate, synchronise or memset, so a caller may
+ *   capture them into a HIP graph.
+ * Errors.  Host-checkable conditions are rejected before anything is
+ *   enqueued, with a non-zero ppd_status and a message from ppd_last_error().
+ *   Invalid data that only the device sees (a token id out of range, a parent
+ *   index out of range in ppd_accept, a NaN logit) sets a bit in the
+ *   workspace's status word (read with ppd_device_status); kernels clamp the
+ *   offending index so that no access leaves its buffer.
+ */
+#ifndef PPD_H
+#define PPD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PPD_OK = 0,
+  PPD_EINVAL = 1,       /* null pointer, bad size or model description     */
+  PPD_ETREE = 2,        /* parent array is not a topological tree          */
+  PPD_ECAPACITY = 3,    /* L + T exceeds the cache capacity                */
+  PPD_EDEVICE = 4,      /* a HIP launch or runtime call failed             */
+  PPD_EUNSUPPORTED = 5, /* shape outside what the kernels implement        */
+  PPD_EWORKSPACE = 6    /* workspace missing or smaller than required      */
+} ppd_status;
+
+typedef enum { PPD_F32 = 0, PPD_BF16 = 1 } ppd_dtype;
+
+#define PPD_T_MAX 128
+#define PPD_MASK_WORDS 2
+
+/* device status bits (ppd_device_status) */
+#define PPD_DEV_BAD_TOKEN 1u   /* an id >= vocab + n_prompt was clamped      */
+#define PPD_DEV_BAD_PARENT 2u  /* ppd_accept saw parent[i] outside [0, i)    */
+#define PPD_DEV_NAN_LOGIT 4u   /* a NaN logit was seen by the greedy argmax  */
+
+/*
+ * Llama-style decoder (the paper's MobileLLaMA / Vicuna family): pre-RMSNorm
+ * (eps rms_eps), rotary embedding with rotate-half pairing (dimension i pairs
+ * with i + head_dim/2, frequency rope_base^(-2i/head_dim)), multi-head
+ * attention with n_kv_heads dividing n_heads, SwiGLU MLP, untied LM head.
+ * All weight pointers are device pointers; per-layer tensors are given as
+ * HOST arrays of n_layers device pointers.  Row-major layouts:
+ *   tok_emb     [vocab][hidden]
+ *   prompt_emb  [n_prompt][hidden]       trained prompt-token embeddings
+ *   attn_norm   [hidden]     per layer
+ *   w_qkv       [(n_heads + 2 n_kv_heads) head_dim][hidden]  rows q | k | v
+ *   w_o         [hidden][n_heads head_dim]
+ *   mlp_norm    [hidden]
+ *   w_gate_up   [2 ffn][hidden]           rows gate | up
+ *   w_down      [hidden][ffn]
+ *   final_norm  [hidden]
+ *   lm_head     [vocab][hidden]
+ */
+typedef struct {
+  int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab, n_prompt;
+  float rms_eps, rope_base;
+  int32_t dtype; /* ppd_dtype */
+  const void *tok_emb, *prompt_emb;
+  const void *const *attn_norm, *const *w_qkv, *const *w_o;
+  const void *const *mlp_norm, *const *w_gate_up, *const *w_down;
+  const void *final_norm, *lm_head;
+} ppd_model;
+
+/*
+ * The single KV cache of the accepted sequence (device memory, caller-owned).
+ *   k  [n_layers][n_kv_heads][capacity][head_dim]   keys after RoPE
+ *   v  [n_layers][n_kv_heads][head_dim][capacity]   values, position-minor
+ * Positions [0, L) hold the accepted prefix.  ppd_verify_step writes the keys
+ * and values of tree node i to position L + i (scratch beyond the prefix);
+ * ppd_kv_compact moves the accepted ones down to L, L+1, ...
+ * len_dev (optional, device int32) receives L + n_path from ppd_kv_compact.
+ */
+typedef struct {
+  void *k, *v;
+  int32_t capacity;
+  int32_t *len_dev;
+} ppd_kv;
+
+/* Bytes of device workspace ppd_verify_step needs for trees of up to t_max
+ * nodes and caches of up to max_len positions.  0 on invalid input. */
+size_t ppd_workspace_bytes(const ppd_model *model, int32_t t_max, int32_t max_len);
+
+/* Zero the workspace's counters and status word (enqueued on `stream`).  Call
+ * once after allocating a workspace; later calls keep it consistent. */
+ppd_status ppd_workspace_init(void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Host-side tree preparation (Section 4.1).  parent: host int32[T].
+ * depth_out: host int32[T], root depth 0.  mask_out: host uint64[T][2] as
+ * described above.  Returns PPD_ETREE if parent is not a topological tree,
+ * PPD_EINVAL for T outside [1, PPD_T_MAX] or null pointers.
+ */
+ppd_status ppd_build_tree_mask(int32_t T, const int32_t *parent, int32_t *depth_out,
+                               uint64_t *mask_out);
+
+/*
+ * One forward pass over the T tree nodes (Sections 3 and 4.1).
+ *   L       tokens already in the cache (host value); needs L + T <= capacity
+ *   ids     device int32[T]
+ *   depth   device int32[T] (from ppd_build_tree_mask)
+ *   mask    device uint64[T][2]
+ *   ws      device workspace of ws_bytes >= ppd_workspace_bytes(model, T, L)
+ *   logits  device float32[T][vocab], or NULL to skip storing logits
+ *   pred    device int32[T]: greedy token of every node (smallest index among
+ *           equal maxima)
+ * Also writes the nodes' keys/values to cache positions L .. L+T-1.
+ */
+ppd_status ppd_verify_step(const ppd_model *model, const ppd_kv *kv, int32_t L, int32_t T,
+                           const int32_t *ids, const int32_t *depth, const uint64_t *mask,
+                           void *ws, size_t ws_bytes, float *logits, int32_t *pred,
+                           void *stream);
+
+/*
+ * Exact-matching verification and acceptance (Section 3).  Node i > 0 is
+ * verified iff its parent is verified (the root always is), ids[i] < vocab
+ * and ids[i] == pred[parent[i]]; prompt nodes never are.  The accepted node
+ * is the deepest verified one (ties: smallest index).  Outputs (device):
+ *   path      int32[T]: accepted node indices root first (path[0] = 0)
+ *   n_path    int32: depth of the accepted node + 1 = tokens emitted this
+ *             step (accepted candidates plus the bonus token)
+ *   next_tok  int32: pred[accepted node], the bonus token and next root
+ * parent, ids, pred: device int32[T].  ws: the workspace (status word).
+ */
+ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids,
+                      const int32_t *pred, int32_t vocab, int32_t *path, int32_t *n_path,
+                      int32_t *next_tok, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Commit accepted keys/values (Section 5.4: one cache shared by guessing and
+ * verification; prompt-token entries are never committed):
+ * cache[L + k] <- cache[L + path[k]] for k < *n_path, every layer and kv head.
+ * path, n_path: device (as written by ppd_accept).  L: host value used by the
+ * matching ppd_verify_step.  Requires L + max_T <= capacity where max_T bounds
+ * *n_path; *n_path is clamped to [0, capacity - L] on the device.
+ */
+ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
+                          const int32_t *path, const int32_t *n_path, void *stream);
+
+/*
+ * Profiling aid, not needed for correctness.  While set, every
+ * ppd_verify_step issued from this thread records start_events[i] before and
+ * stop_events[i] after the i-th launch of kernel `kind` in the step (i <
+ * n_events), on the step's stream, so a caller can time one kernel of the
+ * step with HIP events.  kind: 0 QKV GEMM, 1 tree attention, 2 output
+ * projection, 3 gate/up GEMM, 4 down projection, 5 LM head.  The arrays are
+ * host arrays of hipEvent_t and must stay valid while set; n_events = 0
+ * disables.  Thread-local setting.
+ */
+ppd_status ppd_set_kernel_timer(int32_t kind, void *const *start_events, void *const *stop_events,
+                                int32_t n_events);
+
+/* Synchronously read (and optionally clear) the workspace status word. */
+ppd_status ppd_device_status(void *ws, size_t ws_bytes, uint32_t *status_out, int32_t clear,
+                             void *stream);
+
+/* Message for the last non-OK status returned on this thread. */
+const char *ppd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PPD_H */

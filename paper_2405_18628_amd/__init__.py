@@ -1,0 +1,246 @@
+"""Python binding of libppd, the MI355X (gfx950) PPD tree-verification step.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of libppd.so.  Functions carry the names of the C ABI (include/ppd.h);
+tensors are torch tensors used as device memory, streams are torch streams.
+Importing works without a GPU (the host-side tree builder and the argument
+checks run anywhere); device calls need the built library and a GPU, and
+fail loudly otherwise -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libppd.so")
+
+PPD_OK, PPD_EINVAL, PPD_ETREE, PPD_ECAPACITY, PPD_EDEVICE, PPD_EUNSUPPORTED, PPD_EWORKSPACE = range(7)
+PPD_F32, PPD_BF16 = 0, 1
+PPD_T_MAX = 128
+PPD_MASK_WORDS = 2
+PPD_DEV_BAD_TOKEN, PPD_DEV_BAD_PARENT, PPD_DEV_NAN_LOGIT = 1, 2, 4
+
+_STATUS_NAMES = {0: "PPD_OK", 1: "PPD_EINVAL", 2: "PPD_ETREE", 3: "PPD_ECAPACITY",
+                 4: "PPD_EDEVICE", 5: "PPD_EUNSUPPORTED", 6: "PPD_EWORKSPACE"}
+
+
+class PPDError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class ppd_model(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("hidden", C.c_int32), ("n_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn", C.c_int32),
+                ("vocab", C.c_int32), ("n_prompt", C.c_int32), ("rms_eps", C.c_float),
+                ("rope_base", C.c_float), ("dtype", C.c_int32),
+                ("tok_emb", C.c_void_p), ("prompt_emb", C.c_void_p),
+                ("attn_norm", C.POINTER(C.c_void_p)), ("w_qkv", C.POINTER(C.c_void_p)),
+                ("w_o", C.POINTER(C.c_void_p)), ("mlp_norm", C.POINTER(C.c_void_p)),
+                ("w_gate_up", C.POINTER(C.c_void_p)), ("w_down", C.POINTER(C.c_void_p)),
+                ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
+
+
+class ppd_kv(C.Structure):
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("capacity", C.c_int32),
+                ("len_dev", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """The loaded libppd.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run paper_2405_18628_amd.build.build()")
+        L = C.CDLL(LIB_PATH)
+        vp, i32, sz = C.c_void_p, C.c_int32, C.c_size_t
+        P = C.POINTER
+        L.ppd_workspace_bytes.argtypes = [P(ppd_model), i32, i32]
+        L.ppd_workspace_bytes.restype = sz
+        L.ppd_workspace_init.argtypes = [vp, sz, vp]
+        L.ppd_build_tree_mask.argtypes = [i32, vp, vp, vp]
+        L.ppd_verify_step.argtypes = [P(ppd_model), P(ppd_kv), i32, i32, vp, vp, vp, vp, sz, vp,
+                                      vp, vp]
+        L.ppd_accept.argtypes = [i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
+        L.ppd_kv_compact.argtypes = [P(ppd_model), P(ppd_kv), i32, vp, vp, vp]
+        L.ppd_device_status.argtypes = [vp, sz, P(C.c_uint32), i32, vp]
+        L.ppd_set_kernel_timer.argtypes = [i32, vp, vp, i32]
+        L.ppd_last_error.restype = C.c_char_p
+        for f in ("ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
+                  "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer"):
+            getattr(L, f).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def ppd_last_error() -> str:
+    return lib().ppd_last_error().decode()
+
+
+def _check(status: int):
+    if status != PPD_OK:
+        raise PPDError(status, ppd_last_error())
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _dev(t, dtype=None, name="tensor"):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+# ---------------------------------------------------------------------------
+
+
+class Model:
+    """A ppd_model description over device tensors (kept alive by this object).
+
+    `w` follows the layout of include/ppd.h (see synth.model.make_weights)."""
+
+    def __init__(self, shape, w):
+        import torch
+        dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+        self.shape = shape
+        self.w = w
+        layers = w["layers"]
+        n = shape.n_layers
+
+        def arr(key):
+            for lay in layers:
+                _dev(lay[key], dt, key)
+            return (C.c_void_p * n)(*[_ptr(lay[key]) for lay in layers])
+
+        for key in ("tok_emb", "prompt_emb", "final_norm", "lm_head"):
+            _dev(w[key], dt, key)
+        self._arrays = {k: arr(k) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up",
+                                            "w_down")}
+        a = self._arrays
+        self.desc = ppd_model(
+            shape.n_layers, shape.hidden, shape.n_heads, shape.n_kv_heads, shape.head_dim,
+            shape.ffn, shape.vocab, shape.n_prompt, shape.rms_eps, shape.rope_base,
+            PPD_BF16 if shape.dtype == "bf16" else PPD_F32,
+            _ptr(w["tok_emb"]), _ptr(w["prompt_emb"]),
+            C.cast(a["attn_norm"], C.POINTER(C.c_void_p)), C.cast(a["w_qkv"], C.POINTER(C.c_void_p)),
+            C.cast(a["w_o"], C.POINTER(C.c_void_p)), C.cast(a["mlp_norm"], C.POINTER(C.c_void_p)),
+            C.cast(a["w_gate_up"], C.POINTER(C.c_void_p)), C.cast(a["w_down"], C.POINTER(C.c_void_p)),
+            _ptr(w["final_norm"]), _ptr(w["lm_head"]))
+
+
+class KVCache:
+    """K [layers][kv_heads][capacity][head_dim], V [layers][kv_heads][head_dim][capacity]."""
+
+    def __init__(self, k, v, len_dev=None):
+        self.k, self.v, self.len_dev = k, v, len_dev
+        self.capacity = int(k.shape[2])
+        self.desc = ppd_kv(_ptr(k), _ptr(v), self.capacity, _ptr(len_dev) or None)
+
+
+# ---------------------------------------------------------------------------
+# the C ABI, one Python function per entry point
+
+
+def ppd_workspace_bytes(model: Model, t_max: int, max_len: int) -> int:
+    n = lib().ppd_workspace_bytes(C.byref(model.desc), t_max, max_len)
+    if n == 0:
+        raise PPDError(PPD_EINVAL, ppd_last_error())
+    return int(n)
+
+
+def ppd_workspace_init(ws, stream=None):
+    _dev(ws, None, "ws")
+    _check(lib().ppd_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def ppd_build_tree_mask(parent: Sequence[int]):
+    """Host: (depth int32[T], mask uint64[T][2]) of a topological parent array."""
+    p = np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    T = int(p.shape[0])
+    depth = np.zeros(T, np.int32)
+    mask = np.zeros((T, PPD_MASK_WORDS), np.uint64)
+    _check(lib().ppd_build_tree_mask(T, p.ctypes.data, depth.ctypes.data, mask.ctypes.data))
+    return depth, mask
+
+
+def ppd_verify_step(model: Model, kv: KVCache, L: int, T: int, ids, depth, mask, ws, logits,
+                    pred, stream=None):
+    import torch
+    for t, n in ((ids, "ids"), (depth, "depth"), (pred, "pred")):
+        _dev(t, torch.int32, n)
+    _dev(mask, None, "mask")
+    _dev(ws, None, "ws")
+    _dev(logits, torch.float32, "logits")
+    _check(lib().ppd_verify_step(C.byref(model.desc), C.byref(kv.desc), int(L), int(T), _ptr(ids),
+                                 _ptr(depth), _ptr(mask), _ptr(ws),
+                                 ws.numel() * ws.element_size(), _ptr(logits) or None,
+                                 _ptr(pred), _stream(stream)))
+
+
+def ppd_accept(T: int, parent, ids, pred, vocab: int, path, n_path, next_tok, ws, stream=None):
+    import torch
+    for t, n in ((parent, "parent"), (ids, "ids"), (pred, "pred"), (path, "path"),
+                 (n_path, "n_path"), (next_tok, "next_tok")):
+        _dev(t, torch.int32, n)
+    _check(lib().ppd_accept(int(T), _ptr(parent), _ptr(ids), _ptr(pred), int(vocab), _ptr(path),
+                            _ptr(n_path), _ptr(next_tok), _ptr(ws), ws.numel() * ws.element_size(),
+                            _stream(stream)))
+
+
+def ppd_kv_compact(model: Model, kv: KVCache, L: int, path, n_path, stream=None):
+    _check(lib().ppd_kv_compact(C.byref(model.desc), C.byref(kv.desc), int(L), _ptr(path),
+                                _ptr(n_path), _stream(stream)))
+
+
+def ppd_device_status(ws, clear: bool = False, stream=None) -> int:
+    out = C.c_uint32(0)
+    _check(lib().ppd_device_status(_ptr(ws), ws.numel() * ws.element_size(), C.byref(out),
+                                   int(bool(clear)), _stream(stream)))
+    return int(out.value)
+
+
+KERNEL_KINDS = {"qkv": 0, "attention": 1, "o_proj": 2, "gate_up": 3, "down": 4, "lm_head": 5}
+
+
+def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):
+    """Record HIP events around every launch of one kernel kind in later
+    ppd_verify_step calls of this thread (torch.cuda.Event objects);
+    call with no events to disable.  Returns the ctypes arrays (keep them)."""
+    n = len(start_events)
+    if n == 0:
+        _check(lib().ppd_set_kernel_timer(0, None, None, 0))
+        return None
+    k = KERNEL_KINDS.get(kind, kind)
+    for e in list(start_events) + list(stop_events):
+        if not e.cuda_event:      # torch creates the HIP event on first record
+            e.record()
+    st = (C.c_void_p * n)(*[e.cuda_event for e in start_events])
+    sp = (C.c_void_p * n)(*[e.cuda_event for e in stop_events])
+    _check(lib().ppd_set_kernel_timer(int(k), st, sp, n))
+    return st, sp
+
+
+__all__ = ["ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
+           "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept", "ppd_kv_compact",
+           "ppd_device_status", "ppd_last_error"]

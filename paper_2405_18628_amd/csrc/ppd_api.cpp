@@ -1,0 +1,514 @@
+// Host side of libppd: argument validation, workspace layout and the launch
+// sequence of the verification step.  Everything is enqueued on the caller's
+// stream; nothing is allocated, copied or synchronised (except in
+// ppd_device_status, which is documented as synchronous).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "ppd_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+// optional per-thread kernel timer (ppd_set_kernel_timer)
+struct KernelTimer {
+  int kind = -1;
+  void *const *start = nullptr;
+  void *const *stop = nullptr;
+  int n = 0;
+  int next = 0;  // launches of `kind` seen in the current step
+};
+thread_local KernelTimer g_timer;
+
+enum TimedKind { TK_QKV = 0, TK_ATTN = 1, TK_O = 2, TK_GATEUP = 3, TK_DOWN = 4, TK_LM = 5 };
+
+hipError_t timer_begin(int kind, hipStream_t s, int *slot) {
+  *slot = -1;
+  if (g_timer.kind != kind || g_timer.next >= g_timer.n) return hipSuccess;
+  *slot = g_timer.next++;
+  return hipEventRecord((hipEvent_t)g_timer.start[*slot], s);
+}
+hipError_t timer_end(int slot, hipStream_t s) {
+  if (slot < 0) return hipSuccess;
+  return hipEventRecord((hipEvent_t)g_timer.stop[slot], s);
+}
+
+ppd_status fail(ppd_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define PPD_TRY_HIP(call)                                                               \
+  do {                                                                                  \
+    hipError_t e_ = (call);                                                             \
+    if (e_ != hipSuccess) return fail(PPD_EDEVICE, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kCUs = 256;          // MI355X compute units
+constexpr size_t kAlign = 256;
+constexpr int kAttnCounterBase = 4096;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
+int t_pad_of(int T) { return (T + 15) & ~15; }
+
+ppd_status check_model(const ppd_model *m) {
+  if (!m) return fail(PPD_EINVAL, "model is NULL");
+  if (m->n_layers < 1 || m->hidden < 1 || m->n_heads < 1 || m->n_kv_heads < 1 ||
+      m->head_dim < 2 || m->ffn < 1 || m->vocab < 1 || m->n_prompt < 0)
+    return fail(PPD_EINVAL, "model sizes must be positive");
+  if (m->n_heads % m->n_kv_heads) return fail(PPD_EINVAL, "n_kv_heads must divide n_heads");
+  if (m->head_dim % 2 || m->head_dim > 128)
+    return fail(PPD_EUNSUPPORTED, "head_dim must be even and <= 128");
+  if (!(m->rms_eps >= 0.f) || !(m->rope_base > 0.f))
+    return fail(PPD_EINVAL, "rms_eps must be >= 0 and rope_base > 0");
+  if (m->dtype != PPD_F32 && m->dtype != PPD_BF16) return fail(PPD_EINVAL, "unknown dtype");
+  if (m->dtype == PPD_BF16) {
+    if (m->head_dim != 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need head_dim 128");
+    if (m->hidden % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need hidden % 64 == 0");
+    if (m->ffn % 32) return fail(PPD_EUNSUPPORTED, "bf16 kernels need ffn % 32 == 0");
+    if ((m->vocab + 63) / 64 > kAttnCounterBase)
+      return fail(PPD_EUNSUPPORTED, "vocab too large (max %d)", 64 * kAttnCounterBase);
+  }
+  if (!m->tok_emb || !m->lm_head || !m->final_norm || (m->n_prompt > 0 && !m->prompt_emb))
+    return fail(PPD_EINVAL, "embedding, LM head and final norm pointers must be set");
+  const void *const *arrs[6] = {m->attn_norm, m->w_qkv, m->w_o, m->mlp_norm, m->w_gate_up,
+                                m->w_down};
+  for (int a = 0; a < 6; ++a) {
+    if (!arrs[a]) return fail(PPD_EINVAL, "per-layer pointer array %d is NULL", a);
+    for (int l = 0; l < m->n_layers; ++l)
+      if (!arrs[a][l]) return fail(PPD_EINVAL, "per-layer pointer %d of layer %d is NULL", a, l);
+  }
+  return PPD_OK;
+}
+
+int qkv_rows(const ppd_model *m) { return (m->n_heads + 2 * m->n_kv_heads) * m->head_dim; }
+
+// ---- launch-shape heuristics (also used to size the workspace)
+
+// split-K factor: about two workgroups per compute unit, each wave at least
+// 4 k-steps of 32
+int choose_sk(int n_tiles, int K) {
+  const int nks = K / 32;
+  int sk = (2 * kCUs + n_tiles - 1) / n_tiles;
+  sk = std::min(sk, std::max(1, nks / 16));
+  return std::max(1, std::min(sk, 16));
+}
+
+struct GemmShape {
+  int n_tiles, K;
+};
+
+void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
+  out[0] = {qkv_rows(m) / 64, m->hidden};          // QKV
+  out[1] = {m->hidden / 64, m->n_heads * 128};     // O
+  out[2] = {m->ffn / 32, m->hidden};               // gate/up (32 features per tile)
+  out[3] = {m->hidden / 64, m->ffn};               // down
+  out[4] = {(m->vocab + 63) / 64, m->hidden};      // LM head
+}
+
+int attn_max_splits(const ppd_model *m) {
+  return std::max(1, std::min(PPD_ATTN_MAX_SPLITS, 2 * kCUs / m->n_heads));
+}
+
+void attn_splits(const ppd_model *m, int L, int T, int *splits, int *chunk) {
+  const int nblk = (L + T + 31) / 32;
+  int s = std::min(attn_max_splits(m), std::max(1, nblk / 2));
+  int c = (nblk + s - 1) / s;
+  s = (nblk + c - 1) / c;
+  *splits = s;
+  *chunk = c;
+}
+
+WsLayout layout_of(const ppd_model *m, int T) {
+  WsLayout w{};
+  const int Tp = t_pad_of(T);
+  const size_t es = m->dtype == PPD_BF16 ? 2 : 4;
+  const int H = m->hidden, F = m->ffn, nh = m->n_heads, d = m->head_dim;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  w.n_counters = PPD_MAX_COUNTERS;
+  w.status = take(16);
+  w.counters = take(sizeof(uint32_t) * PPD_MAX_COUNTERS);
+  w.x = take(sizeof(float) * Tp * H);
+  w.xg = take(es * Tp * H + sizeof(float) * Tp);
+  w.max_ss = std::max(1, H / 64);
+  w.ss = take(sizeof(float) * w.max_ss * Tp);
+  w.q = take(es * Tp * nh * d);
+  w.attn_o = take(es * Tp * nh * d);
+  w.act = take(es * Tp * F);
+  if (m->dtype == PPD_F32) {
+    const size_t wide = std::max({(size_t)qkv_rows(m), (size_t)2 * F, (size_t)H, (size_t)m->vocab});
+    w.tmp = take(sizeof(float) * Tp * wide);
+  } else {
+    w.tmp = take(0);
+  }
+  w.max_splits = m->dtype == PPD_BF16 ? attn_max_splits(m) : 0;
+  w.attn_part = take(sizeof(float) * (size_t)nh * w.max_splits * Tp * 132);
+  size_t part = 0;
+  if (m->dtype == PPD_BF16) {
+    GemmShape gs[5];
+    gemm_shapes(m, gs);
+    for (int i = 0; i < 5; ++i) {
+      const int sk = choose_sk(gs[i].n_tiles, gs[i].K);
+      if (sk > 1) part = std::max(part, (size_t)gs[i].n_tiles * sk * 4 * (Tp / 16) * 64 * 4);
+    }
+  }
+  w.max_part_floats = part;
+  w.gemm_part = take(sizeof(float) * part);
+  w.max_amax_tiles = (m->vocab + 63) / 64;
+  w.amax = take(sizeof(float2) * w.max_amax_tiles * Tp);
+  w.rope = take(sizeof(float2) * Tp * (d / 2));
+  w.total = off;
+  return w;
+}
+
+template <typename P>
+P *at(void *ws, size_t off) {
+  return (P *)((char *)ws + off);
+}
+
+ppd_status check_kv(const ppd_model *m, const ppd_kv *kv) {
+  if (!kv || !kv->k || !kv->v) return fail(PPD_EINVAL, "kv cache pointers must be set");
+  if (kv->capacity < 1) return fail(PPD_EINVAL, "kv capacity must be positive");
+  if (m->dtype == PPD_BF16 && kv->capacity % 8)
+    return fail(PPD_EUNSUPPORTED, "bf16 caches need capacity %% 8 == 0");
+  return PPD_OK;
+}
+
+ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const int32_t *ids,
+                     const int32_t *depth, const uint64_t *mask, void *ws, const WsLayout &w,
+                     float *logits, int32_t *pred, hipStream_t s) {
+  const int H = m->hidden, F = m->ffn, nh = m->n_heads, nkv = m->n_kv_heads;
+  const int Tp = t_pad_of(T), MT = Tp / 16;
+  const int cap = kv->capacity;
+  uint32_t *status = at<uint32_t>(ws, w.status);
+  uint32_t *counters = at<uint32_t>(ws, w.counters);
+  float *x = at<float>(ws, w.x);
+  bf16_t *xg = at<bf16_t>(ws, w.xg);
+  float *ss = at<float>(ws, w.ss);
+  bf16_t *q = at<bf16_t>(ws, w.q);
+  bf16_t *attn_o = at<bf16_t>(ws, w.attn_o);
+  bf16_t *act = at<bf16_t>(ws, w.act);
+  float *part = at<float>(ws, w.gemm_part);
+  float2 *amax = at<float2>(ws, w.amax);
+  float2 *rope = at<float2>(ws, w.rope);
+  GemmShape gs[5];
+  gemm_shapes(m, gs);
+  int sk[5];
+  for (int i = 0; i < 5; ++i) sk[i] = choose_sk(gs[i].n_tiles, gs[i].K);
+
+  PPD_TRY_HIP(launch_rope_table(depth, T, L, m->head_dim, m->rope_base, rope, s));
+  PPD_TRY_HIP(launch_embed(PPD_BF16, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
+                           m->attn_norm[0], x, xg, ss, status, s));
+  int n_ss = 1;
+  int splits, chunk;
+  attn_splits(m, L, T, &splits, &chunk);
+  const float inv_h = 1.0f / (float)H;
+
+  for (int l = 0; l < m->n_layers; ++l) {
+    bf16_t *kc = (bf16_t *)kv->k + (size_t)l * nkv * cap * 128;
+    bf16_t *vc = (bf16_t *)kv->v + (size_t)l * nkv * 128 * cap;
+    GemmLaunch g{};
+    g.T = T;
+    g.MT = MT;
+    g.part = part;
+    g.counters = counters;
+    g.inv_h = inv_h;
+    g.eps = m->rms_eps;
+    g.status = status;
+    // QKV + RoPE + cache stores
+    g.kind = GEMM_QKV;
+    g.W = (const bf16_t *)m->w_qkv[l];
+    g.A = xg;
+    g.N = qkv_rows(m);
+    g.K = H;
+    g.sk = sk[0];
+    g.ss = ss;
+    g.n_ss = n_ss;
+    g.rope = rope;
+    g.q = q;
+    g.kc = kc;
+    g.vc = vc;
+    g.nh = nh;
+    g.nkv = nkv;
+    g.cap = cap;
+    g.L = L;
+    int slot;
+    PPD_TRY_HIP(timer_begin(TK_QKV, s, &slot));
+    PPD_TRY_HIP(launch_gemm_bf16(g, gs[0].n_tiles, s));
+    PPD_TRY_HIP(timer_end(slot, s));
+    // tree attention
+    AttnLaunch a{};
+    a.q = q;
+    a.kc = kc;
+    a.vc = vc;
+    a.mask = mask;
+    a.out = attn_o;
+    a.part = at<float>(ws, w.attn_part);
+    a.counters = counters + kAttnCounterBase;
+    a.T = T;
+    a.MT = MT;
+    a.L = L;
+    a.cap = cap;
+    a.nh = nh;
+    a.nkv = nkv;
+    a.splits = splits;
+    a.chunk = chunk;
+    a.scale_log2 = (float)(1.4426950408889634 / std::sqrt(128.0));
+    PPD_TRY_HIP(timer_begin(TK_ATTN, s, &slot));
+    PPD_TRY_HIP(launch_attn_bf16(a, s));
+    PPD_TRY_HIP(timer_end(slot, s));
+    // O projection + residual; operand of the MLP norm
+    GemmLaunch o = g;
+    o.kind = GEMM_RESID;
+    o.W = (const bf16_t *)m->w_o[l];
+    o.A = attn_o;
+    o.N = H;
+    o.K = nh * 128;
+    o.sk = sk[1];
+    o.x = x;
+    o.xg = xg;
+    o.gain = (const bf16_t *)m->mlp_norm[l];
+    o.ss_out = ss;
+    PPD_TRY_HIP(timer_begin(TK_O, s, &slot));
+    PPD_TRY_HIP(launch_gemm_bf16(o, gs[1].n_tiles, s));
+    PPD_TRY_HIP(timer_end(slot, s));
+    n_ss = gs[1].n_tiles;
+    // gate/up + SwiGLU
+    GemmLaunch u = g;
+    u.kind = GEMM_SWIGLU;
+    u.W = (const bf16_t *)m->w_gate_up[l];
+    u.A = xg;
+    u.N = F;
+    u.K = H;
+    u.sk = sk[2];
+    u.ss = ss;
+    u.n_ss = n_ss;
+    u.act = act;
+    PPD_TRY_HIP(timer_begin(TK_GATEUP, s, &slot));
+    PPD_TRY_HIP(launch_gemm_bf16(u, gs[2].n_tiles, s));
+    PPD_TRY_HIP(timer_end(slot, s));
+    // down projection + residual; operand of the next norm
+    GemmLaunch dn = g;
+    dn.kind = GEMM_RESID;
+    dn.W = (const bf16_t *)m->w_down[l];
+    dn.A = act;
+    dn.N = H;
+    dn.K = F;
+    dn.sk = sk[3];
+    dn.x = x;
+    dn.xg = xg;
+    dn.gain = (const bf16_t *)(l + 1 < m->n_layers ? m->attn_norm[l + 1] : m->final_norm);
+    dn.ss_out = ss;
+    PPD_TRY_HIP(timer_begin(TK_DOWN, s, &slot));
+    PPD_TRY_HIP(launch_gemm_bf16(dn, gs[3].n_tiles, s));
+    PPD_TRY_HIP(timer_end(slot, s));
+    n_ss = gs[3].n_tiles;
+  }
+  // final norm + LM head + greedy partials
+  GemmLaunch lm{};
+  lm.kind = GEMM_LOGITS;
+  lm.W = (const bf16_t *)m->lm_head;
+  lm.A = xg;
+  lm.N = m->vocab;
+  lm.K = H;
+  lm.T = T;
+  lm.MT = MT;
+  lm.sk = sk[4];
+  lm.part = part;
+  lm.counters = counters;
+  lm.ss = ss;
+  lm.n_ss = n_ss;
+  lm.inv_h = inv_h;
+  lm.eps = m->rms_eps;
+  lm.logits = logits;
+  lm.amax = amax;
+  lm.status = status;
+  int slot;
+  PPD_TRY_HIP(timer_begin(TK_LM, s, &slot));
+  PPD_TRY_HIP(launch_gemm_bf16(lm, gs[4].n_tiles, s));
+  PPD_TRY_HIP(timer_end(slot, s));
+  PPD_TRY_HIP(launch_argmax_final(amax, gs[4].n_tiles, T, Tp, pred, status, s));
+  return PPD_OK;
+}
+
+ppd_status step_f32(const ppd_model *m, const ppd_kv *kv, int L, int T, const int32_t *ids,
+                    const int32_t *depth, const uint64_t *mask, void *ws, const WsLayout &w,
+                    float *logits, int32_t *pred, hipStream_t s) {
+  const int H = m->hidden, F = m->ffn, nh = m->n_heads, nkv = m->n_kv_heads, d = m->head_dim;
+  const int Tp = t_pad_of(T);
+  const int cap = kv->capacity;
+  uint32_t *status = at<uint32_t>(ws, w.status);
+  float *x = at<float>(ws, w.x);
+  float *xg = at<float>(ws, w.xg);
+  float *r = xg + (size_t)Tp * H;
+  float *q = at<float>(ws, w.q);
+  float *attn_o = at<float>(ws, w.attn_o);
+  float *act = at<float>(ws, w.act);
+  float *tmp = at<float>(ws, w.tmp);
+  float2 *rope = at<float2>(ws, w.rope);
+
+  PPD_TRY_HIP(launch_rope_table(depth, T, L, d, m->rope_base, rope, s));
+  PPD_TRY_HIP(launch_embed(PPD_F32, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
+                           nullptr, x, nullptr, nullptr, status, s));
+  for (int l = 0; l < m->n_layers; ++l) {
+    float *kc = (float *)kv->k + (size_t)l * nkv * cap * d;
+    float *vc = (float *)kv->v + (size_t)l * nkv * d * cap;
+    PPD_TRY_HIP(launch_f32_rownorm(x, (const float *)m->attn_norm[l], T, H, m->rms_eps, xg, s));
+    PPD_TRY_HIP(launch_f32_matmul_scaled(xg, (const float *)m->w_qkv[l], T, qkv_rows(m), H, r,
+                                         tmp, s));
+    PPD_TRY_HIP(launch_f32_qkv_post(tmp, rope, T, nh, nkv, d, q, kc, vc, cap, L, s));
+    PPD_TRY_HIP(launch_f32_attention(q, kc, vc, mask, T, L, cap, nh, nkv, d, attn_o, s));
+    PPD_TRY_HIP(launch_f32_matmul(attn_o, (const float *)m->w_o[l], T, H, nh * d, tmp, s));
+    PPD_TRY_HIP(launch_f32_add(x, tmp, T * H, s));
+    PPD_TRY_HIP(launch_f32_rownorm(x, (const float *)m->mlp_norm[l], T, H, m->rms_eps, xg, s));
+    PPD_TRY_HIP(launch_f32_matmul_scaled(xg, (const float *)m->w_gate_up[l], T, 2 * F, H, r, tmp,
+                                         s));
+    PPD_TRY_HIP(launch_f32_swiglu(tmp, T, F, act, s));
+    PPD_TRY_HIP(launch_f32_matmul(act, (const float *)m->w_down[l], T, H, F, tmp, s));
+    PPD_TRY_HIP(launch_f32_add(x, tmp, T * H, s));
+  }
+  PPD_TRY_HIP(launch_f32_rownorm(x, (const float *)m->final_norm, T, H, m->rms_eps, xg, s));
+  float *lg = logits ? logits : tmp;
+  PPD_TRY_HIP(launch_f32_matmul_scaled(xg, (const float *)m->lm_head, T, m->vocab, H, r, lg, s));
+  PPD_TRY_HIP(launch_f32_argmax(lg, T, m->vocab, pred, status, s));
+  return PPD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ppd_workspace_bytes(const ppd_model *model, int32_t t_max, int32_t max_len) {
+  if (check_model(model) != PPD_OK) return 0;
+  if (t_max < 1 || t_max > PPD_T_MAX || max_len < 0) {
+    fail(PPD_EINVAL, "t_max must be in [1, %d] and max_len >= 0", PPD_T_MAX);
+    return 0;
+  }
+  return layout_of(model, t_max).total;
+}
+
+ppd_status ppd_workspace_init(void *ws, size_t ws_bytes, void *stream) {
+  const size_t need = align_up(16) + sizeof(uint32_t) * PPD_MAX_COUNTERS;
+  if (!ws || ws_bytes < need) return fail(PPD_EWORKSPACE, "workspace needs at least %zu bytes", need);
+  PPD_TRY_HIP(launch_ws_init(ws, need / 4, (hipStream_t)stream));
+  return PPD_OK;
+}
+
+ppd_status ppd_build_tree_mask(int32_t T, const int32_t *parent, int32_t *depth_out,
+                               uint64_t *mask_out) {
+  if (T < 1 || T > PPD_T_MAX) return fail(PPD_EINVAL, "T=%d outside [1, %d]", T, PPD_T_MAX);
+  if (!parent || !depth_out || !mask_out) return fail(PPD_EINVAL, "NULL argument");
+  if (parent[0] != -1) return fail(PPD_ETREE, "parent[0] must be -1 (root)");
+  for (int i = 1; i < T; ++i)
+    if (parent[i] < 0 || parent[i] >= i)
+      return fail(PPD_ETREE, "parent[%d]=%d is not an earlier node", i, parent[i]);
+  for (int i = 0; i < T; ++i) {
+    uint64_t row[PPD_MASK_WORDS] = {0, 0};
+    int dep = -1;
+    for (int j = i; j != -1; j = parent[j]) {
+      row[j >> 6] |= 1ull << (j & 63);
+      ++dep;
+    }
+    depth_out[i] = dep;
+    mask_out[i * PPD_MASK_WORDS + 0] = row[0];
+    mask_out[i * PPD_MASK_WORDS + 1] = row[1];
+  }
+  return PPD_OK;
+}
+
+ppd_status ppd_verify_step(const ppd_model *model, const ppd_kv *kv, int32_t L, int32_t T,
+                           const int32_t *ids, const int32_t *depth, const uint64_t *mask,
+                           void *ws, size_t ws_bytes, float *logits, int32_t *pred,
+                           void *stream) {
+  ppd_status st = check_model(model);
+  if (st != PPD_OK) return st;
+  if ((st = check_kv(model, kv)) != PPD_OK) return st;
+  if (T < 1 || T > PPD_T_MAX) return fail(PPD_EINVAL, "T=%d outside [1, %d]", T, PPD_T_MAX);
+  if (L < 0) return fail(PPD_EINVAL, "L must be >= 0");
+  if ((int64_t)L + T > kv->capacity)
+    return fail(PPD_ECAPACITY, "L + T = %lld exceeds capacity %d", (long long)L + T,
+                kv->capacity);
+  if (!ids || !depth || !mask || !pred) return fail(PPD_EINVAL, "NULL tree or output pointer");
+  const WsLayout w = layout_of(model, T);
+  if (!ws || ws_bytes < w.total)
+    return fail(PPD_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes,
+                w.total);
+  hipStream_t s = (hipStream_t)stream;
+  g_timer.next = 0;
+  if (model->dtype == PPD_BF16)
+    return step_bf16(model, kv, L, T, ids, depth, mask, ws, w, logits, pred, s);
+  return step_f32(model, kv, L, T, ids, depth, mask, ws, w, logits, pred, s);
+}
+
+ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids, const int32_t *pred,
+                      int32_t vocab, int32_t *path, int32_t *n_path, int32_t *next_tok, void *ws,
+                      size_t ws_bytes, void *stream) {
+  if (T < 1 || T > PPD_T_MAX) return fail(PPD_EINVAL, "T=%d outside [1, %d]", T, PPD_T_MAX);
+  if (vocab < 1) return fail(PPD_EINVAL, "vocab must be positive");
+  if (!parent || !ids || !pred || !path || !n_path || !next_tok)
+    return fail(PPD_EINVAL, "NULL argument");
+  if (!ws || ws_bytes < 16) return fail(PPD_EWORKSPACE, "workspace (status word) required");
+  PPD_TRY_HIP(launch_accept(T, parent, ids, pred, vocab, path, n_path, next_tok, (uint32_t *)ws,
+                            (hipStream_t)stream));
+  return PPD_OK;
+}
+
+ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
+                          const int32_t *path, const int32_t *n_path, void *stream) {
+  ppd_status st = check_model(model);
+  if (st != PPD_OK) return st;
+  if ((st = check_kv(model, kv)) != PPD_OK) return st;
+  if (L < 0 || L >= kv->capacity)
+    return fail(PPD_ECAPACITY, "L=%d must be in [0, capacity=%d)", L, kv->capacity);
+  if (!path || !n_path) return fail(PPD_EINVAL, "NULL path");
+  PPD_TRY_HIP(launch_kv_compact(model->dtype, kv->k, kv->v, model->n_layers, model->n_kv_heads,
+                                kv->capacity, model->head_dim, L, path, n_path, kv->len_dev,
+                                (hipStream_t)stream));
+  return PPD_OK;
+}
+
+ppd_status ppd_device_status(void *ws, size_t ws_bytes, uint32_t *status_out, int32_t clear,
+                             void *stream) {
+  if (!ws || ws_bytes < 16 || !status_out) return fail(PPD_EINVAL, "NULL or short workspace");
+  hipStream_t s = (hipStream_t)stream;
+  PPD_TRY_HIP(hipMemcpyAsync(status_out, ws, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  PPD_TRY_HIP(hipStreamSynchronize(s));
+  if (clear) PPD_TRY_HIP(launch_ws_init(ws, 4, s));
+  return PPD_OK;
+}
+
+ppd_status ppd_set_kernel_timer(int32_t kind, void *const *start_events, void *const *stop_events,
+                                int32_t n_events) {
+  if (n_events <= 0) {
+    g_timer = KernelTimer{};
+    return PPD_OK;
+  }
+  if (kind < TK_QKV || kind > TK_LM || !start_events || !stop_events)
+    return fail(PPD_EINVAL, "bad kernel timer arguments");
+  g_timer.kind = kind;
+  g_timer.start = start_events;
+  g_timer.stop = stop_events;
+  g_timer.n = n_events;
+  g_timer.next = 0;
+  return PPD_OK;
+}
+
+const char *ppd_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,161 @@
+// Internal declarations shared by the HIP kernels and the host driver of
+// libppd.  Device helpers: bfloat16 bit conversions (round to nearest even),
+// MFMA operand types, wavefront reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/ppd.h"
+
+typedef uint16_t bf16_t;  // raw bfloat16 storage word
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+#define PPD_WAVE 64
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// float -> bfloat16, round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ floatx4 mfma16x16x32(bf16x8 a, bf16x8 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, PPD_WAVE);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, PPD_WAVE));
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// workspace layout (computed on the host, passed to kernels as pointers)
+
+struct WsLayout {
+  size_t status;      // uint32 [4]
+  size_t counters;    // uint32 [n_counters]
+  size_t x;           // float  [T_pad][H]        residual stream
+  size_t xg;          // act    [T_pad][H]        x * gain (next norm's operand)
+  size_t ss;          // float  [max_ss][T_pad]   sum-of-squares partials
+  size_t q;           // act    [T_pad][nh][d]    queries after RoPE
+  size_t attn_o;      // act    [T_pad][nh d]     attention output
+  size_t act;         // act    [T_pad][F]        SwiGLU output
+  size_t tmp;         // float  [T_pad][max(qkv_rows, 2F, V)]  (fp32 path only)
+  size_t attn_part;   // float  [nh][max_splits][T_pad][d + 2]
+  size_t gemm_part;   // float  [max_part_floats]
+  size_t amax;        // float2 [max_amax_tiles][T_pad]
+  size_t rope;        // float2 [T_pad][d/2]      (cos, sin)
+  size_t total;
+  int n_counters, max_ss, max_splits, max_amax_tiles;
+  size_t max_part_floats;
+};
+
+#define PPD_MAX_COUNTERS 8192
+#define PPD_GEMM_BN 64         // output rows per GEMM tile
+#define PPD_ATTN_MAX_SPLITS 64
+
+// ---------------------------------------------------------------------------
+// kernel launchers (defined in the .hip files, called by the host driver)
+
+struct GemmLaunch {
+  // operands
+  const bf16_t *W;  // [N][K] (SwiGLU: gate rows then up rows, 2F x K)
+  const bf16_t *A;  // [T_pad][K]
+  int N, K, T, MT;  // N = output rows (SwiGLU: F), MT = T_pad / 16
+  int kind;         // GemmKind
+  int sk;           // split-K factor
+  float *part;
+  uint32_t *counters;
+  // epilogue inputs
+  const float *ss;  // norm partials for row scaling (QKV, SwiGLU, LOGITS)
+  int n_ss;
+  float inv_h, eps;
+  const float2 *rope;  // [T_pad][64]
+  // QKV outputs
+  bf16_t *q;           // [T_pad][nh][128]
+  bf16_t *kc, *vc;     // layer slice of the caches
+  int nh, nkv, cap, L;
+  // RESID
+  float *x;
+  bf16_t *xg;
+  const bf16_t *gain;  // next norm's gain [N]
+  float *ss_out;       // [n_tiles][T_pad]
+  // SWIGLU
+  bf16_t *act;         // [T_pad][N]
+  // LOGITS
+  float *logits;       // [T][N] or null
+  float2 *amax;        // [n_tiles][T_pad]
+  uint32_t *status;
+};
+
+enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_SWIGLU = 2, GEMM_LOGITS = 3 };
+
+hipError_t launch_gemm_bf16(const GemmLaunch &g, int n_tiles, hipStream_t s);
+
+struct AttnLaunch {
+  const bf16_t *q;   // [T_pad][nh][d]
+  const bf16_t *kc;  // [nkv][cap][d]
+  const bf16_t *vc;  // [nkv][d][cap]
+  const uint64_t *mask;
+  bf16_t *out;       // [T_pad][nh d]
+  float *part;       // [nh][splits][T_pad][d + 2]
+  uint32_t *counters;
+  int T, MT, L, cap, nh, nkv, splits, chunk;  // chunk: cached keys per split (multiple of 32)
+  float scale_log2;  // log2(e) / sqrt(d)
+};
+hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s);
+
+hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
+                        int T, int vocab, int n_prompt, int H, const void *gain, float *x,
+                        void *xg, float *ss, uint32_t *status, hipStream_t s);
+hipError_t launch_rope_table(const int32_t *depth, int T, int L, int d, float base, float2 *rope,
+                             hipStream_t s);
+hipError_t launch_argmax_final(const float2 *amax, int n_tiles, int T, int T_pad, int32_t *pred,
+                               uint32_t *status, hipStream_t s);
+hipError_t launch_accept(int T, const int32_t *parent, const int32_t *ids, const int32_t *pred,
+                         int vocab, int32_t *path, int32_t *n_path, int32_t *next_tok,
+                         uint32_t *status, hipStream_t s);
+hipError_t launch_kv_compact(int dtype, void *k, void *v, int n_layers, int nkv, int cap, int d,
+                             int L, const int32_t *path, const int32_t *n_path, int32_t *len_dev,
+                             hipStream_t s);
+hipError_t launch_ws_init(void *ws, size_t n_words, hipStream_t s);
+
+// fp32 path (simple kernels for float32 models)
+// xg = x * gain and r[t] = 1/sqrt(mean(x^2)+eps); r is stored after xg's T_pad rows
+hipError_t launch_f32_rownorm(const float *x, const float *gain, int T, int H, float eps,
+                              float *xg, hipStream_t s);
+hipError_t launch_f32_matmul(const float *A, const float *W, int T, int N, int K, float *out,
+                             hipStream_t s);
+hipError_t launch_f32_matmul_scaled(const float *A, const float *W, int T, int N, int K,
+                                    const float *r, float *out, hipStream_t s);
+hipError_t launch_f32_qkv_post(const float *qkv, const float2 *rope, int T, int nh, int nkv, int d,
+                               float *q, float *kc, float *vc, int cap, int L, hipStream_t s);
+hipError_t launch_f32_attention(const float *q, const float *kc, const float *vc,
+                                const uint64_t *mask, int T, int L, int cap, int nh, int nkv,
+                                int d, float *out, hipStream_t s);
+hipError_t launch_f32_add(float *x, const float *y, int n, hipStream_t s);
+hipError_t launch_f32_swiglu(const float *gu, int T, int F, float *act, hipStream_t s);
+hipError_t launch_f32_argmax(const float *logits, int T, int V, int32_t *pred, uint32_t *status,
+                             hipStream_t s);

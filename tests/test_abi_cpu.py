@@ -1,0 +1,120 @@
+"""C ABI checks that need no GPU: the library loads and exports every entry
+point its header declares; the host tree builder is bit-exact against the
+oracle; host-side validation rejects bad arguments before any device work."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_2405_18628_amd as ppd
+from synth.trees import make_tree
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    hdr = open(os.path.join(ROOT, "include", "ppd.h")).read()
+    return sorted(set(re.findall(r"\b(ppd_[a-z_]+)\s*\(", hdr)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = ppd.lib()
+    names = _declared()
+    assert {"ppd_verify_step", "ppd_accept", "ppd_kv_compact", "ppd_build_tree_mask"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+@pytest.mark.parametrize("spec", ["candidates:10", "candidates:32", "total:64", "total:128",
+                                  "chain:128", "chain:1"])
+def test_build_tree_mask_bit_exact(spec):
+    for seed in range(20):
+        if spec.startswith("chain"):
+            n = int(spec.split(":")[1])
+            parent = [-1] + list(range(n - 1))
+        else:
+            parent = make_tree(spec, 1000, 3, 5, seed, 1).parent
+        depth, mask = ppd.ppd_build_tree_mask(parent)
+        od, anc = O.build_mask(parent)
+        assert np.array_equal(depth, od.astype(np.int32))
+        assert np.array_equal(mask, O.pack_mask(anc))
+        if spec.startswith("chain"):
+            break
+
+
+@pytest.mark.parametrize("parent,code", [([0], ppd.PPD_ETREE), ([-1, 1], ppd.PPD_ETREE),
+                                         ([-1, 0, 3], ppd.PPD_ETREE), ([-1, -1], ppd.PPD_ETREE),
+                                         ([], ppd.PPD_EINVAL),
+                                         ([-1] + list(range(128)), ppd.PPD_EINVAL)])
+def test_build_tree_mask_rejects(parent, code):
+    with pytest.raises(ppd.PPDError) as e:
+        ppd.ppd_build_tree_mask(parent)
+    assert e.value.status == code
+
+
+def _fake_model(dtype=ppd.PPD_BF16, **kw):
+    """A model description whose pointers are non-null but never dereferenced:
+    every call below fails validation (or is host-only) before device work."""
+    n = kw.get("n_layers", 2)
+    fake = C.c_void_p(0x1000)
+    arr = (C.c_void_p * n)(*([0x1000] * n))
+    keep = [arr]
+    m = ppd.ppd_model(n, kw.get("hidden", 512), kw.get("n_heads", 4), kw.get("n_kv_heads", 4),
+                      kw.get("head_dim", 128), kw.get("ffn", 1376), kw.get("vocab", 1000), 3,
+                      1e-6, 10000.0, dtype, fake, fake,
+                      *[C.cast(arr, C.POINTER(C.c_void_p)) for _ in range(6)], fake, fake)
+    return m, keep
+
+
+def test_workspace_bytes_and_model_validation():
+    L = ppd.lib()
+    m, keep = _fake_model()
+    n64 = L.ppd_workspace_bytes(C.byref(m), 64, 4096)
+    n128 = L.ppd_workspace_bytes(C.byref(m), 128, 4096)
+    assert 0 < n64 <= n128
+    assert L.ppd_workspace_bytes(C.byref(m), 0, 10) == 0
+    assert L.ppd_workspace_bytes(C.byref(m), 129, 10) == 0
+    for bad in (dict(head_dim=64), dict(hidden=500), dict(ffn=1000), dict(n_kv_heads=3)):
+        mb, kb = _fake_model(**bad)
+        assert L.ppd_workspace_bytes(C.byref(mb), 16, 10) == 0
+        assert ppd.ppd_last_error()
+    mf, kf = _fake_model(ppd.PPD_F32, head_dim=64, hidden=256, ffn=688)
+    assert L.ppd_workspace_bytes(C.byref(mf), 40, 200) > 0
+
+
+def test_verify_rejects_before_enqueue():
+    L = ppd.lib()
+    m, keep = _fake_model()
+    kv = ppd.ppd_kv(0x2000, 0x3000, 256, None)
+    fake = 0x4000
+    ws_bytes = L.ppd_workspace_bytes(C.byref(m), 16, 256)
+
+    def call(T=16, Lc=0, kvd=kv, wsb=ws_bytes, ids=fake):
+        return L.ppd_verify_step(C.byref(m), C.byref(kvd), Lc, T, ids, fake, fake, fake, wsb,
+                                 None, fake, None)
+    assert call(T=0) == ppd.PPD_EINVAL
+    assert call(T=129) == ppd.PPD_EINVAL
+    assert call(Lc=-1) == ppd.PPD_EINVAL
+    assert call(Lc=250) == ppd.PPD_ECAPACITY
+    assert call(wsb=ws_bytes - 1) == ppd.PPD_EWORKSPACE
+    assert call(ids=None) == ppd.PPD_EINVAL
+    assert call(kvd=ppd.ppd_kv(0x2000, 0x3000, 252, None)) == ppd.PPD_EUNSUPPORTED
+    assert call(kvd=ppd.ppd_kv(None, 0x3000, 256, None)) == ppd.PPD_EINVAL
+    assert "capacity" in ppd.ppd_last_error() or ppd.ppd_last_error()
+
+
+def test_accept_and_compact_reject_before_enqueue():
+    L = ppd.lib()
+    m, keep = _fake_model()
+    f = 0x4000
+    assert L.ppd_accept(0, f, f, f, 10, f, f, f, f, 64, None) == ppd.PPD_EINVAL
+    assert L.ppd_accept(129, f, f, f, 10, f, f, f, f, 64, None) == ppd.PPD_EINVAL
+    assert L.ppd_accept(4, f, f, f, 0, f, f, f, f, 64, None) == ppd.PPD_EINVAL
+    assert L.ppd_accept(4, f, f, f, 10, f, f, f, None, 64, None) == ppd.PPD_EWORKSPACE
+    kv = ppd.ppd_kv(0x2000, 0x3000, 256, None)
+    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 256, f, f, None) == ppd.PPD_ECAPACITY
+    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 10, None, f, None) == ppd.PPD_EINVAL
+    assert L.ppd_workspace_init(None, 0, None) == ppd.PPD_EWORKSPACE
