@@ -210,46 +210,62 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
     return;
   }
 
-  // publish this split's (O, m, l); row stride 132 floats
-  float *mypart = p.part + ((size_t)h * p.splits + split) * T_pad * 132;
+  // Publish this split's (O, m, l), row stride 132 floats, with agent-scope
+  // relaxed atomic stores: they write through to memory that every XCD sees,
+  // without the L2 write-back and invalidate that a device fence costs.  The
+  // ticket is taken only after the stores have completed (s_waitcnt), and
+  // the last split reads the partials back with agent-scope atomic loads,
+  // which bypass any stale copy in its own L2.
+  uint64_t *mypart = (uint64_t *)(p.part + ((size_t)h * p.splits + split) * T_pad * 132);
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int qt = wave + 4 * q;
     if (qt >= p.MT) continue;
     const int t = qt * 16 + lr;
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) *(floatx4 *)(mypart + (size_t)t * 132 + dt * 16 + lg * 4) = o[q][dt];
-    if (lg == 0) {
-      mypart[(size_t)t * 132 + 128] = m_run[q];
-      mypart[(size_t)t * 132 + 129] = l_run[q];
+    for (int dt = 0; dt < 8; ++dt) {
+      uint64_t *d = mypart + ((size_t)t * 132 + dt * 16 + lg * 4) / 2;
+      const floatx4 v = o[q][dt];
+      __hip_atomic_store(d, __builtin_bit_cast(uint64_t, float2{v[0], v[1]}), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(d + 1, __builtin_bit_cast(uint64_t, float2{v[2], v[3]}), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
     }
+    if (lg == 0)
+      __hip_atomic_store(mypart + ((size_t)t * 132 + 128) / 2,
+                         __builtin_bit_cast(uint64_t, float2{m_run[q], l_run[q]}), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
   }
-  __threadfence();
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    const unsigned prev = atomicAdd(&p.counters[h], 1u);
+    const unsigned prev =
+        __hip_atomic_fetch_add(&p.counters[h], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int last = prev == (unsigned)(p.splits - 1);
-    if (last) p.counters[h] = 0u;
+    if (last) __hip_atomic_store(&p.counters[h], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     last_s = last;
   }
   __syncthreads();
   if (!last_s) return;
-  __threadfence();
 
   // combine the splits of head h in split order: thread -> (t, 4 dims)
-  const float *hp = p.part + (size_t)h * p.splits * T_pad * 132;
+  const uint64_t *hp = (const uint64_t *)(p.part + (size_t)h * p.splits * T_pad * 132);
+  auto ld2 = [](const uint64_t *a) {
+    return __builtin_bit_cast(float2, __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  };
   for (int w = threadIdx.x; w < p.T * 32; w += 256) {
     const int t = w >> 5, d4 = (w & 31) * 4;
     float M = -INFINITY;
-    for (int s = 0; s < p.splits; ++s) M = fmaxf(M, hp[((size_t)s * T_pad + t) * 132 + 128]);
+    for (int s = 0; s < p.splits; ++s) M = fmaxf(M, ld2(hp + (((size_t)s * T_pad + t) * 132 + 128) / 2).x);
     floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
     float lsum = 0.f;
     for (int s = 0; s < p.splits; ++s) {
-      const float *row = hp + ((size_t)s * T_pad + t) * 132;
-      const float ms = row[128];
-      const float sc = ms == -INFINITY ? 0.f : exp2f(ms - M);
-      lsum += sc * row[129];
-      acc += sc * *(const floatx4 *)(row + d4);
+      const uint64_t *row = hp + ((size_t)s * T_pad + t) * 132 / 2;
+      const float2 ml = ld2(row + 64);
+      const float sc = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M);
+      lsum += sc * ml.y;
+      const float2 a = ld2(row + d4 / 2), b = ld2(row + d4 / 2 + 1);
+      acc += sc * floatx4{a.x, a.y, b.x, b.y};
     }
     const float inv = 1.f / lsum;
     *(u32x2 *)(p.out + (size_t)t * p.nh * 128 + h * 128 + d4) =

@@ -1,201 +1,282 @@
 // Skinny-M bfloat16 GEMMs of the verification forward pass, with fused
 // epilogues.  out[row][t] = sum_k W[row][k] * A[t][k] for the T <= 128 tree
 // tokens t, fp32 accumulation on the gfx950 matrix cores
-// (v_mfma_f32_16x16x32_bf16: weights are the 16-row A operand, tokens the
+// (v_mfma_f32_16x16x32_bf16: weight rows are the 16-row A operand, tokens the
 // 16-column B operand).
 //
 // The step is bound by streaming the weights from HBM once (arithmetic
 // intensity ~T flop/byte, far below the MI355X ridge), so the kernel is built
 // around the weight stream:
-//  * a workgroup owns a 64-row tile of W and one slice of K (split-K across
-//    workgroups when N alone gives too few tiles); its 4 waves split the
-//    slice's K range, so every weight and activation byte is loaded by
-//    exactly one lane, straight from global memory into MFMA operand
-//    registers (16 bytes per lane, no LDS staging);
-//  * loads are double-buffered in registers, weights with a non-temporal hint
-//    (streamed once), activations through L2 (shared by every workgroup);
-//  * the 4 waves' partial tiles are summed in LDS in a fixed order; split-K
-//    partials go to the workspace and the last workgroup of a tile (atomic
-//    ticket) adds them in split order, so results never depend on timing;
+//  * a workgroup owns a tile of BN weight rows (128, or 64 for the residual
+//    projections) and one slice of K (split-K across workgroups where N alone
+//    gives too few tiles);
+//  * K is walked in 64-wide chunks.  Each chunk of weights and activations
+//    is fetched cooperatively with 16-byte direct-to-LDS transfers
+//    (global_load_lds_dwordx4) in which 8 consecutive lanes cover one row's
+//    full 128-byte line (the pattern that streams at full HBM rate).  An
+//    NS-slot LDS ring keeps NS-1 chunks in flight; 16-byte columns are
+//    XOR-swizzled per row pair, so the MFMA operand reads are conflict-free;
+//  * each workgroup starts its K walk at its own chunk offset, which spreads
+//    the lockstep workgroups over the HBM channels;
+//  * each wave owns whole 16-row sub-tiles (two of them, 64 rows apart, for
+//    128-row tiles: the RoPE and SwiGLU partners), so no reduction between
+//    waves is needed;
+//  * split-K partials go to the workspace with agent-scope relaxed atomic
+//    stores (coherent across the XCDs without L2 write-back/invalidate); the
+//    last workgroup of a tile (atomic ticket) adds them in split order, so
+//    results never depend on timing;
 //  * the epilogue is fused: RMSNorm row scale, RoPE + query/key/value stores
 //    into the cache (QKV), residual add + next norm operand + sum of squares
-//    (O / down projection), SwiGLU (gate/up), logits + argmax partials (LM
-//    head).
+//    (output / down projection), SwiGLU (gate/up), logits + argmax partials
+//    (LM head).
 #include "ppd_internal.h"
 
 namespace {
 
-constexpr int BN = PPD_GEMM_BN;  // 64 rows = 4 sub-tiles of 16
-constexpr int U = 2;             // k-steps (32 each) per pipeline stage
+#ifndef PPD_GEMM_NS
+#define PPD_GEMM_NS 3
+#endif
+constexpr int NS = PPD_GEMM_NS;  // LDS ring slots (chunks requested ahead + 1)
+constexpr int KC = 64;           // K per chunk: two MFMA k-steps, one 128-byte line per row
 
-__device__ __forceinline__ u32x4 ldg_nt(const bf16_t *p) {
-  return __builtin_nontemporal_load((const u32x4 *)p);
-}
-__device__ __forceinline__ u32x4 ldg(const bf16_t *p) { return *(const u32x4 *)p; }
-
-// first W row of sub-tile j (0..3) of `tile`
 template <int KIND>
-__device__ __forceinline__ int subtile_row(int tile, int j, int F) {
-  if constexpr (KIND == GEMM_QKV) {
-    // tile = (head part hp, half hh): sub-tiles 0,1 hold dims 32hh..32hh+31,
-    // sub-tiles 2,3 the RoPE partners 64 + 32hh ..
-    return (tile >> 1) * 128 + (tile & 1) * 32 + (j & 1) * 16 + (j >> 1) * 64;
-  } else if constexpr (KIND == GEMM_SWIGLU) {
-    // features 32 tile .. 32 tile + 31: sub-tiles 0,1 gate rows, 2,3 up rows
-    return (j >> 1) * F + tile * 32 + (j & 1) * 16;
+constexpr int kSub = (KIND == GEMM_RESID) ? 1 : 2;  // 16-row sub-tiles per wave
+template <int KIND>
+constexpr int kBN = 64 * kSub<KIND>;                 // rows per tile
+
+// weight row of tile row r (0 <= r < BN)
+template <int KIND>
+__device__ __forceinline__ int tile_row(int tile, int r, int F) {
+  if constexpr (KIND == GEMM_SWIGLU) {
+    // 64 features: gate rows f0..f0+63, then the matching up rows
+    return r < 64 ? tile * 64 + r : F + tile * 64 + (r - 64);
   } else {
-    return tile * BN + j * 16;
+    // QKV: tile = one head's 128 rows (dims 0..127); others: consecutive rows
+    return tile * kBN<KIND> + r;
   }
 }
 
+__device__ __forceinline__ void amax_merge(float &v, int &i, float v2, int i2) {
+  if (i2 >= 0 && (i < 0 || v2 > v || (v2 == v && i2 < i))) {
+    v = v2;
+    i = i2;
+  }
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+// 16-byte column swizzle of a 128-byte LDS row: logical column c of row r is
+// stored at physical column c ^ ((r >> 1) & 7).  Sixteen consecutive rows
+// read at one logical column then cover all 64 banks exactly once.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+
+// One 16-byte-per-lane global -> LDS transfer (global_load_lds_dwordx4): lane
+// l's 16 bytes land at LDS byte lds_addr + 16 l.  Issued as inline assembly so
+// that the compiler does not track the LDS write: its waitcnt pass would
+// otherwise drain every transfer in flight before each LDS read; the kernel
+// waits explicitly (s_waitcnt vmcnt + barrier) instead.
+__device__ __forceinline__ void dma16(const void *g, unsigned lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
+               : "memory", "m0");
+}
+
+// s_waitcnt immediate for "at most n vector-memory operations outstanding"
+// (expcnt and lgkmcnt left at their maxima, i.e. not waited on)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
 template <int MT, int KIND>
-__global__ __launch_bounds__(256, (MT <= 4 ? 2 : 1)) void gemm_bf16_kernel(GemmLaunch g) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
+  constexpr int SUB = kSub<KIND>;
+  constexpr int BN = kBN<KIND>;
+  constexpr int T_pad = MT * 16;
+  constexpr int WBLK = BN / 8;                // 8-row blocks of weights per chunk
+  constexpr int ABLK = T_pad / 8;             // 8-row blocks of activations per chunk
+  constexpr int NW = WBLK / 4;                // per wave (BN is a multiple of 32)
+  constexpr int NA = (ABLK + 3) / 4;          // per wave (excess loads hit a dummy block)
+  constexpr int LPC = NW + NA;                // vector loads per wave per chunk
+  constexpr int SLOT = (BN + T_pad) * 128;    // bytes of one ring slot
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[NS * SLOT + 1024];
+  __shared__ float rs_s[128];
+  __shared__ float red_s[4][128][2];
+  __shared__ int last_s;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15;         // MFMA row (weights) / column (tokens) within a 16-tile
+  const int lg = lane >> 4;         // this lane's 16-byte k group within a 32-step
   const int split = blockIdx.x % g.sk;
   const int tile = blockIdx.x / g.sk;
   const int K = g.K;
-  const int rows_total = (KIND == GEMM_SWIGLU) ? 2 * g.N : (KIND == GEMM_QKV ? g.N : g.N);
-  const int lr = lane & 15;         // row within sub-tile (A operand) / token within tile (B)
-  const int kg = (lane >> 4) * 8;   // this lane's 8-element k group within a 32-step
-
-  // k-steps of this split, then of this wave
   const int nks = K >> 5;
-  const int s0 = (int)((long)nks * split / g.sk), s1 = (int)((long)nks * (split + 1) / g.sk);
-  const int w0 = s0 + (s1 - s0) * wave / 4, w1 = s0 + (s1 - s0) * (wave + 1) / 4;
+  const int k_begin = (int)((long)nks * split / g.sk) * 32;
+  const int k_end = (int)((long)nks * (split + 1) / g.sk) * 32;
+  const int n_chunks = (k_end - k_begin + KC - 1) / KC;
+  const int rows_total = KIND == GEMM_SWIGLU ? 2 * g.N : g.N;
 
-  const bf16_t *wrow[4];
+  // ---- load slots.  A wave instruction moves one 8-row block: lane l lands
+  // at LDS byte 16 l of the block, i.e. row (l >> 3), physical column l & 7,
+  // so it fetches logical column swz(row, l & 7) of that row from memory.
+  const int wv = __builtin_amdgcn_readfirstlane(wave);  // wave index as a scalar
+  const unsigned lds_base = (unsigned)(size_t)(lds_void_t *)lds;
+  const int brow = lane >> 3;
+  const bf16_t *wsrc[NW];
+  int wcol[NW];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    int r = subtile_row<KIND>(tile, j, g.N) + lr;
-    r = r < rows_total ? r : rows_total - 1;
-    wrow[j] = g.W + (size_t)r * K + kg;
+  for (int i = 0; i < NW; ++i) {
+    const int r = (wave + 4 * i) * 8 + brow;
+    const int c = swz(r, lane & 7);
+    int row = tile_row<KIND>(tile, r, g.N);
+    row = row < rows_total ? row : rows_total - 1;
+    wsrc[i] = g.W + (size_t)row * K + c * 8;
+    wcol[i] = c * 8;
   }
-  const bf16_t *arow[MT];
+  const bf16_t *asrc[NA];
+  int acol[NA];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) arow[mt] = g.A + (size_t)(mt * 16 + lr) * K + kg;
-
-  floatx4 acc[4][MT];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  u32x4 wb0[U][4], ab0[U][MT], wb1[U][4], ab1[U][MT];
-  const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
-
-#define PPD_LOAD(WB, AB, KS)                                              \
-  _Pragma("unroll") for (int u = 0; u < U; ++u) {                         \
-    const int ks_ = (KS) + u;                                             \
-    if (ks_ < w1) {                                                       \
-      _Pragma("unroll") for (int j = 0; j < 4; ++j) WB[u][j] = ldg_nt(wrow[j] + ks_ * 32); \
-      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) AB[u][mt] = ldg(arow[mt] + ks_ * 32); \
-    } else {                                                              \
-      _Pragma("unroll") for (int j = 0; j < 4; ++j) WB[u][j] = zero;      \
-      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt) AB[u][mt] = zero; \
-    }                                                                     \
+  for (int i = 0; i < NA; ++i) {
+    const int blk = wave + 4 * i;
+    const int r = (blk < ABLK ? blk : 0) * 8 + brow;
+    const int c = swz(r, lane & 7);
+    asrc[i] = g.A + (size_t)r * K + c * 8;
+    acol[i] = c * 8;
   }
-#define PPD_COMPUTE(WB, AB)                                               \
-  _Pragma("unroll") for (int u = 0; u < U; ++u)                           \
-    _Pragma("unroll") for (int j = 0; j < 4; ++j)                         \
-      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt)                   \
-        acc[j][mt] = mfma16x16x32(as_bf16x8(WB[u][j]), as_bf16x8(AB[u][mt]), acc[j][mt]);
 
-  PPD_LOAD(wb0, ab0, w0);
-  for (int ks = w0; ks < w1; ks += 2 * U) {
-    PPD_LOAD(wb1, ab1, ks + U);
-    PPD_COMPUTE(wb0, ab0);
-    PPD_LOAD(wb0, ab0, ks + 2 * U);
-    PPD_COMPUTE(wb1, ab1);
-  }
-#undef PPD_LOAD
-#undef PPD_COMPUTE
+  floatx4 acc[SUB][MT];
+#pragma unroll
+  for (int q = 0; q < SUB; ++q)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // ---- sum the 4 waves' partial tiles (fixed order); waves 0 and 1 keep
-  // sub-tiles (w, w + 2) -- the RoPE / SwiGLU partner pairs.
-  __shared__ floatx4 red[4][4][64];
-  __shared__ float rs_s[128];
-  __shared__ float pair_s[2][128][2];
-  __shared__ int last_s;
-  floatx4 res[2][MT];
+  // Chunk C goes to ring slot C % NS; columns past the slice end (and the
+  // padding transfers of waves without an activation block) read 16 zero
+  // bytes of the workspace.
+  const bf16_t *zp = g.zeros;
+  // Each workgroup walks its slice starting at its own chunk offset: all
+  // workgroups start together, and rows 8 KB apart otherwise hit the same
+  // HBM channels in lockstep.
+  const int rot = n_chunks > 0 ? (int)(blockIdx.x % (unsigned)n_chunks) : 0;
+  auto issue = [&](int C) {
+    const int cc = C < n_chunks ? (C + rot) % n_chunks : C;
+    const int k0 = k_begin + cc * KC;
+    const unsigned slot = lds_base + (unsigned)((C % NS) * SLOT);
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
+    for (int i = 0; i < NW; ++i)
+      dma16(k0 + wcol[i] < k_end ? wsrc[i] + k0 : zp, slot + (unsigned)((wv + 4 * i) * 1024));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) red[wave][j][lane] = acc[j][mt];
-    __syncthreads();
-    if (wave < 2) {
+    for (int i = 0; i < NA; ++i) {
+      const int blk = wv + 4 * i;  // scalar
+      if (blk < ABLK)
+        dma16(k0 + acol[i] < k_end ? asrc[i] + k0 : zp, slot + (unsigned)(BN * 128 + blk * 1024));
+      else
+        dma16(zp, lds_base + (unsigned)(NS * SLOT));
+    }
+  };
+
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int j = wave + 2 * p;
-        res[p][mt] = ((red[0][j][lane] + red[1][j][lane]) + red[2][j][lane]) + red[3][j][lane];
+  for (int c = 0; c < NS - 1; ++c) issue(c);
+  for (int c = 0; c < n_chunks; ++c) {
+    // own transfers of chunk c done (chunks c+1 .. c+NS-2 may still fly),
+    // then every wave's; the barrier also retires all reads of chunk c-1,
+    // whose slot the next request overwrites.  (A bare s_barrier: a fence
+    // would wait for every transfer in flight.)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPC));
+    asm volatile("s_barrier" ::: "memory");
+    issue(c + NS - 1);
+    const unsigned char *wl = lds + (c % NS) * SLOT;
+    const unsigned char *al = wl + BN * 128;
+#pragma unroll
+    for (int s = 0; s < KC / 32; ++s) {
+      u32x4 wf[SUB], af[MT];
+#pragma unroll
+      for (int q = 0; q < SUB; ++q) {
+        const int r = (wave + 4 * q) * 16 + lr;
+        wf[q] = *(const u32x4 *)(wl + r * 128 + swz(r, s * 4 + lg) * 16);
       }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int r = mt * 16 + lr;
+        af[mt] = *(const u32x4 *)(al + r * 128 + swz(r, s * 4 + lg) * 16);
+      }
+#pragma unroll
+      for (int q = 0; q < SUB; ++q)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          acc[q][mt] = mfma16x16x32(as_bf16x8(wf[q]), as_bf16x8(af[mt]), acc[q][mt]);
     }
-    __syncthreads();
   }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
 
-  // ---- split-K: publish the partial tile; the last workgroup sums all
+  // ---- split-K: publish the partial tile; the last workgroup sums all.
+  // Partials are written and read with agent-scope relaxed atomics (coherent
+  // across the XCDs without writing back or invalidating whole L2 caches);
+  // every store has completed (vmcnt 0) before the ticket is taken.
   if (g.sk > 1) {
-    const size_t tile_floats = (size_t)4 * MT * 64 * 4;
-    if (wave < 2) {
-      floatx4 *dst = (floatx4 *)(g.part + (size_t)blockIdx.x * tile_floats);
+    constexpr size_t tile_u64 = (size_t)4 * SUB * MT * 64 * 2;
+    {
+      uint64_t *dst = (uint64_t *)g.part + (size_t)blockIdx.x * tile_u64;
 #pragma unroll
-      for (int p = 0; p < 2; ++p)
+      for (int q = 0; q < SUB; ++q)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) dst[((wave * 2 + p) * MT + mt) * 64 + lane] = res[p][mt];
+        for (int mt = 0; mt < MT; ++mt) {
+          const size_t o = (size_t)(((wave * SUB + q) * MT + mt) * 64 + lane) * 2;
+          const floatx4 r = acc[q][mt];
+          __hip_atomic_store(dst + o, __builtin_bit_cast(uint64_t, float2{r[0], r[1]}),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(dst + o + 1, __builtin_bit_cast(uint64_t, float2{r[2], r[3]}),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
-    __threadfence();
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) {
-      unsigned prev = atomicAdd(&g.counters[tile], 1u);
-      int last = prev == (unsigned)(g.sk - 1);
-      if (last) g.counters[tile] = 0u;
+    if (tid == 0) {
+      const unsigned prev =
+          __hip_atomic_fetch_add(&g.counters[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int last = prev == (unsigned)(g.sk - 1);
+      if (last) __hip_atomic_store(&g.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       last_s = last;
     }
     __syncthreads();
     if (!last_s) return;
-    __threadfence();
-    if (wave < 2) {
 #pragma unroll
-      for (int p = 0; p < 2; ++p)
+    for (int q = 0; q < SUB; ++q)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) res[p][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < g.sk; ++s) {
-        const floatx4 *src = (const floatx4 *)(g.part + (size_t)(tile * g.sk + s) * tile_floats);
+      for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < g.sk; ++s) {
+      const uint64_t *src = (const uint64_t *)g.part + (size_t)(tile * g.sk + s) * tile_u64;
 #pragma unroll
-        for (int p = 0; p < 2; ++p)
+      for (int q = 0; q < SUB; ++q)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            res[p][mt] += src[((wave * 2 + p) * MT + mt) * 64 + lane];
-      }
+        for (int mt = 0; mt < MT; ++mt) {
+          const size_t o = (size_t)(((wave * SUB + q) * MT + mt) * 64 + lane) * 2;
+          const float2 a = __builtin_bit_cast(
+              float2, __hip_atomic_load(src + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+          const float2 b = __builtin_bit_cast(
+              float2, __hip_atomic_load(src + o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+          acc[q][mt] += floatx4{a.x, a.y, b.x, b.y};
+        }
     }
   }
 
   // ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) from the
   // producer's sum-of-squares partials (summed in partial order)
   if constexpr (KIND != GEMM_RESID) {
-    if (threadIdx.x < MT * 16) {
-      const int t = threadIdx.x;
-      const int T_pad = MT * 16;
+    if (tid < T_pad) {
       float s = 0.f;
-      for (int p = 0; p < g.n_ss; ++p) s += g.ss[(size_t)p * T_pad + t];
-      rs_s[t] = rsqrtf(s * g.inv_h + g.eps);
+      for (int p = 0; p < g.n_ss; ++p) s += g.ss[(size_t)p * T_pad + tid];
+      rs_s[tid] = rsqrtf(s * g.inv_h + g.eps);
     }
     __syncthreads();
   }
-  if (wave >= 2) {
-    if constexpr (KIND == GEMM_RESID || KIND == GEMM_LOGITS) {
-      __syncthreads();  // matches the pair exchange below
-    }
-    return;
-  }
 
-  const int r4 = (lane >> 4) * 4;  // first of this lane's 4 rows within a sub-tile
+  // accumulator layout: lane holds rows 4 (lane / 16) + e of its sub-tile,
+  // token column lane % 16 of token tile mt
+  const int r4 = (lane >> 4) * 4;
   const int T = g.T;
-  const int T_pad = MT * 16;
 
   if constexpr (KIND == GEMM_QKV) {
-    const int hp = tile >> 1;
-    const int i0 = (tile & 1) * 32 + wave * 16 + r4;  // dims i0..i0+3 and +64
+    const int hp = tile;                // head part: q heads, then k, then v
+    const int i0 = wave * 16 + r4;      // dims i0..i0+3 and their partners +64
     const int nh = g.nh, nkv = g.nkv;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -205,8 +286,8 @@ __global__ __launch_bounds__(256, (MT <= 4 ? 2 : 1)) void gemm_bf16_kernel(GemmL
       float lo[4], hi[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        lo[e] = res[0][mt][e] * rs;
-        hi[e] = res[1][mt][e] * rs;
+        lo[e] = acc[0][mt][e] * rs;
+        hi[e] = acc[1][mt][e] * rs;
       }
       if (hp < nh + nkv) {
 #pragma unroll
@@ -216,14 +297,10 @@ __global__ __launch_bounds__(256, (MT <= 4 ? 2 : 1)) void gemm_bf16_kernel(GemmL
           lo[e] = a * cs.x - b * cs.y;
           hi[e] = b * cs.x + a * cs.y;
         }
-        u32x2 plo = u32x2{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
-        u32x2 phi = u32x2{pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
-        bf16_t *dst;
-        if (hp < nh) {
-          dst = g.q + ((size_t)t * nh + hp) * 128;
-        } else {
-          dst = g.kc + ((size_t)(hp - nh) * g.cap + g.L + t) * 128;
-        }
+        const u32x2 plo = u32x2{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
+        const u32x2 phi = u32x2{pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
+        bf16_t *dst = hp < nh ? g.q + ((size_t)t * nh + hp) * 128
+                              : g.kc + ((size_t)(hp - nh) * g.cap + g.L + t) * 128;
         *(u32x2 *)(dst + i0) = plo;
         *(u32x2 *)(dst + i0 + 64) = phi;
       } else {
@@ -236,7 +313,7 @@ __global__ __launch_bounds__(256, (MT <= 4 ? 2 : 1)) void gemm_bf16_kernel(GemmL
       }
     }
   } else if constexpr (KIND == GEMM_SWIGLU) {
-    const int f0 = tile * 32 + wave * 16 + r4;
+    const int f0 = tile * 64 + wave * 16 + r4;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int t = mt * 16 + lr;
@@ -245,67 +322,55 @@ __global__ __launch_bounds__(256, (MT <= 4 ? 2 : 1)) void gemm_bf16_kernel(GemmL
       float a[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float gt = res[0][mt][e] * rs, up = res[1][mt][e] * rs;
+        const float gt = acc[0][mt][e] * rs, up = acc[1][mt][e] * rs;
         a[e] = gt / (1.f + expf(-gt)) * up;
       }
       *(u32x2 *)(g.act + (size_t)t * g.N + f0) =
           u32x2{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3])};
     }
   } else if constexpr (KIND == GEMM_RESID) {
-    float sq[MT];
+    const int n = tile * 64 + wave * 16 + r4;
+    const uint2 gw = *(const uint2 *)(g.gain + n);
+    const float g0 = bf16_to_f32(gw.x & 0xffff), g1 = bf16_to_f32(gw.x >> 16);
+    const float g2 = bf16_to_f32(gw.y & 0xffff), g3 = bf16_to_f32(gw.y >> 16);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int t = mt * 16 + lr;
-      sq[mt] = 0.f;
-      if (t >= T) continue;
-#pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int n = tile * BN + (wave + 2 * p) * 16 + r4;
+      float sq = 0.f;
+      if (t < T) {
         float *xp = g.x + (size_t)t * g.N + n;
         floatx4 xv = *(floatx4 *)xp;
-        xv += res[p][mt];
+        xv += acc[0][mt];
         *(floatx4 *)xp = xv;
-        const uint2 gw = *(const uint2 *)(g.gain + n);
-        const float g0 = bf16_to_f32(gw.x & 0xffff), g1 = bf16_to_f32(gw.x >> 16);
-        const float g2 = bf16_to_f32(gw.y & 0xffff), g3 = bf16_to_f32(gw.y >> 16);
         *(u32x2 *)(g.xg + (size_t)t * g.N + n) =
             u32x2{pack_bf16x2(xv[0] * g0, xv[1] * g1), pack_bf16x2(xv[2] * g2, xv[3] * g3)};
-        sq[mt] += (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
+        sq = (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
       }
-    }
-    // reduce over the 4 lane groups (rows), then over the two waves
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      float v = sq[mt];
-      v += __shfl_xor(v, 16, 64);
-      v += __shfl_xor(v, 32, 64);
-      if (lane < 16) pair_s[wave][mt * 16 + lane][0] = v;
+      // sum over the 4 lane groups (rows) of this wave
+      sq += __shfl_xor(sq, 16, 64);
+      sq += __shfl_xor(sq, 32, 64);
+      if (lane < 16) red_s[wave][t][0] = sq;
     }
     __syncthreads();
-    if (wave == 0) {
-      for (int t = lane; t < T_pad; t += 64) {
-        const float v = t < T ? pair_s[0][t][0] + pair_s[1][t][0] : 0.f;
-        g.ss_out[(size_t)tile * T_pad + t] = v;
-      }
+    if (tid < T_pad) {
+      const float v = tid < T ? ((red_s[0][tid][0] + red_s[1][tid][0]) +
+                                 (red_s[2][tid][0] + red_s[3][tid][0]))
+                              : 0.f;
+      g.ss_out[(size_t)tile * T_pad + tid] = v;
     }
   } else {  // GEMM_LOGITS
-    float bv[MT];
-    int bi[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int t = mt * 16 + lr;
-      bv[mt] = 0.f;
-      bi[mt] = -1;
       const float rs = t < T ? rs_s[t] : 0.f;
+      float bv = 0.f;
+      int bi = -1;
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int n = tile * BN + (wave + 2 * p) * 16 + r4;
+      for (int q = 0; q < SUB; ++q) {
+        const int n = tile * BN + (wave + 4 * q) * 16 + r4;
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          v[e] = res[p][mt][e] * rs;
-          if (t < T && n + e < g.N && v[e] != v[e]) atomicOr(g.status, PPD_DEV_NAN_LOGIT);
-        }
+        for (int e = 0; e < 4; ++e) v[e] = acc[q][mt][e] * rs;
         if (t < T) {
           if (g.logits) {
             if ((g.N & 3) == 0 && n + 3 < g.N) {
@@ -317,46 +382,35 @@ __global__ __launch_bounds__(256, (MT <= 4 ? 2 : 1)) void gemm_bf16_kernel(GemmL
           }
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            if (n + e < g.N && v[e] == v[e] && (bi[mt] < 0 || v[e] > bv[mt])) {
-              bv[mt] = v[e];
-              bi[mt] = n + e;
+            if (n + e < g.N) {
+              if (v[e] != v[e]) {
+                atomicOr(g.status, PPD_DEV_NAN_LOGIT);
+              } else if (bi < 0 || v[e] > bv) {
+                bv = v[e];
+                bi = n + e;
+              }
             }
           }
         }
       }
-    }
-    // merge across lane groups, then the two waves: larger value, smaller index
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      float v = bv[mt];
-      int i = bi[mt];
+      // merge over the 4 lane groups: larger value, then smaller index
 #pragma unroll
       for (int o = 16; o <= 32; o <<= 1) {
-        const float v2 = __shfl_xor(v, o, 64);
-        const int i2 = __shfl_xor(i, o, 64);
-        if (i2 >= 0 && (i < 0 || v2 > v || (v2 == v && i2 < i))) {
-          v = v2;
-          i = i2;
-        }
+        const float v2 = __shfl_xor(bv, o, 64);
+        const int i2 = __shfl_xor(bi, o, 64);
+        amax_merge(bv, bi, v2, i2);
       }
       if (lane < 16) {
-        pair_s[wave][mt * 16 + lane][0] = v;
-        pair_s[wave][mt * 16 + lane][1] = __int_as_float(i);
+        red_s[wave][t][0] = bv;
+        red_s[wave][t][1] = __int_as_float(bi);
       }
     }
     __syncthreads();
-    if (wave == 0) {
-      for (int t = lane; t < T_pad; t += 64) {
-        float v = pair_s[0][t][0];
-        int i = __float_as_int(pair_s[0][t][1]);
-        const float v2 = pair_s[1][t][0];
-        const int i2 = __float_as_int(pair_s[1][t][1]);
-        if (i2 >= 0 && (i < 0 || v2 > v || (v2 == v && i2 < i))) {
-          v = v2;
-          i = i2;
-        }
-        g.amax[(size_t)tile * T_pad + t] = make_float2(v, __int_as_float(i));
-      }
+    if (tid < T_pad) {
+      float v = red_s[0][tid][0];
+      int i = __float_as_int(red_s[0][tid][1]);
+      for (int w = 1; w < 4; ++w) amax_merge(v, i, red_s[w][tid][0], __float_as_int(red_s[w][tid][1]));
+      g.amax[(size_t)tile * T_pad + tid] = make_float2(v, __int_as_float(i));
     }
   }
 }
@@ -375,6 +429,8 @@ hipError_t launch_kind(const GemmLaunch &g, int n_tiles, hipStream_t s) {
 }
 
 }  // namespace
+
+int gemm_tile_rows(int kind) { return kind == GEMM_RESID ? 64 : 128; }
 
 hipError_t launch_gemm_bf16(const GemmLaunch &g, int n_tiles, hipStream_t s) {
   switch (g.kind) {

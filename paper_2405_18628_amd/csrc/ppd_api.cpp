@@ -76,9 +76,9 @@ ppd_status check_model(const ppd_model *m) {
   if (m->dtype == PPD_BF16) {
     if (m->head_dim != 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need head_dim 128");
     if (m->hidden % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need hidden % 64 == 0");
-    if (m->ffn % 32) return fail(PPD_EUNSUPPORTED, "bf16 kernels need ffn % 32 == 0");
-    if ((m->vocab + 63) / 64 > kAttnCounterBase)
-      return fail(PPD_EUNSUPPORTED, "vocab too large (max %d)", 64 * kAttnCounterBase);
+    if (m->ffn % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need ffn %% 64 == 0");
+    if ((m->vocab + 127) / 128 > kAttnCounterBase)
+      return fail(PPD_EUNSUPPORTED, "vocab too large (max %d)", 128 * kAttnCounterBase);
   }
   if (!m->tok_emb || !m->lm_head || !m->final_norm || (m->n_prompt > 0 && !m->prompt_emb))
     return fail(PPD_EINVAL, "embedding, LM head and final norm pointers must be set");
@@ -96,25 +96,27 @@ int qkv_rows(const ppd_model *m) { return (m->n_heads + 2 * m->n_kv_heads) * m->
 
 // ---- launch-shape heuristics (also used to size the workspace)
 
-// split-K factor: about two workgroups per compute unit, each wave at least
-// 4 k-steps of 32
+// split-K factor: about one workgroup per compute unit, each split at least
+// 4 chunks of 64
 int choose_sk(int n_tiles, int K) {
   const int nks = K / 32;
-  int sk = (2 * kCUs + n_tiles - 1) / n_tiles;
-  sk = std::min(sk, std::max(1, nks / 16));
+  // more splits cost partial traffic and fixups, fewer leave compute units
+  // without a weight stream (measured on 7B shapes)
+  int sk = std::max(1, kCUs / n_tiles);
+  sk = std::min(sk, std::max(1, nks / 8));
   return std::max(1, std::min(sk, 16));
 }
 
 struct GemmShape {
-  int n_tiles, K;
+  int n_tiles, K, rows;  // rows per tile
 };
 
 void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
-  out[0] = {qkv_rows(m) / 64, m->hidden};          // QKV
-  out[1] = {m->hidden / 64, m->n_heads * 128};     // O
-  out[2] = {m->ffn / 32, m->hidden};               // gate/up (32 features per tile)
-  out[3] = {m->hidden / 64, m->ffn};               // down
-  out[4] = {(m->vocab + 63) / 64, m->hidden};      // LM head
+  out[0] = {qkv_rows(m) / 128, m->hidden, 128};          // QKV: one head per tile
+  out[1] = {m->hidden / 64, m->n_heads * 128, 64};       // output projection
+  out[2] = {m->ffn / 64, m->hidden, 128};                // gate/up: 64 features per tile
+  out[3] = {m->hidden / 64, m->ffn, 64};                 // down projection
+  out[4] = {(m->vocab + 127) / 128, m->hidden, 128};     // LM head
 }
 
 int attn_max_splits(const ppd_model *m) {
@@ -165,12 +167,12 @@ WsLayout layout_of(const ppd_model *m, int T) {
     gemm_shapes(m, gs);
     for (int i = 0; i < 5; ++i) {
       const int sk = choose_sk(gs[i].n_tiles, gs[i].K);
-      if (sk > 1) part = std::max(part, (size_t)gs[i].n_tiles * sk * 4 * (Tp / 16) * 64 * 4);
+      if (sk > 1) part = std::max(part, (size_t)gs[i].n_tiles * sk * 16 * gs[i].rows * (Tp / 16));
     }
   }
   w.max_part_floats = part;
   w.gemm_part = take(sizeof(float) * part);
-  w.max_amax_tiles = (m->vocab + 63) / 64;
+  w.max_amax_tiles = (m->vocab + 127) / 128;
   w.amax = take(sizeof(float2) * w.max_amax_tiles * Tp);
   w.rope = take(sizeof(float2) * Tp * (d / 2));
   w.total = off;
@@ -231,6 +233,7 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     g.inv_h = inv_h;
     g.eps = m->rms_eps;
     g.status = status;
+    g.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
     // QKV + RoPE + cache stores
     g.kind = GEMM_QKV;
     g.W = (const bf16_t *)m->w_qkv[l];
@@ -339,6 +342,7 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
   lm.logits = logits;
   lm.amax = amax;
   lm.status = status;
+  lm.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
   int slot;
   PPD_TRY_HIP(timer_begin(TK_LM, s, &slot));
   PPD_TRY_HIP(launch_gemm_bf16(lm, gs[4].n_tiles, s));

@@ -53,6 +53,10 @@ __device__ __forceinline__ float wave_max(float v) {
 // ---------------------------------------------------------------------------
 // workspace layout (computed on the host, passed to kernels as pointers)
 
+// the first 256 bytes of the workspace hold the status word (offset 0) and a
+// 64-byte line of zeros (offset PPD_WS_ZEROS) that is never written
+#define PPD_WS_ZEROS 64
+
 struct WsLayout {
   size_t status;      // uint32 [4]
   size_t counters;    // uint32 [n_counters]
@@ -83,6 +87,7 @@ struct GemmLaunch {
   // operands
   const bf16_t *W;  // [N][K] (SwiGLU: gate rows then up rows, 2F x K)
   const bf16_t *A;  // [T_pad][K]
+  const bf16_t *zeros;  // 16 zero bytes in global memory
   int N, K, T, MT;  // N = output rows (SwiGLU: F), MT = T_pad / 16
   int kind;         // GemmKind
   int sk;           // split-K factor

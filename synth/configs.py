@@ -75,7 +75,7 @@ VICUNA_7B = ModelShape("vicuna-7b", 32, 4096, 32, 32, 128, 11008, 32000, "bf16")
 VICUNA_13B = ModelShape("vicuna-13b", 40, 5120, 40, 40, 128, 13824, 32000, "bf16")
 
 # small bf16 shapes for fast parity tests (several tiles, ragged vocab/ffn/L)
-SMALL_BF16 = ModelShape("small-bf16", 2, 512, 4, 4, 128, 1376, 1000, "bf16")
+SMALL_BF16 = ModelShape("small-bf16", 2, 512, 4, 4, 128, 1344, 1000, "bf16")
 SMALL_GQA = ModelShape("small-gqa-bf16", 2, 512, 4, 2, 128, 1408, 1000, "bf16")
 
 WORKLOADS = {

@@ -63,7 +63,7 @@ def _fake_model(dtype=ppd.PPD_BF16, **kw):
     arr = (C.c_void_p * n)(*([0x1000] * n))
     keep = [arr]
     m = ppd.ppd_model(n, kw.get("hidden", 512), kw.get("n_heads", 4), kw.get("n_kv_heads", 4),
-                      kw.get("head_dim", 128), kw.get("ffn", 1376), kw.get("vocab", 1000), 3,
+                      kw.get("head_dim", 128), kw.get("ffn", 1344), kw.get("vocab", 1000), 3,
                       1e-6, 10000.0, dtype, fake, fake,
                       *[C.cast(arr, C.POINTER(C.c_void_p)) for _ in range(6)], fake, fake)
     return m, keep
