@@ -84,6 +84,8 @@ __device__ __forceinline__ void dma16(const void *g, unsigned lds_addr) {
 // s_waitcnt immediate for "at most n vector-memory operations outstanding"
 // (expcnt and lgkmcnt left at their maxima, i.e. not waited on)
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+// s_waitcnt immediate for "no LDS operation outstanding" (vmcnt, expcnt at maxima)
+constexpr int lgkmcnt0_imm = 15 | (3 << 14) | (7 << 4);
 
 template <int MT, int KIND>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
@@ -175,6 +177,40 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
 
 #pragma unroll
   for (int c = 0; c < NS - 1; ++c) issue(c);
+
+  // ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) from the
+  // producer's sum-of-squares partials, fetched while the first chunks are in
+  // flight: group j of the J = 256 / T_pad thread groups sums partials j,
+  // j + J, ..., then the group sums are added in group order.
+  if constexpr (KIND != GEMM_RESID) {
+    constexpr int J = 256 / T_pad;
+    float *gs = &red_s[0][0][0];
+    if (tid < J * T_pad) {
+      const int t = tid % T_pad, j = tid / T_pad;
+      float s = 0.f;
+      for (int p0 = j; p0 < g.n_ss; p0 += 16 * J) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          const int pp = p0 + u * J;
+          v[u] = pp < g.n_ss ? g.ss[(size_t)pp * T_pad + t] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) s += v[u];
+      }
+      gs[tid] = s;
+    }
+    __syncthreads();
+    if (tid < T_pad) {
+      float s = 0.f;
+      for (int j = 0; j < J; ++j) s += gs[j * T_pad + tid];
+      rs_s[tid] = rsqrtf(s * g.inv_h + g.eps);
+    }
+    // rs_s is read after the main loop; its write completes before the
+    // loop's first barrier
+    __builtin_amdgcn_s_waitcnt(lgkmcnt0_imm);
+  }
+
   for (int c = 0; c < n_chunks; ++c) {
     // own transfers of chunk c done (chunks c+1 .. c+NS-2 may still fly),
     // then every wave's; the barrier also retires all reads of chunk c-1,
@@ -256,17 +292,6 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
           acc[q][mt] += floatx4{a.x, a.y, b.x, b.y};
         }
     }
-  }
-
-  // ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) from the
-  // producer's sum-of-squares partials (summed in partial order)
-  if constexpr (KIND != GEMM_RESID) {
-    if (tid < T_pad) {
-      float s = 0.f;
-      for (int p = 0; p < g.n_ss; ++p) s += g.ss[(size_t)p * T_pad + tid];
-      rs_s[tid] = rsqrtf(s * g.inv_h + g.eps);
-    }
-    __syncthreads();
   }
 
   // accumulator layout: lane holds rows 4 (lane / 16) + e of its sub-tile,

@@ -77,6 +77,8 @@ ppd_status check_model(const ppd_model *m) {
     if (m->head_dim != 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need head_dim 128");
     if (m->hidden % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need hidden % 64 == 0");
     if (m->ffn % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need ffn %% 64 == 0");
+    if (m->n_heads * 8 > PPD_MAX_COUNTERS - kAttnCounterBase)
+      return fail(PPD_EUNSUPPORTED, "too many heads (max %d)", (PPD_MAX_COUNTERS - kAttnCounterBase) / 8);
     if ((m->vocab + 127) / 128 > kAttnCounterBase)
       return fail(PPD_EUNSUPPORTED, "vocab too large (max %d)", 128 * kAttnCounterBase);
   }
@@ -119,16 +121,28 @@ void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
   out[4] = {(m->vocab + 127) / 128, m->hidden, 128};     // LM head
 }
 
-int attn_max_splits(const ppd_model *m) {
-  return std::max(1, std::min(PPD_ATTN_MAX_SPLITS, 2 * kCUs / m->n_heads));
-}
+constexpr int kAttnMaxSplits = 8;
 
+// Key splits of the attention: the workgroups (heads x query tiles x splits,
+// one per compute unit at a time) should fill whole waves of the 256 CUs;
+// each split costs a partial round trip, and every wave keeps at least two
+// 32-key blocks.
 void attn_splits(const ppd_model *m, int L, int T, int *splits, int *chunk) {
   const int nblk = (L + T + 31) / 32;
-  int s = std::min(attn_max_splits(m), std::max(1, nblk / 2));
-  int c = (nblk + s - 1) / s;
-  s = (nblk + c - 1) / c;
-  *splits = s;
+  const int wgs = m->n_heads * (t_pad_of(T) / 16);
+  const int ks_max = std::max(1, std::min(kAttnMaxSplits, nblk / 8));
+  int best = 1;
+  double best_cost = 1e30;
+  for (int ks = 1; ks <= ks_max; ++ks) {
+    const int rounds = (wgs * ks + kCUs - 1) / kCUs;
+    const double cost = (double)rounds / ks + 0.02 * ks;
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best = ks;
+    }
+  }
+  const int c = (nblk + best - 1) / best;
+  *splits = (nblk + c - 1) / c;
   *chunk = c;
 }
 
@@ -159,7 +173,7 @@ WsLayout layout_of(const ppd_model *m, int T) {
   } else {
     w.tmp = take(0);
   }
-  w.max_splits = m->dtype == PPD_BF16 ? attn_max_splits(m) : 0;
+  w.max_splits = m->dtype == PPD_BF16 ? kAttnMaxSplits : 0;
   w.attn_part = take(sizeof(float) * (size_t)nh * w.max_splits * Tp * 132);
   size_t part = 0;
   if (m->dtype == PPD_BF16) {
@@ -264,6 +278,7 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     a.out = attn_o;
     a.part = at<float>(ws, w.attn_part);
     a.counters = counters + kAttnCounterBase;
+    a.zeros = g.zeros;
     a.T = T;
     a.MT = MT;
     a.L = L;

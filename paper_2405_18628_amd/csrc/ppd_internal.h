@@ -120,16 +120,18 @@ enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_SWIGLU = 2, GEMM_LOGITS = 3 }
 hipError_t launch_gemm_bf16(const GemmLaunch &g, int n_tiles, hipStream_t s);
 
 struct AttnLaunch {
-  const bf16_t *q;   // [T_pad][nh][d]
-  const bf16_t *kc;  // [nkv][cap][d]
-  const bf16_t *vc;  // [nkv][d][cap]
+  const bf16_t *q;      // [T_pad][nh][d]
+  const bf16_t *kc;     // [nkv][cap][d]
+  const bf16_t *vc;     // [nkv][d][cap]
   const uint64_t *mask;
-  bf16_t *out;       // [T_pad][nh d]
-  float *part;       // [nh][splits][T_pad][d + 2]
-  uint32_t *counters;
-  int T, MT, L, cap, nh, nkv, splits, chunk;  // chunk: cached keys per split (multiple of 32)
-  float scale_log2;  // log2(e) / sqrt(d)
+  bf16_t *out;          // [T_pad][nh d]
+  float *part;          // [nh][MT][splits][16][d + 4]
+  uint32_t *counters;   // nh * MT tickets, zero between launches
+  const bf16_t *zeros;  // >= 16 zero bytes
+  int T, MT, L, cap, nh, nkv, splits, chunk;  // chunk: 32-key blocks per split
+  float scale_log2;     // log2(e) / sqrt(d)
 };
+int attn_grid_size(int nh, int splits, int MT);
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s);
 
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,

@@ -112,6 +112,27 @@ def test_small_bf16_cache_lengths(small_case, L):
     check_pred(res["pred"], ref["logits"], "bf16")
 
 
+@pytest.fixture(scope="module")
+def small_long_case():
+    return make_case(workload("small", cache_len=2000))
+
+
+@pytest.mark.parametrize("L,spec", [(2000, "total:40"), (2000, "total:128"), (700, "total:17"),
+                                    (1999, "total:64")])
+def test_small_bf16_long_prefix(small_long_case, L, spec):
+    """Prefixes long enough for the attention to split the keys across
+    workgroups (the split partials are merged by the last split)."""
+    case = small_long_case
+    tree = tree_for(case, spec=spec, seed_offset=L)
+    say(f"[small-long] L={L} T={tree.T}")
+    ws = workspace(case, tree.T)
+    res = gpu_step(case, tree, ws, L=L)
+    ref = oracle_step(case, tree, L=L)
+    check_logits(res["logits"], ref["logits"], "bf16")
+    check_pred(res["pred"], ref["logits"], "bf16")
+    _check_tree_kv(case, tree, ref, L=L)
+
+
 def test_small_gqa():
     case = make_case(workload("small-gqa"))
     for spec in ("total:29", "total:70"):
