@@ -179,10 +179,10 @@ ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
 
 /*
  * Profiling aid, not needed for correctness.  While set, every
- * ppd_verify_step issued from this thread records start_events[i] before and
- * stop_events[i] after the i-th launch of kernel `kind` in the step (i <
- * n_events), on the step's stream, so a caller can time one kernel of the
- * step with HIP events.  kind: 0 QKV GEMM, 1 tree attention, 2 output
+ * ppd_verify_step issued from this thread launches the i-th kernel of kind
+ * `kind` in the step (i < n_events) with start_events[i] / stop_events[i]
+ * attached to the dispatch itself (hipExtLaunchKernelGGL), so they take the
+ * kernel's own start and end times on the step's stream.  kind: 0 QKV GEMM, 1 tree attention, 2 output
  * projection, 3 gate/up GEMM, 4 down projection, 5 LM head.  The arrays are
  * host arrays of hipEvent_t and must stay valid while set; n_events = 0
  * disables.  Thread-local setting.

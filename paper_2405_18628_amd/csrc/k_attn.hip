@@ -343,6 +343,10 @@ int attn_grid_size(int nh, int splits, int MT) { return ((nh * splits + 7) / 8) 
 
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
   dim3 grid(attn_grid_size(a.nh, a.splits, a.MT)), block(256);
-  hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, a);
+  if (a.ev_start)
+    hipExtLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, (hipEvent_t)a.ev_start,
+                          (hipEvent_t)a.ev_stop, 0, a);
+  else
+    hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, a);
   return hipGetLastError();
 }

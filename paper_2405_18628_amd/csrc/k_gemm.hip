@@ -175,8 +175,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
     }
   };
 
-#pragma unroll
-  for (int c = 0; c < NS - 1; ++c) issue(c);
+  for (int c = 0; c < NS - 1 && c < n_chunks; ++c) issue(c);
 
   // ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) from the
   // producer's sum-of-squares partials, fetched while the first chunks are in
@@ -193,7 +192,8 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
           const int pp = p0 + u * J;
-          v[u] = pp < g.n_ss ? g.ss[(size_t)pp * T_pad + t] : 0.f;
+          const float x = g.ss[(size_t)(pp < g.n_ss ? pp : 0) * T_pad + t];  // a valid row
+          v[u] = pp < g.n_ss ? x : 0.f;
         }
 #pragma unroll
         for (int u = 0; u < 16; ++u) s += v[u];
@@ -211,14 +211,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
     __builtin_amdgcn_s_waitcnt(lgkmcnt0_imm);
   }
 
-  for (int c = 0; c < n_chunks; ++c) {
-    // own transfers of chunk c done (chunks c+1 .. c+NS-2 may still fly),
-    // then every wave's; the barrier also retires all reads of chunk c-1,
-    // whose slot the next request overwrites.  (A bare s_barrier: a fence
-    // would wait for every transfer in flight.)
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPC));
-    asm volatile("s_barrier" ::: "memory");
-    issue(c + NS - 1);
+  auto compute = [&](int c) {
     const unsigned char *wl = lds + (c % NS) * SLOT;
     const unsigned char *al = wl + BN * 128;
 #pragma unroll
@@ -240,8 +233,47 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
         for (int mt = 0; mt < MT; ++mt)
           acc[q][mt] = mfma16x16x32(as_bf16x8(wf[q]), as_bf16x8(af[mt]), acc[q][mt]);
     }
+  };
+
+  // Steady state: each iteration requests the chunk NS-1 ahead.
+  const int n_main = n_chunks - (NS - 1);
+  for (int c = 0; c < n_main; ++c) {
+    // own transfers of chunk c done (chunks c+1 .. c+NS-2 may still fly),
+    // then every wave's; the barrier also retires all reads of chunk c-1,
+    // whose slot the next request overwrites.  (A bare s_barrier: a fence
+    // would wait for every transfer in flight.)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPC));
+    asm volatile("s_barrier" ::: "memory");
+    issue(c + NS - 1);
+    compute(c);
   }
+
+  // Epilogue operands, requested now so that their latency overlaps the
+  // last chunks' (RoPE factors for QKV; residual stream and next norm gain
+  // for the residual projections).
+  const int r4 = (lane >> 4) * 4;  // accumulator rows 4 (lane / 16) + e
+  [[maybe_unused]] floatx4 rope_r[MT][2];
+  [[maybe_unused]] floatx4 x_r[MT];
+  [[maybe_unused]] uint2 gain_r;
+  if constexpr (KIND == GEMM_QKV) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)(mt * 16 + lr) * 64 + wave * 16 + r4);
+      rope_r[mt][0] = rp[0];
+      rope_r[mt][1] = rp[1];
+    }
+  } else if constexpr (KIND == GEMM_RESID) {
+    const int n = tile * 64 + wave * 16 + r4;
+    gain_r = *(const uint2 *)(g.gain + n);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) x_r[mt] = *(const floatx4 *)(g.x + (size_t)(mt * 16 + lr) * g.N + n);
+  }
+
+  // Tail: the last chunks are all requested already; wait for them once
+  // (no padding transfers whose latency every workgroup would wait out).
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  asm volatile("s_barrier" ::: "memory");
+  for (int c = n_main > 0 ? n_main : 0; c < n_chunks; ++c) compute(c);
 
   // ---- split-K: publish the partial tile; the last workgroup sums all.
   // Partials are written and read with agent-scope relaxed atomics (coherent
@@ -278,25 +310,39 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
     for (int q = 0; q < SUB; ++q)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < g.sk; ++s) {
-      const uint64_t *src = (const uint64_t *)g.part + (size_t)(tile * g.sk + s) * tile_u64;
+    // U splits' partials are requested together, then added in split order
+    constexpr int U = SUB * MT <= 4 ? 4 : (SUB * MT <= 8 ? 2 : 1);
+    for (int s0 = 0; s0 < g.sk; s0 += U) {
+      float2 buf[U][SUB][MT][2];
 #pragma unroll
-      for (int q = 0; q < SUB; ++q)
+      for (int u = 0; u < U; ++u) {
+        const int s = s0 + u < g.sk ? s0 + u : s0;
+        const uint64_t *src = (const uint64_t *)g.part + (size_t)(tile * g.sk + s) * tile_u64;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const size_t o = (size_t)(((wave * SUB + q) * MT + mt) * 64 + lane) * 2;
-          const float2 a = __builtin_bit_cast(
-              float2, __hip_atomic_load(src + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-          const float2 b = __builtin_bit_cast(
-              float2, __hip_atomic_load(src + o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-          acc[q][mt] += floatx4{a.x, a.y, b.x, b.y};
-        }
+        for (int q = 0; q < SUB; ++q)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const size_t o = (size_t)(((wave * SUB + q) * MT + mt) * 64 + lane) * 2;
+            buf[u][q][mt][0] = __builtin_bit_cast(
+                float2, __hip_atomic_load(src + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+            buf[u][q][mt][1] = __builtin_bit_cast(
+                float2, __hip_atomic_load(src + o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+          }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (s0 + u < g.sk)
+#pragma unroll
+          for (int q = 0; q < SUB; ++q)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[q][mt] += floatx4{buf[u][q][mt][0].x, buf[u][q][mt][0].y, buf[u][q][mt][1].x,
+                                    buf[u][q][mt][1].y};
     }
   }
 
   // accumulator layout: lane holds rows 4 (lane / 16) + e of its sub-tile,
   // token column lane % 16 of token tile mt
-  const int r4 = (lane >> 4) * 4;
   const int T = g.T;
 
   if constexpr (KIND == GEMM_QKV) {
@@ -315,9 +361,11 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
         hi[e] = acc[1][mt][e] * rs;
       }
       if (hp < nh + nkv) {
+        const float cs_all[8] = {rope_r[mt][0][0], rope_r[mt][0][1], rope_r[mt][0][2], rope_r[mt][0][3],
+                                 rope_r[mt][1][0], rope_r[mt][1][1], rope_r[mt][1][2], rope_r[mt][1][3]};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float2 cs = g.rope[(size_t)t * 64 + i0 + e];
+          const float2 cs = float2{cs_all[2 * e], cs_all[2 * e + 1]};
           const float a = lo[e], b = hi[e];
           lo[e] = a * cs.x - b * cs.y;
           hi[e] = b * cs.x + a * cs.y;
@@ -355,7 +403,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
     }
   } else if constexpr (KIND == GEMM_RESID) {
     const int n = tile * 64 + wave * 16 + r4;
-    const uint2 gw = *(const uint2 *)(g.gain + n);
+    const uint2 gw = gain_r;
     const float g0 = bf16_to_f32(gw.x & 0xffff), g1 = bf16_to_f32(gw.x >> 16);
     const float g2 = bf16_to_f32(gw.y & 0xffff), g3 = bf16_to_f32(gw.y >> 16);
 #pragma unroll
@@ -364,7 +412,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
       float sq = 0.f;
       if (t < T) {
         float *xp = g.x + (size_t)t * g.N + n;
-        floatx4 xv = *(floatx4 *)xp;
+        floatx4 xv = x_r[mt];
         xv += acc[0][mt];
         *(floatx4 *)xp = xv;
         *(u32x2 *)(g.xg + (size_t)t * g.N + n) =
@@ -445,7 +493,13 @@ hipError_t launch_kind(const GemmLaunch &g, int n_tiles, hipStream_t s) {
   dim3 grid(n_tiles * g.sk), block(256);
   switch (g.MT) {
 #define PPD_CASE(M) \
-  case M: hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND>), grid, block, 0, s, g); break;
+  case M:                                                                                   \
+    if (g.ev_start)                                                                         \
+      hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND>), grid, block, 0, s,                 \
+                            (hipEvent_t)g.ev_start, (hipEvent_t)g.ev_stop, 0, g);           \
+    else                                                                                    \
+      hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND>), grid, block, 0, s, g);                \
+    break;
     PPD_CASE(1) PPD_CASE(2) PPD_CASE(3) PPD_CASE(4) PPD_CASE(5) PPD_CASE(6) PPD_CASE(7) PPD_CASE(8)
 #undef PPD_CASE
     default: return hipErrorInvalidValue;

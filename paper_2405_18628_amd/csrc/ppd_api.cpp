@@ -28,15 +28,15 @@ thread_local KernelTimer g_timer;
 
 enum TimedKind { TK_QKV = 0, TK_ATTN = 1, TK_O = 2, TK_GATEUP = 3, TK_DOWN = 4, TK_LM = 5 };
 
-hipError_t timer_begin(int kind, hipStream_t s, int *slot) {
-  *slot = -1;
-  if (g_timer.kind != kind || g_timer.next >= g_timer.n) return hipSuccess;
-  *slot = g_timer.next++;
-  return hipEventRecord((hipEvent_t)g_timer.start[*slot], s);
-}
-hipError_t timer_end(int slot, hipStream_t s) {
-  if (slot < 0) return hipSuccess;
-  return hipEventRecord((hipEvent_t)g_timer.stop[slot], s);
+// Events of the next timed launch of `kind` (both null when not timed).  The
+// kernel is then launched with hipExtLaunchKernelGGL, which records them at
+// the dispatch's own start and end, so they measure the kernel alone.
+void timer_events(int kind, void **start, void **stop) {
+  *start = *stop = nullptr;
+  if (g_timer.kind != kind || g_timer.next >= g_timer.n) return;
+  *start = g_timer.start[g_timer.next];
+  *stop = g_timer.stop[g_timer.next];
+  ++g_timer.next;
 }
 
 ppd_status fail(ppd_status s, const char *fmt, ...) {
@@ -265,10 +265,8 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     g.nkv = nkv;
     g.cap = cap;
     g.L = L;
-    int slot;
-    PPD_TRY_HIP(timer_begin(TK_QKV, s, &slot));
+    timer_events(TK_QKV, &g.ev_start, &g.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(g, gs[0].n_tiles, s));
-    PPD_TRY_HIP(timer_end(slot, s));
     // tree attention
     AttnLaunch a{};
     a.q = q;
@@ -288,9 +286,8 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     a.splits = splits;
     a.chunk = chunk;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt(128.0));
-    PPD_TRY_HIP(timer_begin(TK_ATTN, s, &slot));
+    timer_events(TK_ATTN, &a.ev_start, &a.ev_stop);
     PPD_TRY_HIP(launch_attn_bf16(a, s));
-    PPD_TRY_HIP(timer_end(slot, s));
     // O projection + residual; operand of the MLP norm
     GemmLaunch o = g;
     o.kind = GEMM_RESID;
@@ -303,9 +300,8 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     o.xg = xg;
     o.gain = (const bf16_t *)m->mlp_norm[l];
     o.ss_out = ss;
-    PPD_TRY_HIP(timer_begin(TK_O, s, &slot));
+    timer_events(TK_O, &o.ev_start, &o.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(o, gs[1].n_tiles, s));
-    PPD_TRY_HIP(timer_end(slot, s));
     n_ss = gs[1].n_tiles;
     // gate/up + SwiGLU
     GemmLaunch u = g;
@@ -318,9 +314,8 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     u.ss = ss;
     u.n_ss = n_ss;
     u.act = act;
-    PPD_TRY_HIP(timer_begin(TK_GATEUP, s, &slot));
+    timer_events(TK_GATEUP, &u.ev_start, &u.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(u, gs[2].n_tiles, s));
-    PPD_TRY_HIP(timer_end(slot, s));
     // down projection + residual; operand of the next norm
     GemmLaunch dn = g;
     dn.kind = GEMM_RESID;
@@ -333,9 +328,8 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     dn.xg = xg;
     dn.gain = (const bf16_t *)(l + 1 < m->n_layers ? m->attn_norm[l + 1] : m->final_norm);
     dn.ss_out = ss;
-    PPD_TRY_HIP(timer_begin(TK_DOWN, s, &slot));
+    timer_events(TK_DOWN, &dn.ev_start, &dn.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(dn, gs[3].n_tiles, s));
-    PPD_TRY_HIP(timer_end(slot, s));
     n_ss = gs[3].n_tiles;
   }
   // final norm + LM head + greedy partials
@@ -358,10 +352,8 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
   lm.amax = amax;
   lm.status = status;
   lm.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
-  int slot;
-  PPD_TRY_HIP(timer_begin(TK_LM, s, &slot));
+  timer_events(TK_LM, &lm.ev_start, &lm.ev_stop);
   PPD_TRY_HIP(launch_gemm_bf16(lm, gs[4].n_tiles, s));
-  PPD_TRY_HIP(timer_end(slot, s));
   PPD_TRY_HIP(launch_argmax_final(amax, gs[4].n_tiles, T, Tp, pred, status, s));
   return PPD_OK;
 }

@@ -3,6 +3,7 @@
 // MFMA operand types, wavefront reductions.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -113,6 +114,7 @@ struct GemmLaunch {
   float *logits;       // [T][N] or null
   float2 *amax;        // [n_tiles][T_pad]
   uint32_t *status;
+  void *ev_start, *ev_stop;  // optional events at the dispatch's start / end
 };
 
 enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_SWIGLU = 2, GEMM_LOGITS = 3 };
@@ -130,6 +132,7 @@ struct AttnLaunch {
   const bf16_t *zeros;  // >= 16 zero bytes
   int T, MT, L, cap, nh, nkv, splits, chunk;  // chunk: 32-key blocks per split
   float scale_log2;     // log2(e) / sqrt(d)
+  void *ev_start, *ev_stop;  // optional events at the dispatch's start / end
 };
 int attn_grid_size(int nh, int splits, int MT);
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s);
