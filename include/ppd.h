@@ -14,7 +14,7 @@
  *   ppd_accept           device: exact-matching verification, longest
  *                        accepted root path, bonus token (Section 3)
  *   ppd_kv_compact       device: commit the accepted nodes' keys/values to
- *                        the single shared KV cache (Section 5.4)
+ *                        the single shared KV cache (Section 5.3)
  *
  * Conventions shared by every call
  * --------------------------------
@@ -167,7 +167,7 @@ ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids,
                       int32_t *next_tok, void *ws, size_t ws_bytes, void *stream);
 
 /*
- * Commit accepted keys/values (Section 5.4: one cache shared by guessing and
+ * Commit accepted keys/values (Section 5.3: one cache shared by guessing and
  * verification; prompt-token entries are never committed):
  * cache[L + k] <- cache[L + path[k]] for k < *n_path, every layer and kv head.
  * path, n_path: device (as written by ppd_accept).  L: host value used by the

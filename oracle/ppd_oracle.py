@@ -15,7 +15,7 @@ Plain, slow, float64 numpy.  Each function restates what the paper computes:
 * Section 4.1 (customised sparse tree attention, after SpecInfer): every node
   attends to the cached prefix, to its own ancestors and to itself, and to
   nothing else, so many candidates are scored without growing the batch.
-* Section 5.4 (memory): a single KV cache is shared by guessing and
+* Section 5.3 (memory efficiency): a single KV cache is shared by guessing and
   verification; only accepted tokens are committed to it.
 
 The decoder is Llama-style (the paper's MobileLLaMA / Vicuna family):

@@ -224,7 +224,7 @@ hipError_t launch_accept(int T, const int32_t *parent, const int32_t *ids, const
 }
 
 // ---------------------------------------------------------------------------
-// KV compaction (Section 5.4: one cache; only accepted tokens are committed):
+// KV compaction (Section 5.3: one cache; only accepted tokens are committed):
 // cache[L + k] <- cache[L + path[k]], k < n.  Sources are read into LDS before
 // any destination is written, so overlapping moves are safe.  One block per
 // (layer, kv head).
