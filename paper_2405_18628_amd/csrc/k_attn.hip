@@ -29,8 +29,8 @@
 //                                8 (m / 4) + 4 kt + (m % 4), so each lane's 8
 //                                probabilities are 8 consecutive keys, i.e. a
 //                                valid B operand.
-// Softmax runs in fp32 in the log2 domain; P is rounded to bf16 for the PV
-// product.
+// Softmax runs in fp32 in the log2 domain; P enters the PV product as the sum
+// of two bf16 parts (hi, lo), i.e. to about 16 significant bits.
 #include "ppd_internal.h"
 
 namespace {
@@ -225,13 +225,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
         psum += pv[e];
       }
       l_run = l_run * alpha + psum;
+      // P = hi + lo, both bf16: the PV product then carries P to ~16
+      // significant bits (two MFMAs per tile; the kernel is bound by HBM)
+      float plo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) plo[e] = pv[e] - bf16_to_f32(f32_to_bf16(pv[e]));
       const u32x4 pb = u32x4{pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
                              pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
+      const u32x4 pl = u32x4{pack_bf16x2(plo[0], plo[1]), pack_bf16x2(plo[2], plo[3]),
+                             pack_bf16x2(plo[4], plo[5]), pack_bf16x2(plo[6], plo[7])};
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
         const int r = dt * 16 + lr;
         const u32x4 va = *(const u32x4 *)(vs_l + r * 64 + ((lg ^ ((lr >> 2) & 3)) * 16));
         o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pb), o[dt] * alpha);
+        o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pl), o[dt]);
       }
     }
   }
@@ -266,14 +274,15 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
     acc1 += sc * *(const floatx4 *)(src + 4);
   }
   const int t = qt * 16 + tq;
-  bf16_t *dst = p.out + (size_t)t * p.nh * 128 + h * 128 + d8;
+  auto store_out = [&](floatx4 v0, floatx4 v1) {
+    bf16_t *dst = p.out + (size_t)t * p.nh * 128 + h * 128 + d8;
+    *(u32x4 *)dst = u32x4{pack_bf16x2(v0[0], v0[1]), pack_bf16x2(v0[2], v0[3]),
+                          pack_bf16x2(v1[0], v1[1]), pack_bf16x2(v1[2], v1[3])};
+  };
   if (KS == 1) {
     if (t < p.T) {
       const float inv = 1.f / lsum;
-      acc0 *= inv;
-      acc1 *= inv;
-      *(u32x4 *)dst = u32x4{pack_bf16x2(acc0[0], acc0[1]), pack_bf16x2(acc0[2], acc0[3]),
-                            pack_bf16x2(acc1[0], acc1[1]), pack_bf16x2(acc1[2], acc1[3])};
+      store_out(acc0 * inv, acc1 * inv);
     }
     return;
   }
@@ -331,10 +340,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
     acc1 += sc * floatx4{c.x, c.y, d.x, d.y};
   }
   const float inv = 1.f / lsum;
-  acc0 *= inv;
-  acc1 *= inv;
-  *(u32x4 *)dst = u32x4{pack_bf16x2(acc0[0], acc0[1]), pack_bf16x2(acc0[2], acc0[3]),
-                        pack_bf16x2(acc1[0], acc1[1]), pack_bf16x2(acc1[2], acc1[3])};
+  store_out(acc0 * inv, acc1 * inv);
 }
 
 }  // namespace
