@@ -37,29 +37,22 @@ namespace {
 
 constexpr int KSLOT = 8192;               // 32 keys x 256 bytes
 constexpr int VSLOT = 8192;               // 128 dims x 64 bytes (32 keys)
-constexpr int SLOT = KSLOT + VSLOT;       // one ring slot
-constexpr int QBYTES = 4096;              // 16 queries x 256 bytes
-constexpr int MBYTES = 1024;              // ancestor masks (16 x 16 bytes used)
-constexpr int WAVE_LDS = 2 * SLOT + QBYTES + MBYTES;
+constexpr int SLOT = KSLOT + VSLOT;       // one block in LDS
+constexpr int WAVE_LDS = SLOT;            // per wave (also holds its merge rows)
 constexpr int OROW = 132;                 // merge row: 128 dims + padding (floats)
+#ifndef PPD_ATTN_RING
+#define PPD_ATTN_RING 2
+#endif
+constexpr int RING = PPD_ATTN_RING;       // blocks in flight per wave (registers)
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-// One 16-byte-per-lane global -> LDS transfer: lane l's bytes land at LDS
-// byte lds_addr + 16 l.  Inline assembly, so that the compiler does not
-// track the LDS write (the kernel waits on vmcnt explicitly).
-__device__ __forceinline__ void dma16(const void *g, unsigned lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
-               : "memory", "m0");
+// LDS row of the K slot holding key j (j < 32) of a block: MFMA row m of key
+// tile kt holds key 8 (m / 4) + 4 kt + (m % 4)
+__device__ __forceinline__ int row_of_key(int j) {
+  const int a = j >> 3, kt = (j >> 2) & 1, e = j & 3;
+  return kt * 16 + a * 4 + e;
 }
 
-// key (within its 32-key block) held by LDS row R of the block's K slot
-__device__ __forceinline__ int key_of_row(int R) {
-  const int kt = R >> 4, m = R & 15;
-  return 8 * (m >> 2) + 4 * kt + (m & 3);
-}
-
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
+__global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnLaunch p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[4 * WAVE_LDS];
   __shared__ float ml_s[4][16][2];
   __shared__ int last_s;
@@ -80,64 +73,78 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
   const int nblk = (n_keys + 31) >> 5;
   const int b0 = min(nblk, ks * p.chunk), b1 = min(nblk, b0 + p.chunk);
   const int cpw = (b1 - b0 + 3) >> 2;
-  const int wb0 = min(b1, b0 + wave * cpw), wb1 = min(b1, wb0 + cpw);
+  const int wvs = __builtin_amdgcn_readfirstlane(wave);  // wave index as a scalar
+  const int wb0 = min(b1, b0 + wvs * cpw), wb1 = min(b1, wb0 + cpw);
   const int nw = wb1 - wb0;
   const bf16_t *kbase = p.kc + (size_t)kvh * p.cap * 128;
   const bf16_t *vbase = p.vc + (size_t)kvh * 128 * p.cap;
-  const bf16_t *zp = p.zeros;
-
-  const int wv = __builtin_amdgcn_readfirstlane(wave);
-  const unsigned wbase = (unsigned)(size_t)(lds_void_t *)lds + (unsigned)(wv * WAVE_LDS);
+  const u32x4 *zp = (const u32x4 *)p.zeros;
   unsigned char *wl = lds + wave * WAVE_LDS;
 
-  // ---- queries and masks of the tile -> this wave's LDS
-  {
+  // ---- this lane's queries (B operand) and ancestor masks
+  const int tq_l = qt * 16 + lr;
+  const bool qlive = tq_l < p.T;
+  u32x4 qf[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = 4 * i + (lane >> 4);
-      const int t = qt * 16 + row;
-      dma16(t < p.T ? (const void *)(p.q + ((size_t)t * p.nh + h) * 128 + (lane & 15) * 8) : zp,
-            wbase + 2 * SLOT + i * 1024);
-    }
-    const int t = qt * 16 + lane;
-    dma16(lane < 16 && t < p.T ? (const void *)(p.mask + 2 * t) : zp, wbase + 2 * SLOT + QBYTES);
-  }
+  for (int ds = 0; ds < 4; ++ds)
+    qf[ds] = *(qlive ? (const u32x4 *)(p.q + ((size_t)tq_l * p.nh + h) * 128 + ds * 32 + lg * 8) : zp);
+  const uint64_t mk0 = qlive ? p.mask[2 * tq_l] : 0ull;
+  const uint64_t mk1 = qlive ? p.mask[2 * tq_l + 1] : 0ull;
 
-  // ---- per-lane transfer offsets of a block (elements from the block start)
-  int koff[8], voff[8], vkey[8];
+  // ---- register ring.  A block is loaded with 16-byte non-temporal loads:
+  // K rows are contiguous (8 KB per block), lane + 64 i covers 16-byte chunk
+  // c of it (key c / 16, column c % 16); V^T chunk c is dim row c / 4, keys
+  // 8 (c % 4) .. + 7 of the block.
+  u32x4 kr[RING][8], vr[RING][8];
+  // Past its run a wave re-reads its last block (any in-bounds block does:
+  // the data is never staged), so every iteration issues the same loads.
+  const int b_last = wb1 > 0 ? wb1 - 1 : 0;
+  auto load = [&](int b, u32x4 (&kd)[8], u32x4 (&vd)[8]) {
+    const int bb = min(b, b_last);
+    const u32x4 *kb = (const u32x4 *)(kbase + (size_t)bb * 32 * 128);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) kd[i] = __builtin_nontemporal_load(kb + lane + 64 * i);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = lane + 64 * i;
+      vd[i] = __builtin_nontemporal_load(
+          (const u32x4 *)(vbase + (size_t)(c >> 2) * p.cap + bb * 32 + (c & 3) * 8));
+    }
+  };
+  // Block b -> this wave's LDS slot, swizzled (K: physical 16-byte column =
+  // logical ^ (row % 16); V^T: logical ^ ((row / 4) % 4)); keys past the
+  // last valid one are cleared (value groups; key rows are masked anyway)
+  // LDS byte offsets of this lane's chunks (the same for every block)
+  int kofs[8], vofs[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    // K: LDS row R = 4 i + lane / 16 (256 bytes), physical 16-byte column
-    // lane % 16 holds logical column c = phys ^ (R % 16)
-    const int R = 4 * i + (lane >> 4);
-    const int c = (lane & 15) ^ (R & 15);
-    koff[i] = key_of_row(R) * 128 + c * 8;
-    // V^T: LDS row r = 16 i + lane / 4 (64 bytes), physical column lane % 4
-    // holds logical column (8 keys) c = phys ^ ((r / 4) % 4)
-    const int r = 16 * i + (lane >> 2);
-    const int cv = (lane & 3) ^ ((r >> 2) & 3);
-    voff[i] = r * p.cap + cv * 8;
-    vkey[i] = cv * 8;
+    const int c = lane + 64 * i;
+    const int R = row_of_key(c >> 4);
+    kofs[i] = R * 256 + (((c & 15) ^ (R & 15)) * 16);
+    const int r = c >> 2, cv = c & 3;
+    vofs[i] = KSLOT + r * 64 + ((cv ^ ((r >> 2) & 3)) * 16);
   }
-  int kkey[8];
+  const int vkey = (lane & 3) * 8;  // first key of this lane's value chunks
+  auto stage = [&](int b, const u32x4 (&kd)[8], const u32x4 (&vd)[8]) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) kkey[i] = key_of_row(4 * i + (lane >> 4));
-
-  // Block b (of this wave's run; past the run: zero lines) -> ring slot s.
-  // Keys past the end read zeros, except the tail of a partly valid
-  // 8-key value group, which is cleared in LDS after arrival.
-  auto issue = [&](int b, int s) {
-    const bool in_run = b < wb1;
-    const int key0 = b * 32;
-    const unsigned slot = wbase + (unsigned)(s * SLOT);
+    for (int i = 0; i < 8; ++i) *(u32x4 *)(wl + kofs[i]) = kd[i];
+    const int nv = n_keys - b * 32;  // valid keys in this block (may exceed 32)
+    if (nv >= 32) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      dma16(in_run && key0 + kkey[i] < n_keys ? (const void *)(kbase + (size_t)key0 * 128 + koff[i]) : zp,
-            slot + i * 1024);
+      for (int i = 0; i < 8; ++i) *(u32x4 *)(wl + vofs[i]) = vd[i];
+    } else {
+      const int keep_n = nv - vkey;
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      dma16(in_run && key0 + vkey[i] < n_keys ? (const void *)(vbase + key0 + voff[i]) : zp,
-            slot + KSLOT + i * 1024);
+      for (int i = 0; i < 8; ++i) {
+        u32x4 v = vd[i];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t keep = (2 * w < keep_n ? 0xffffu : 0u) | (2 * w + 1 < keep_n ? 0xffff0000u : 0u);
+          v[w] &= keep;
+        }
+        *(u32x4 *)(wl + vofs[i]) = v;
+      }
+    }
   };
 
   floatx4 o[8];
@@ -145,43 +152,26 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
   for (int dt = 0; dt < 8; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  issue(wb0, 0);
-  issue(wb0 + 1, 1);
-  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");  // queries, masks, block 0
-
-  if (nw > 0) {
-    u32x4 qf[4];
 #pragma unroll
-    for (int ds = 0; ds < 4; ++ds) qf[ds] = *(const u32x4 *)(wl + 2 * SLOT + lr * 256 + (ds * 4 + lg) * 16);
-    const uint64_t mk0 = *(const uint64_t *)(wl + 2 * SLOT + QBYTES + lr * 16);
-    const uint64_t mk1 = *(const uint64_t *)(wl + 2 * SLOT + QBYTES + lr * 16 + 8);
+  for (int j = 0; j < RING; ++j) load(wb0 + j, kr[j], vr[j]);
+  __builtin_amdgcn_sched_barrier(0);
 
-    for (int i = 0; i < nw; ++i) {
-      if (i > 0) {
-        issue(wb0 + i + 1, (i + 1) & 1);  // into the slot block i-1 used
-        asm volatile("s_waitcnt vmcnt(16)" ::: "memory");  // block i arrived
-      }
-      const unsigned char *ks_l = wl + (i & 1) * SLOT;
-      const unsigned char *vs_l = ks_l + KSLOT;
+  for (int c0 = 0; c0 < nw; c0 += RING) {
+#pragma unroll
+    for (int j = 0; j < RING; ++j) {
+      const int i = c0 + j;
+      const bool live = i < nw;
+      // stage block i (its loads were issued RING blocks ago), then reuse
+      // the registers for block i + RING; the wave's own LDS operations run
+      // in order, so block i-1's reads precede these writes
+      if (live) stage(wb0 + i, kr[j], vr[j]);
+      __builtin_amdgcn_sched_barrier(0);
+      load(wb0 + i + RING, kr[j], vr[j]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (!live) continue;
+      const unsigned char *ks_l = wl;
+      const unsigned char *vs_l = wl + KSLOT;
       const int key0 = (wb0 + i) * 32;
-      const int nv = n_keys - key0;  // valid keys in this block (may exceed 32)
-      if (nv < 32 && (nv & 7)) {
-        // clear the invalid tail of the partly valid 8-key group, rows lane, lane + 64
-        const int c = nv >> 3;
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int r = lane + 64 * hh;
-          u32x4 *ptr = (u32x4 *)(wl + (i & 1) * SLOT + KSLOT + r * 64 + ((c ^ ((r >> 2) & 3)) * 16));
-          u32x4 v = *ptr;
-          const int keep_n = nv & 7;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const uint32_t keep = (2 * w < keep_n ? 0xffffu : 0u) | (2 * w + 1 < keep_n ? 0xffff0000u : 0u);
-            v[w] &= keep;
-          }
-          *ptr = v;
-        }
-      }
       // S^T for the two 16-key tiles
       floatx4 s[2];
 #pragma unroll
@@ -196,19 +186,38 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
       // scale, mask, block max: this lane holds keys key0 + 8 lg + 4 kt + e
       float sv[8];
       float bmax = -INFINITY;
+      if (key0 + 32 <= p.L) {
+        // the whole block is cached prefix: visible to every node
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int j = key0 + lg * 8 + kt * 4 + e;
-          const int jj = j - p.L;  // tree node index of key j (if j >= L)
+          for (int e = 0; e < 4; ++e) {
+            const float x = s[kt][e] * p.scale_log2;
+            sv[kt * 4 + e] = x;
+            bmax = fmaxf(bmax, x);
+          }
+      } else {
+        // this lane's 8 keys key0 + 8 lg .. + 7: visibility bits from the
+        // prefix bound and the ancestor mask (bit j - L for tree keys)
+        const int j0 = key0 + lg * 8;
+        uint32_t visb = 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int j = j0 + u;
+          const int jj = j - p.L;
           const uint64_t word = jj < 64 ? mk0 : mk1;
-          const int anc = (int)((word >> (jj & 63)) & 1ull);
-          const int vis = (j < p.L) | ((j < n_keys) & anc);
-          const float x = vis ? s[kt][e] * p.scale_log2 : -INFINITY;
-          sv[kt * 4 + e] = x;
-          bmax = fmaxf(bmax, x);
+          const uint32_t anc = (uint32_t)((word >> (jj & 63)) & 1ull);
+          visb |= ((uint32_t)(j < p.L) | ((uint32_t)(j < n_keys) & anc)) << u;
         }
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float x = (visb >> (kt * 4 + e)) & 1u ? s[kt][e] * p.scale_log2 : -INFINITY;
+            sv[kt * 4 + e] = x;
+            bmax = fmaxf(bmax, x);
+          }
+      }
       bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
       bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
       // no divergence around the MFMAs: a query with nothing visible yet uses
@@ -246,7 +255,6 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnLaunch p) {
   // per-query l over the 4 lane groups (m is already uniform)
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // trailing zero-line transfers
 
   // ---- merge the four waves through LDS (this wave's ring is free now)
   float *ow = (float *)wl;  // [16][OROW]
