@@ -80,7 +80,11 @@ typedef enum { PPD_F32 = 0, PPD_BF16 = 1 } ppd_dtype;
  * with i + head_dim/2, frequency rope_base^(-2i/head_dim)), multi-head
  * attention with n_kv_heads dividing n_heads, SwiGLU MLP, untied LM head.
  * All weight pointers are device pointers; per-layer tensors are given as
- * HOST arrays of n_layers device pointers.  Row-major layouts:
+ * HOST arrays of n_layers device pointers.  For PPD_BF16 models the five
+ * projection matrices (w_qkv, w_o, w_gate_up, w_down, lm_head) are passed in
+ * the packed form written by ppd_pack_weight from the row-major matrices
+ * below; every other tensor, and every tensor of PPD_F32 models, is passed
+ * row-major as listed.  Row-major layouts:
  *   tok_emb     [vocab][hidden]
  *   prompt_emb  [n_prompt][hidden]       trained prompt-token embeddings
  *   attn_norm   [hidden]     per layer
@@ -101,6 +105,39 @@ typedef struct {
   const void *const *mlp_norm, *const *w_gate_up, *const *w_down;
   const void *final_norm, *lm_head;
 } ppd_model;
+
+/*
+ * Weight packing for PPD_BF16 models.  The verification step streams every
+ * projection weight from HBM once per step (its cost is that stream), so the
+ * library keeps them in the order its matrix-core GEMMs consume them: 128-row
+ * tiles x 64-column chunks, each chunk a run of 1 KB operand fragments of 16
+ * rows x 32 columns in the lane order of the gfx950 bf16 MFMA instruction.
+ * Rows and columns past the matrix are zero-filled (e.g. the LM head's last
+ * tile when vocab % 128 != 0).  The packed form depends only on the matrix,
+ * not on T or L; pack once at load time.
+ *   kind  which matrix (ppd_weight_kind); rows, cols: its row-major shape,
+ *         i.e. PPD_W_QKV [(n_heads + 2 n_kv_heads) 128][hidden],
+ *         PPD_W_O [hidden][n_heads 128], PPD_W_GATE_UP [2 ffn][hidden],
+ *         PPD_W_DOWN [hidden][ffn], PPD_W_LM_HEAD [vocab][hidden].
+ *         cols % 64 == 0; rows % 128 == 0 except for the LM head.
+ *   src   device bfloat16 [rows][cols], row-major (not modified)
+ *   dst   device buffer of ppd_packed_weight_bytes(kind, rows, cols) bytes,
+ *         caller-owned, must not overlap src
+ * ppd_packed_weight_bytes returns 0 for invalid arguments (message in
+ * ppd_last_error).  ppd_pack_weight enqueues one kernel on `stream`;
+ * PPD_EINVAL / PPD_EUNSUPPORTED for bad arguments, nothing enqueued.
+ */
+typedef enum {
+  PPD_W_QKV = 0,
+  PPD_W_O = 1,
+  PPD_W_GATE_UP = 2,
+  PPD_W_DOWN = 3,
+  PPD_W_LM_HEAD = 4
+} ppd_weight_kind;
+
+size_t ppd_packed_weight_bytes(int32_t kind, int32_t rows, int32_t cols);
+ppd_status ppd_pack_weight(int32_t kind, int32_t rows, int32_t cols, const void *src, void *dst,
+                           void *stream);
 
 /*
  * The single KV cache of the accepted sequence (device memory, caller-owned).

@@ -23,6 +23,7 @@ PPD_F32, PPD_BF16 = 0, 1
 PPD_T_MAX = 128
 PPD_MASK_WORDS = 2
 PPD_DEV_BAD_TOKEN, PPD_DEV_BAD_PARENT, PPD_DEV_NAN_LOGIT = 1, 2, 4
+PPD_W_QKV, PPD_W_O, PPD_W_GATE_UP, PPD_W_DOWN, PPD_W_LM_HEAD = range(5)
 
 _STATUS_NAMES = {0: "PPD_OK", 1: "PPD_EINVAL", 2: "PPD_ETREE", 3: "PPD_ECAPACITY",
                  4: "PPD_EDEVICE", 5: "PPD_EUNSUPPORTED", 6: "PPD_EWORKSPACE"}
@@ -74,7 +75,10 @@ def lib() -> C.CDLL:
         L.ppd_device_status.argtypes = [vp, sz, P(C.c_uint32), i32, vp]
         L.ppd_set_kernel_timer.argtypes = [i32, vp, vp, i32]
         L.ppd_last_error.restype = C.c_char_p
-        for f in ("ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
+        L.ppd_packed_weight_bytes.argtypes = [i32, i32, i32]
+        L.ppd_packed_weight_bytes.restype = sz
+        L.ppd_pack_weight.argtypes = [i32, i32, i32, vp, vp, vp]
+        for f in ("ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
                   "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -118,35 +122,51 @@ def _dev(t, dtype=None, name="tensor"):
 class Model:
     """A ppd_model description over device tensors (kept alive by this object).
 
-    `w` follows the layout of include/ppd.h (see synth.model.make_weights)."""
+    `w` follows the row-major layout of include/ppd.h (see
+    synth.model.make_weights).  For bf16 models the five projection matrices
+    are packed once here (ppd_pack_weight) and the description points at the
+    packed copies; `w` itself is left unchanged."""
 
-    def __init__(self, shape, w):
+    _PACKED = {"w_qkv": PPD_W_QKV, "w_o": PPD_W_O, "w_gate_up": PPD_W_GATE_UP,
+               "w_down": PPD_W_DOWN}
+
+    def __init__(self, shape, w, stream=None):
         import torch
         dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
         self.shape = shape
         self.w = w
         layers = w["layers"]
         n = shape.n_layers
+        bf16 = shape.dtype == "bf16"
+        self.packed = {k: [] for k in self._PACKED}
 
         def arr(key):
+            ptrs = []
             for lay in layers:
                 _dev(lay[key], dt, key)
-            return (C.c_void_p * n)(*[_ptr(lay[key]) for lay in layers])
+                if bf16 and key in self._PACKED:
+                    pk = ppd_pack_weight(self._PACKED[key], lay[key], stream)
+                    self.packed[key].append(pk)
+                    ptrs.append(_ptr(pk))
+                else:
+                    ptrs.append(_ptr(lay[key]))
+            return (C.c_void_p * n)(*ptrs)
 
         for key in ("tok_emb", "prompt_emb", "final_norm", "lm_head"):
             _dev(w[key], dt, key)
         self._arrays = {k: arr(k) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up",
                                             "w_down")}
+        self.lm_head = ppd_pack_weight(PPD_W_LM_HEAD, w["lm_head"], stream) if bf16 else w["lm_head"]
         a = self._arrays
         self.desc = ppd_model(
             shape.n_layers, shape.hidden, shape.n_heads, shape.n_kv_heads, shape.head_dim,
             shape.ffn, shape.vocab, shape.n_prompt, shape.rms_eps, shape.rope_base,
-            PPD_BF16 if shape.dtype == "bf16" else PPD_F32,
+            PPD_BF16 if bf16 else PPD_F32,
             _ptr(w["tok_emb"]), _ptr(w["prompt_emb"]),
             C.cast(a["attn_norm"], C.POINTER(C.c_void_p)), C.cast(a["w_qkv"], C.POINTER(C.c_void_p)),
             C.cast(a["w_o"], C.POINTER(C.c_void_p)), C.cast(a["mlp_norm"], C.POINTER(C.c_void_p)),
             C.cast(a["w_gate_up"], C.POINTER(C.c_void_p)), C.cast(a["w_down"], C.POINTER(C.c_void_p)),
-            _ptr(w["final_norm"]), _ptr(w["lm_head"]))
+            _ptr(w["final_norm"]), _ptr(self.lm_head))
 
 
 class KVCache:
@@ -167,6 +187,25 @@ def ppd_workspace_bytes(model: Model, t_max: int, max_len: int) -> int:
     if n == 0:
         raise PPDError(PPD_EINVAL, ppd_last_error())
     return int(n)
+
+
+def ppd_packed_weight_bytes(kind: int, rows: int, cols: int) -> int:
+    n = lib().ppd_packed_weight_bytes(int(kind), int(rows), int(cols))
+    if n == 0:
+        raise PPDError(PPD_EINVAL, ppd_last_error())
+    return int(n)
+
+
+def ppd_pack_weight(kind: int, src, stream=None):
+    """Packed copy (a new uint8 device tensor) of the row-major bf16 matrix
+    `src` [rows][cols], in the layout the bf16 GEMMs read."""
+    import torch
+    _dev(src, torch.bfloat16, "weight")
+    rows, cols = (int(x) for x in src.shape)
+    dst = torch.empty(ppd_packed_weight_bytes(kind, rows, cols), dtype=torch.uint8,
+                      device=src.device)
+    _check(lib().ppd_pack_weight(int(kind), rows, cols, _ptr(src), _ptr(dst), _stream(stream)))
+    return dst
 
 
 def ppd_workspace_init(ws, stream=None):
@@ -241,6 +280,6 @@ def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):
     return st, sp
 
 
-__all__ = ["ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
+__all__ = ["ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
            "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept", "ppd_kv_compact",
            "ppd_device_status", "ppd_last_error"]

@@ -7,52 +7,49 @@
 // The step is bound by streaming the weights from HBM once (arithmetic
 // intensity ~T flop/byte, far below the MI355X ridge), so the kernel is built
 // around the weight stream:
-//  * a workgroup owns a tile of BN weight rows (128, or 64 for the residual
-//    projections) and one slice of K (split-K across workgroups where N alone
-//    gives too few tiles);
-//  * K is walked in 64-wide chunks.  Each chunk of weights and activations
-//    is fetched cooperatively with 16-byte direct-to-LDS transfers
-//    (global_load_lds_dwordx4) in which 8 consecutive lanes cover one row's
-//    full 128-byte line (the pattern that streams at full HBM rate).  An
-//    NS-slot LDS ring keeps NS-1 chunks in flight; 16-byte columns are
-//    XOR-swizzled per row pair, so the MFMA operand reads are conflict-free;
-//  * each workgroup starts its K walk at its own chunk offset, which spreads
-//    the lockstep workgroups over the HBM channels;
-//  * each wave owns whole 16-row sub-tiles (two of them, 64 rows apart, for
-//    128-row tiles: the RoPE and SwiGLU partners), so no reduction between
-//    waves is needed;
-//  * split-K partials go to the workspace with agent-scope relaxed atomic
-//    stores (coherent across the XCDs without L2 write-back/invalidate); the
-//    last workgroup of a tile (atomic ticket) adds them in split order, so
-//    results never depend on timing;
-//  * the epilogue is fused: RMSNorm row scale, RoPE + query/key/value stores
-//    into the cache (QKV), residual add + next norm operand + sum of squares
-//    (output / down projection), SwiGLU (gate/up), logits + argmax partials
-//    (LM head).
+//  * weights are pre-packed (launch_pack_weight) so that every MFMA operand
+//    fragment -- 16 rows x 32 columns, in the lane order the instruction
+//    reads it -- is one contiguous 1 KB; a wave loads its fragments straight
+//    into registers with 16-byte non-temporal loads, PPD_GEMM_RING chunks
+//    ahead, with no LDS on the weight path (weights are not shared between
+//    waves);
+//  * the activations (the same for every workgroup, served from L2) follow
+//    the same register ring and are staged per chunk in a double-buffered,
+//    XOR-swizzled LDS slot read by the four waves;
+//  * a compute unit's load path sustains only ~35 GB/s, so a GEMM needs
+//    (nearly) every CU streaming to approach the HBM rate.  GEMMs with enough
+//    128-row tiles run one whole tile per workgroup and finish it in place
+//    (fused epilogue).  The others are cut Stream-K style: the (tile, chunk)
+//    units are split into equal contiguous ranges, one per compute unit; a
+//    workgroup streams across tile boundaries and stores the partial sums of
+//    each tile segment, and a small finish kernel (one workgroup per tile and
+//    16-token block) adds a tile's partials in workgroup order and runs the
+//    epilogue -- the kernel boundary orders the two, so no cross-workgroup
+//    synchronisation is needed and results never depend on timing;
+//  * the epilogue: RMSNorm row scale, RoPE + query/key/value stores into the
+//    cache (QKV), residual add + next norm operand + sum of squares (output /
+//    down projection), SwiGLU (gate/up), logits + argmax partials (LM head).
+#include <algorithm>
+
 #include "ppd_internal.h"
 
 namespace {
 
-#ifndef PPD_GEMM_NS
-#define PPD_GEMM_NS 3
-#endif
-constexpr int NS = PPD_GEMM_NS;  // LDS ring slots (chunks requested ahead + 1)
-constexpr int KC = 64;           // K per chunk: two MFMA k-steps, one 128-byte line per row
+constexpr int KC = 64;            // K per chunk: two MFMA k-steps
+constexpr int BN = PPD_GEMM_BN;   // rows per tile: 8 sub-tiles of 16, wave w owns w and w + 4
+constexpr int R = PPD_GEMM_RING;  // chunks requested ahead
+constexpr int FRAG = 64;          // u32x4 per packed operand fragment (1 KB)
+constexpr int UNIT = 16 * FRAG;   // u32x4 per packed (tile, chunk): 8 sub-tiles x 2 k-steps
 
+// weight row of tile row r (0 <= r < 128)
 template <int KIND>
-constexpr int kSub = (KIND == GEMM_RESID) ? 1 : 2;  // 16-row sub-tiles per wave
-template <int KIND>
-constexpr int kBN = 64 * kSub<KIND>;                 // rows per tile
-
-// weight row of tile row r (0 <= r < BN)
-template <int KIND>
-__device__ __forceinline__ int tile_row(int tile, int r, int F) {
+__device__ __forceinline__ int tile_row(int tile, int r, int N) {
   if constexpr (KIND == GEMM_SWIGLU) {
     // 64 features: gate rows f0..f0+63, then the matching up rows
-    return r < 64 ? tile * 64 + r : F + tile * 64 + (r - 64);
+    return r < 64 ? tile * 64 + r : N + tile * 64 + (r - 64);
   } else {
     // QKV: tile = one head's 128 rows (dims 0..127); others: consecutive rows
-    return tile * kBN<KIND> + r;
+    return tile * BN + r;
   }
 }
 
@@ -63,297 +60,107 @@ __device__ __forceinline__ void amax_merge(float &v, int &i, float v2, int i2) {
   }
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
-
 // 16-byte column swizzle of a 128-byte LDS row: logical column c of row r is
 // stored at physical column c ^ ((r >> 1) & 7).  Sixteen consecutive rows
 // read at one logical column then cover all 64 banks exactly once.
 __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
-// One 16-byte-per-lane global -> LDS transfer (global_load_lds_dwordx4): lane
-// l's 16 bytes land at LDS byte lds_addr + 16 l.  Issued as inline assembly so
-// that the compiler does not track the LDS write: its waitcnt pass would
-// otherwise drain every transfer in flight before each LDS read; the kernel
-// waits explicitly (s_waitcnt vmcnt + barrier) instead.
-__device__ __forceinline__ void dma16(const void *g, unsigned lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
-               : "memory", "m0");
+// ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) of tokens
+// tok0 .. tok0 + NT - 1 from the producer's sum-of-squares partials
+// ss[p][T_pad]: group j of the J = 256 / NT thread groups sums partials j,
+// j + J, ... in order (the first 16 per thread requested by rs_request, so
+// that a caller can overlap their latency), then the group sums are added in
+// group order.
+template <int NT>
+__device__ __forceinline__ void rs_request(const GemmLaunch &g, int tok0, float (&ssv)[16]) {
+  constexpr int J = 256 / NT;
+  const int tid = threadIdx.x, t = tid % NT, j = tid / NT;
+  const int T_pad = g.MT * 16;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int pp = j + i * J;
+    const bool use = tid < J * NT && pp < g.n_ss;
+    const float v = g.ss[(size_t)(use ? pp : 0) * T_pad + tok0 + t];  // always a valid row
+    ssv[i] = use ? v : 0.f;
+  }
 }
 
-// s_waitcnt immediate for "at most n vector-memory operations outstanding"
-// (expcnt and lgkmcnt left at their maxima, i.e. not waited on)
-constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-// s_waitcnt immediate for "no LDS operation outstanding" (vmcnt, expcnt at maxima)
-constexpr int lgkmcnt0_imm = 15 | (3 << 14) | (7 << 4);
-
-template <int MT, int KIND>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
-  constexpr int SUB = kSub<KIND>;
-  constexpr int BN = kBN<KIND>;
-  constexpr int T_pad = MT * 16;
-  constexpr int WBLK = BN / 8;                // 8-row blocks of weights per chunk
-  constexpr int ABLK = T_pad / 8;             // 8-row blocks of activations per chunk
-  constexpr int NW = WBLK / 4;                // per wave (BN is a multiple of 32)
-  constexpr int NA = (ABLK + 3) / 4;          // per wave (excess loads hit a dummy block)
-  constexpr int LPC = NW + NA;                // vector loads per wave per chunk
-  constexpr int SLOT = (BN + T_pad) * 128;    // bytes of one ring slot
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[NS * SLOT + 1024];
-  __shared__ float rs_s[128];
-  __shared__ float red_s[4][128][2];
-  __shared__ int last_s;
-
+template <int NT>
+__device__ __forceinline__ void rs_finish(const GemmLaunch &g, int tok0, const float (&ssv)[16],
+                                          float *gs, float *rs_s) {
+  constexpr int J = 256 / NT;
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 15;         // MFMA row (weights) / column (tokens) within a 16-tile
-  const int lg = lane >> 4;         // this lane's 16-byte k group within a 32-step
-  const int split = blockIdx.x % g.sk;
-  const int tile = blockIdx.x / g.sk;
-  const int K = g.K;
-  const int nks = K >> 5;
-  const int k_begin = (int)((long)nks * split / g.sk) * 32;
-  const int k_end = (int)((long)nks * (split + 1) / g.sk) * 32;
-  const int n_chunks = (k_end - k_begin + KC - 1) / KC;
-  const int rows_total = KIND == GEMM_SWIGLU ? 2 * g.N : g.N;
-
-  // ---- load slots.  A wave instruction moves one 8-row block: lane l lands
-  // at LDS byte 16 l of the block, i.e. row (l >> 3), physical column l & 7,
-  // so it fetches logical column swz(row, l & 7) of that row from memory.
-  const int wv = __builtin_amdgcn_readfirstlane(wave);  // wave index as a scalar
-  const unsigned lds_base = (unsigned)(size_t)(lds_void_t *)lds;
-  const int brow = lane >> 3;
-  const bf16_t *wsrc[NW];
-  int wcol[NW];
+  const int T_pad = g.MT * 16;
+  float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    const int r = (wave + 4 * i) * 8 + brow;
-    const int c = swz(r, lane & 7);
-    int row = tile_row<KIND>(tile, r, g.N);
-    row = row < rows_total ? row : rows_total - 1;
-    wsrc[i] = g.W + (size_t)row * K + c * 8;
-    wcol[i] = c * 8;
+  for (int i = 0; i < 16; ++i) s += ssv[i];
+  if (tid < J * NT) {
+    const int t = tid % NT, j = tid / NT;
+    for (int pp = j + 16 * J; pp < g.n_ss; pp += J) s += g.ss[(size_t)pp * T_pad + tok0 + t];
+    gs[tid] = s;
   }
-  const bf16_t *asrc[NA];
-  int acol[NA];
-#pragma unroll
-  for (int i = 0; i < NA; ++i) {
-    const int blk = wave + 4 * i;
-    const int r = (blk < ABLK ? blk : 0) * 8 + brow;
-    const int c = swz(r, lane & 7);
-    asrc[i] = g.A + (size_t)r * K + c * 8;
-    acol[i] = c * 8;
+  __syncthreads();
+  if (tid < NT) {
+    float v = 0.f;
+    for (int j = 0; j < J; ++j) v += gs[j * NT + tid];
+    rs_s[tok0 + tid] = rsqrtf(v * g.inv_h + g.eps);
   }
+}
 
-  floatx4 acc[SUB][MT];
-#pragma unroll
-  for (int q = 0; q < SUB; ++q)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+// ---- epilogue operands
+template <int KIND, int MTE>
+struct EpiOperands {
+  floatx4 rope[MTE][2];  // QKV: (cos, sin) of dims i0..i0+3 for each token tile
+  floatx4 x[2][MTE];     // RESID: residual stream of the lane's rows
+  uint2 gain[2];         // RESID: next norm gain of the lane's rows
+};
 
-  // Chunk C goes to ring slot C % NS; columns past the slice end (and the
-  // padding transfers of waves without an activation block) read 16 zero
-  // bytes of the workspace.
-  const bf16_t *zp = g.zeros;
-  // Each workgroup walks its slice starting at its own chunk offset: all
-  // workgroups start together, and rows 8 KB apart otherwise hit the same
-  // HBM channels in lockstep.
-  const int rot = n_chunks > 0 ? (int)(blockIdx.x % (unsigned)n_chunks) : 0;
-  auto issue = [&](int C) {
-    const int cc = C < n_chunks ? (C + rot) % n_chunks : C;
-    const int k0 = k_begin + cc * KC;
-    const unsigned slot = lds_base + (unsigned)((C % NS) * SLOT);
-#pragma unroll
-    for (int i = 0; i < NW; ++i)
-      dma16(k0 + wcol[i] < k_end ? wsrc[i] + k0 : zp, slot + (unsigned)((wv + 4 * i) * 1024));
-#pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const int blk = wv + 4 * i;  // scalar
-      if (blk < ABLK)
-        dma16(k0 + acol[i] < k_end ? asrc[i] + k0 : zp, slot + (unsigned)(BN * 128 + blk * 1024));
-      else
-        dma16(zp, lds_base + (unsigned)(NS * SLOT));
-    }
-  };
-
-  for (int c = 0; c < NS - 1 && c < n_chunks; ++c) issue(c);
-
-  // ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) from the
-  // producer's sum-of-squares partials, fetched while the first chunks are in
-  // flight: group j of the J = 256 / T_pad thread groups sums partials j,
-  // j + J, ..., then the group sums are added in group order.
-  if constexpr (KIND != GEMM_RESID) {
-    constexpr int J = 256 / T_pad;
-    float *gs = &red_s[0][0][0];
-    if (tid < J * T_pad) {
-      const int t = tid % T_pad, j = tid / T_pad;
-      float s = 0.f;
-      for (int p0 = j; p0 < g.n_ss; p0 += 16 * J) {
-        float v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          const int pp = p0 + u * J;
-          const float x = g.ss[(size_t)(pp < g.n_ss ? pp : 0) * T_pad + t];  // a valid row
-          v[u] = pp < g.n_ss ? x : 0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < 16; ++u) s += v[u];
-      }
-      gs[tid] = s;
-    }
-    __syncthreads();
-    if (tid < T_pad) {
-      float s = 0.f;
-      for (int j = 0; j < J; ++j) s += gs[j * T_pad + tid];
-      rs_s[tid] = rsqrtf(s * g.inv_h + g.eps);
-    }
-    // rs_s is read after the main loop; its write completes before the
-    // loop's first barrier
-    __builtin_amdgcn_s_waitcnt(lgkmcnt0_imm);
-  }
-
-  auto compute = [&](int c) {
-    const unsigned char *wl = lds + (c % NS) * SLOT;
-    const unsigned char *al = wl + BN * 128;
-#pragma unroll
-    for (int s = 0; s < KC / 32; ++s) {
-      u32x4 wf[SUB], af[MT];
-#pragma unroll
-      for (int q = 0; q < SUB; ++q) {
-        const int r = (wave + 4 * q) * 16 + lr;
-        wf[q] = *(const u32x4 *)(wl + r * 128 + swz(r, s * 4 + lg) * 16);
-      }
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int r = mt * 16 + lr;
-        af[mt] = *(const u32x4 *)(al + r * 128 + swz(r, s * 4 + lg) * 16);
-      }
-#pragma unroll
-      for (int q = 0; q < SUB; ++q)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          acc[q][mt] = mfma16x16x32(as_bf16x8(wf[q]), as_bf16x8(af[mt]), acc[q][mt]);
-    }
-  };
-
-  // Steady state: each iteration requests the chunk NS-1 ahead.
-  const int n_main = n_chunks - (NS - 1);
-  for (int c = 0; c < n_main; ++c) {
-    // own transfers of chunk c done (chunks c+1 .. c+NS-2 may still fly),
-    // then every wave's; the barrier also retires all reads of chunk c-1,
-    // whose slot the next request overwrites.  (A bare s_barrier: a fence
-    // would wait for every transfer in flight.)
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * LPC));
-    asm volatile("s_barrier" ::: "memory");
-    issue(c + NS - 1);
-    compute(c);
-  }
-
-  // Epilogue operands, requested now so that their latency overlaps the
-  // last chunks' (RoPE factors for QKV; residual stream and next norm gain
-  // for the residual projections).
-  const int r4 = (lane >> 4) * 4;  // accumulator rows 4 (lane / 16) + e
-  [[maybe_unused]] floatx4 rope_r[MT][2];
-  [[maybe_unused]] floatx4 x_r[MT];
-  [[maybe_unused]] uint2 gain_r;
+template <int KIND, int MTE>
+__device__ __forceinline__ void epi_request(const GemmLaunch &g, int t, int mt0,
+                                            EpiOperands<KIND, MTE> &o) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, r4 = (lane >> 4) * 4;
   if constexpr (KIND == GEMM_QKV) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)(mt * 16 + lr) * 64 + wave * 16 + r4);
-      rope_r[mt][0] = rp[0];
-      rope_r[mt][1] = rp[1];
+    for (int mt = 0; mt < MTE; ++mt) {
+      const floatx4 *rp =
+          (const floatx4 *)(g.rope + (size_t)((mt0 + mt) * 16 + lr) * 64 + wave * 16 + r4);
+      o.rope[mt][0] = rp[0];
+      o.rope[mt][1] = rp[1];
     }
   } else if constexpr (KIND == GEMM_RESID) {
-    const int n = tile * 64 + wave * 16 + r4;
-    gain_r = *(const uint2 *)(g.gain + n);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) x_r[mt] = *(const floatx4 *)(g.x + (size_t)(mt * 16 + lr) * g.N + n);
-  }
-
-  // Tail: the last chunks are all requested already; wait for them once
-  // (no padding transfers whose latency every workgroup would wait out).
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-  asm volatile("s_barrier" ::: "memory");
-  for (int c = n_main > 0 ? n_main : 0; c < n_chunks; ++c) compute(c);
-
-  // ---- split-K: publish the partial tile; the last workgroup sums all.
-  // Partials are written and read with agent-scope relaxed atomics (coherent
-  // across the XCDs without writing back or invalidating whole L2 caches);
-  // every store has completed (vmcnt 0) before the ticket is taken.
-  if (g.sk > 1) {
-    constexpr size_t tile_u64 = (size_t)4 * SUB * MT * 64 * 2;
-    {
-      uint64_t *dst = (uint64_t *)g.part + (size_t)blockIdx.x * tile_u64;
+    for (int q = 0; q < 2; ++q) {
+      const int n = t * BN + (wave + 4 * q) * 16 + r4;
+      o.gain[q] = *(const uint2 *)(g.gain + n);
 #pragma unroll
-      for (int q = 0; q < SUB; ++q)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const size_t o = (size_t)(((wave * SUB + q) * MT + mt) * 64 + lane) * 2;
-          const floatx4 r = acc[q][mt];
-          __hip_atomic_store(dst + o, __builtin_bit_cast(uint64_t, float2{r[0], r[1]}),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(dst + o + 1, __builtin_bit_cast(uint64_t, float2{r[2], r[3]}),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (tid == 0) {
-      const unsigned prev =
-          __hip_atomic_fetch_add(&g.counters[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int last = prev == (unsigned)(g.sk - 1);
-      if (last) __hip_atomic_store(&g.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      last_s = last;
-    }
-    __syncthreads();
-    if (!last_s) return;
-#pragma unroll
-    for (int q = 0; q < SUB; ++q)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // U splits' partials are requested together, then added in split order
-    constexpr int U = SUB * MT <= 4 ? 4 : (SUB * MT <= 8 ? 2 : 1);
-    for (int s0 = 0; s0 < g.sk; s0 += U) {
-      float2 buf[U][SUB][MT][2];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int s = s0 + u < g.sk ? s0 + u : s0;
-        const uint64_t *src = (const uint64_t *)g.part + (size_t)(tile * g.sk + s) * tile_u64;
-#pragma unroll
-        for (int q = 0; q < SUB; ++q)
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const size_t o = (size_t)(((wave * SUB + q) * MT + mt) * 64 + lane) * 2;
-            buf[u][q][mt][0] = __builtin_bit_cast(
-                float2, __hip_atomic_load(src + o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-            buf[u][q][mt][1] = __builtin_bit_cast(
-                float2, __hip_atomic_load(src + o + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-          }
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (s0 + u < g.sk)
-#pragma unroll
-          for (int q = 0; q < SUB; ++q)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-              acc[q][mt] += floatx4{buf[u][q][mt][0].x, buf[u][q][mt][0].y, buf[u][q][mt][1].x,
-                                    buf[u][q][mt][1].y};
+      for (int mt = 0; mt < MTE; ++mt)
+        o.x[q][mt] = *(const floatx4 *)(g.x + (size_t)((mt0 + mt) * 16 + lr) * g.N + n);
     }
   }
+}
 
-  // accumulator layout: lane holds rows 4 (lane / 16) + e of its sub-tile,
-  // token column lane % 16 of token tile mt
-  const int T = g.T;
-
+// Epilogue of tile t for token tiles mt0 .. mt0 + MTE - 1 from the complete
+// sums in acc.  Accumulator layout: the lane holds rows 4 (lane / 16) + e of
+// sub-tiles wave and wave + 4, token (mt0 + mt) 16 + lane % 16.  Called by
+// all 256 threads (it has barriers); rs_s holds the row scales by token.
+template <int KIND, int MTE>
+__device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
+                                         const floatx4 (&acc)[2][MTE],
+                                         const EpiOperands<KIND, MTE> &o, const float *rs_s,
+                                         float (*red_s)[128][2]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, r4 = (lane >> 4) * 4;
+  const int T = g.T, T_pad = g.MT * 16;
   if constexpr (KIND == GEMM_QKV) {
-    const int hp = tile;                // head part: q heads, then k, then v
-    const int i0 = wave * 16 + r4;      // dims i0..i0+3 and their partners +64
+    const int hp = t;               // head part: q heads, then k, then v
+    const int i0 = wave * 16 + r4;  // dims i0..i0+3 and their partners +64
     const int nh = g.nh, nkv = g.nkv;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int t = mt * 16 + lr;
-      if (t >= T) continue;
-      const float rs = rs_s[t];
+    for (int mt = 0; mt < MTE; ++mt) {
+      const int tk = (mt0 + mt) * 16 + lr;
+      if (tk >= T) continue;
+      const float rs = rs_s[tk];
       float lo[4], hi[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -361,23 +168,23 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
         hi[e] = acc[1][mt][e] * rs;
       }
       if (hp < nh + nkv) {
-        const float cs_all[8] = {rope_r[mt][0][0], rope_r[mt][0][1], rope_r[mt][0][2], rope_r[mt][0][3],
-                                 rope_r[mt][1][0], rope_r[mt][1][1], rope_r[mt][1][2], rope_r[mt][1][3]};
+        const float cs[8] = {o.rope[mt][0][0], o.rope[mt][0][1], o.rope[mt][0][2], o.rope[mt][0][3],
+                             o.rope[mt][1][0], o.rope[mt][1][1], o.rope[mt][1][2], o.rope[mt][1][3]};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float2 cs = float2{cs_all[2 * e], cs_all[2 * e + 1]};
+          const float c = cs[2 * e], sn = cs[2 * e + 1];
           const float a = lo[e], b = hi[e];
-          lo[e] = a * cs.x - b * cs.y;
-          hi[e] = b * cs.x + a * cs.y;
+          lo[e] = a * c - b * sn;
+          hi[e] = b * c + a * sn;
         }
         const u32x2 plo = u32x2{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
         const u32x2 phi = u32x2{pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
-        bf16_t *dst = hp < nh ? g.q + ((size_t)t * nh + hp) * 128
-                              : g.kc + ((size_t)(hp - nh) * g.cap + g.L + t) * 128;
+        bf16_t *dst = hp < nh ? g.q + ((size_t)tk * nh + hp) * 128
+                              : g.kc + ((size_t)(hp - nh) * g.cap + g.L + tk) * 128;
         *(u32x2 *)(dst + i0) = plo;
         *(u32x2 *)(dst + i0 + 64) = phi;
       } else {
-        bf16_t *vb = g.vc + (size_t)(hp - nh - nkv) * 128 * g.cap + g.L + t;
+        bf16_t *vb = g.vc + (size_t)(hp - nh - nkv) * 128 * g.cap + g.L + tk;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           vb[(size_t)(i0 + e) * g.cap] = f32_to_bf16(lo[e]);
@@ -386,71 +193,73 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
       }
     }
   } else if constexpr (KIND == GEMM_SWIGLU) {
-    const int f0 = tile * 64 + wave * 16 + r4;
+    const int f0 = t * 64 + wave * 16 + r4;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int t = mt * 16 + lr;
-      if (t >= T) continue;
-      const float rs = rs_s[t];
+    for (int mt = 0; mt < MTE; ++mt) {
+      const int tk = (mt0 + mt) * 16 + lr;
+      if (tk >= T) continue;
+      const float rs = rs_s[tk];
       float a[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float gt = acc[0][mt][e] * rs, up = acc[1][mt][e] * rs;
         a[e] = gt / (1.f + expf(-gt)) * up;
       }
-      *(u32x2 *)(g.act + (size_t)t * g.N + f0) =
+      *(u32x2 *)(g.act + (size_t)tk * g.N + f0) =
           u32x2{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3])};
     }
   } else if constexpr (KIND == GEMM_RESID) {
-    const int n = tile * 64 + wave * 16 + r4;
-    const uint2 gw = gain_r;
-    const float g0 = bf16_to_f32(gw.x & 0xffff), g1 = bf16_to_f32(gw.x >> 16);
-    const float g2 = bf16_to_f32(gw.y & 0xffff), g3 = bf16_to_f32(gw.y >> 16);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int t = mt * 16 + lr;
+    for (int mt = 0; mt < MTE; ++mt) {
+      const int tk = (mt0 + mt) * 16 + lr;
       float sq = 0.f;
-      if (t < T) {
-        float *xp = g.x + (size_t)t * g.N + n;
-        floatx4 xv = x_r[mt];
-        xv += acc[0][mt];
-        *(floatx4 *)xp = xv;
-        *(u32x2 *)(g.xg + (size_t)t * g.N + n) =
-            u32x2{pack_bf16x2(xv[0] * g0, xv[1] * g1), pack_bf16x2(xv[2] * g2, xv[3] * g3)};
-        sq = (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
+      if (tk < T) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const int n = t * BN + (wave + 4 * q) * 16 + r4;
+          const uint2 gw = o.gain[q];
+          const float g0 = bf16_to_f32(gw.x & 0xffff), g1 = bf16_to_f32(gw.x >> 16);
+          const float g2 = bf16_to_f32(gw.y & 0xffff), g3 = bf16_to_f32(gw.y >> 16);
+          floatx4 xv = o.x[q][mt];
+          xv += acc[q][mt];
+          *(floatx4 *)(g.x + (size_t)tk * g.N + n) = xv;
+          *(u32x2 *)(g.xg + (size_t)tk * g.N + n) =
+              u32x2{pack_bf16x2(xv[0] * g0, xv[1] * g1), pack_bf16x2(xv[2] * g2, xv[3] * g3)};
+          sq += (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
+        }
       }
       // sum over the 4 lane groups (rows) of this wave
       sq += __shfl_xor(sq, 16, 64);
       sq += __shfl_xor(sq, 32, 64);
-      if (lane < 16) red_s[wave][t][0] = sq;
+      if (lane < 16) red_s[wave][tk][0] = sq;
     }
     __syncthreads();
-    if (tid < T_pad) {
-      const float v = tid < T ? ((red_s[0][tid][0] + red_s[1][tid][0]) +
-                                 (red_s[2][tid][0] + red_s[3][tid][0]))
-                              : 0.f;
-      g.ss_out[(size_t)tile * T_pad + tid] = v;
+    if (tid < MTE * 16) {
+      const int tk = mt0 * 16 + tid;
+      const float v = tk < T ? ((red_s[0][tk][0] + red_s[1][tk][0]) + (red_s[2][tk][0] + red_s[3][tk][0]))
+                             : 0.f;
+      g.ss_out[(size_t)t * T_pad + tk] = v;
     }
   } else {  // GEMM_LOGITS
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int t = mt * 16 + lr;
-      const float rs = t < T ? rs_s[t] : 0.f;
+    for (int mt = 0; mt < MTE; ++mt) {
+      const int tk = (mt0 + mt) * 16 + lr;
+      const float rs = tk < T ? rs_s[tk] : 0.f;
       float bv = 0.f;
       int bi = -1;
 #pragma unroll
-      for (int q = 0; q < SUB; ++q) {
-        const int n = tile * BN + (wave + 4 * q) * 16 + r4;
+      for (int q = 0; q < 2; ++q) {
+        const int n = t * BN + (wave + 4 * q) * 16 + r4;
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[q][mt][e] * rs;
-        if (t < T) {
+        if (tk < T) {
           if (g.logits) {
             if ((g.N & 3) == 0 && n + 3 < g.N) {
-              *(floatx4 *)(g.logits + (size_t)t * g.N + n) = floatx4{v[0], v[1], v[2], v[3]};
+              *(floatx4 *)(g.logits + (size_t)tk * g.N + n) = floatx4{v[0], v[1], v[2], v[3]};
             } else {
               for (int e = 0; e < 4; ++e)
-                if (n + e < g.N) g.logits[(size_t)t * g.N + n + e] = v[e];
+                if (n + e < g.N) g.logits[(size_t)tk * g.N + n + e] = v[e];
             }
           }
 #pragma unroll
@@ -468,55 +277,327 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmLaunch g) {
       }
       // merge over the 4 lane groups: larger value, then smaller index
 #pragma unroll
-      for (int o = 16; o <= 32; o <<= 1) {
-        const float v2 = __shfl_xor(bv, o, 64);
-        const int i2 = __shfl_xor(bi, o, 64);
+      for (int off = 16; off <= 32; off <<= 1) {
+        const float v2 = __shfl_xor(bv, off, 64);
+        const int i2 = __shfl_xor(bi, off, 64);
         amax_merge(bv, bi, v2, i2);
       }
       if (lane < 16) {
-        red_s[wave][t][0] = bv;
-        red_s[wave][t][1] = __int_as_float(bi);
+        red_s[wave][tk][0] = bv;
+        red_s[wave][tk][1] = __int_as_float(bi);
       }
     }
     __syncthreads();
-    if (tid < T_pad) {
-      float v = red_s[0][tid][0];
-      int i = __float_as_int(red_s[0][tid][1]);
-      for (int w = 1; w < 4; ++w) amax_merge(v, i, red_s[w][tid][0], __float_as_int(red_s[w][tid][1]));
-      g.amax[(size_t)tile * T_pad + tid] = make_float2(v, __int_as_float(i));
+    if (tid < MTE * 16) {
+      const int tk = mt0 * 16 + tid;
+      float v = red_s[0][tk][0];
+      int i = __float_as_int(red_s[0][tk][1]);
+      for (int w = 1; w < 4; ++w) amax_merge(v, i, red_s[w][tk][0], __float_as_int(red_s[w][tk][1]));
+      g.amax[(size_t)t * T_pad + tk] = make_float2(v, __int_as_float(i));
     }
   }
 }
 
+// partial sums of tile t by its contributor `slot`: [8 sub-tile pairs x MT][64
+// lanes] floatx4, sub-tile pair index (wave 2 + q) MT + mt
+__device__ __forceinline__ floatx4 *partial_of(const GemmLaunch &g, int t, int slot) {
+  return (floatx4 *)g.part + ((size_t)t * g.maxc + slot) * (size_t)(8 * g.MT * 64);
+}
+
+// ---- the GEMM.  Workgroup w of G owns the units [u0, u1) (see
+// PPD_GEMM_RING); SPLIT: store the partial of every tile segment, else every
+// segment is a whole tile and is finished in place.
+template <int MT, int KIND, bool SPLIT>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
+  constexpr int T_pad = MT * 16;
+  constexpr int NAP = (T_pad * 8 + 255) / 256;  // 16-byte activation pieces per thread per chunk
+  __shared__ __attribute__((aligned(16))) unsigned char lds_a[2][T_pad * 128];
+  __shared__ float rs_s[128];
+  __shared__ float red_s[4][128][2];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15;  // MFMA row (weights) / column (tokens) within a 16-tile
+  const int lg = lane >> 4;  // this lane's 16-byte k group within a 32-step
+  const int K = g.K, kc = g.kc_pad, G = g.G;
+  const long Ng = (long)g.n_tiles * kc / R;
+  // this workgroup's units [u0, u1) (uniform: kept in scalar registers)
+  const int u0 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x) * R);
+  const int u1 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x + 1) * R);
+
+  // norm row scales, requested before the weight stream starts
+  constexpr bool kScale = !SPLIT && KIND != GEMM_RESID;
+  [[maybe_unused]] float ssv[16];
+  if constexpr (kScale) rs_request<T_pad>(g, 0, ssv);
+
+  // ---- register rings.  Unit u's weight fragments for this wave: sub-tiles
+  // wave and wave + 4, k-steps 0 and 1.  Its activation pieces: 16-byte piece
+  // e = tid + 256 i of the [T_pad][64] chunk (row e / 8, column e % 8).
+  // Requests past the range read one 16-byte line (lane offsets masked to 0),
+  // so every iteration issues the same loads.
+  const u32x4 *wp = (const u32x4 *)g.W;
+  u32x4 wr[R][4], ar[R][NAP];
+  auto request_w = [&](int u, u32x4(&dw)[4]) {
+    const int live = u < u1 ? 63 : 0;
+    const int uu = u < u1 ? u : u1 - 1;
+    const u32x4 *wu = wp + (size_t)uu * UNIT + (lane & live);
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+        dw[q * 2 + s] = __builtin_nontemporal_load(wu + ((wave + 4 * q) * 2 + s) * FRAG);
+  };
+  // per-lane element offsets of the activation pieces within a chunk;
+  // pieces e >= T_pad * 8 (odd MT) load row 0 and are not staged
+  int aoff[NAP];
+#pragma unroll
+  for (int i = 0; i < NAP; ++i) {
+    int e = tid + 256 * i;
+    if constexpr (T_pad * 8 % 256 != 0) e = e < T_pad * 8 ? e : 0;
+    aoff[i] = (e >> 3) * K + (e & 7) * 8;
+  }
+  // u: unit to request; cu: its chunk within its tile
+  auto request_a = [&](int u, int cu, u32x4(&da)[NAP]) {
+    const int k0 = cu * KC;
+    const bool kin = k0 < K;  // padding chunks read zeros
+    const bf16_t *base = kin ? g.A + k0 : g.zeros;
+    // past the range and in padding chunks every lane reads the base line.
+    // The mask is opaque to the compiler, so that it issues the same loads
+    // on every path instead of branching on it.
+    int keep = __builtin_amdgcn_readfirstlane((u < u1 && kin) ? -1 : 0);
+    asm volatile("" : "+s"(keep));
+#pragma unroll
+    for (int i = 0; i < NAP; ++i) da[i] = *(const u32x4 *)(base + (aoff[i] & keep));
+  };
+  auto stage = [&](const u32x4(&da)[NAP], int slot) {
+#pragma unroll
+    for (int i = 0; i < NAP; ++i) {
+      const int e = tid + 256 * i;
+      if (T_pad * 8 % 256 == 0 || e < T_pad * 8) {
+        const int r = e >> 3, c = e & 7;
+        *(u32x4 *)(&lds_a[slot][r * 128 + swz(r, c) * 16]) = da[i];
+      }
+    }
+  };
+
+  floatx4 acc[2][MT];
+  int tile = u0 / kc;
+  [[maybe_unused]] EpiOperands<KIND, MT> eo;
+  if constexpr (!SPLIT) epi_request<KIND, MT>(g, tile, 0, eo);
+  const int c0 = u0 - tile * kc;  // first unit's chunk (a multiple of R)
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    request_w(u0 + j, wr[j]);
+    request_a(u0 + j, c0 + j, ar[j]);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (kScale) rs_finish<T_pad>(g, 0, ssv, &red_s[0][0][0], rs_s);
+  // rs_s is read by epilogues after the main loop's barriers; red_s is next
+  // written by an epilogue, after them as well
+
+  // ---- main loop over segments (the units of one tile within [u0, u1)),
+  // R units per trip.  Unit u: stage its activations (requested R units ago)
+  // into LDS slot (u - u0) & 1 and request unit u + R's into the freed
+  // registers; barrier; multiply with the weight fragments requested R units
+  // ago, then request unit u + R's weights into them.  The slot staged here
+  // was last read for unit u - 2, which every wave finished before unit
+  // u - 1's barrier.  The accumulators are zeroed per segment, so the inner
+  // loop carries them unchanged.
+  int gc = c0;  // chunk of unit gu within its tile
+  for (int gu = u0; gu < u1;) {
+    const int ue = min(u1, (tile + 1) * kc);
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (; gu < ue; gu += R) {
+      // chunk of unit gu + R + j: gc + R + j, wrapped into the next tile
+      const int nc = gc + R < kc ? gc + R : gc + R - kc;
+#pragma unroll
+      for (int j = 0; j < R; ++j) {
+        const int u = gu + j;
+        const int slot = (u - u0) & 1;
+        stage(ar[j], slot);
+        __builtin_amdgcn_sched_barrier(0);
+        request_a(u + R, nc + j, ar[j]);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        const unsigned char *al = lds_a[slot];
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          u32x4 af[MT];
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const int r = mt * 16 + lr;
+            af[mt] = *(const u32x4 *)(al + r * 128 + swz(r, s * 4 + lg) * 16);
+          }
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[q][mt] = mfma16x16x32(as_bf16x8(wr[j][q * 2 + s]), as_bf16x8(af[mt]), acc[q][mt]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        request_w(u + R, wr[j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      gc = nc;
+    }
+    if constexpr (SPLIT) {
+      // this segment's partial, in slot (this workgroup - the tile's first
+      // contributor); plain stores: the finish kernel runs after this grid
+      const int first = gemm_group_owner(Ng, G, (long)tile * kc / R);
+      floatx4 *dst = partial_of(g, tile, blockIdx.x - first);
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) dst[((wave * 2 + q) * MT + mt) * 64 + lane] = acc[q][mt];
+      ++tile;
+    } else {
+      epilogue<KIND, MT>(g, tile, 0, acc, eo, rs_s, red_s);
+      if (ue < u1) {
+        __syncthreads();  // red_s is written again by the next tile's epilogue
+        epi_request<KIND, MT>(g, ++tile, 0, eo);
+      }
+    }
+  }
+}
+
+// ---- finish of a split GEMM: workgroup (tile, 16-token block mt) adds the
+// tile's partials in contributor (workgroup) order and runs the epilogue for
+// the block's tokens.  The waves and lanes keep the GEMM's accumulator layout.
 template <int KIND>
-hipError_t launch_kind(const GemmLaunch &g, int n_tiles, hipStream_t s) {
-  dim3 grid(n_tiles * g.sk), block(256);
+__global__ __launch_bounds__(256) void gemm_finish_kernel(GemmLaunch g) {
+  __shared__ float rs_s[128];
+  __shared__ float red_s[4][128][2];
+  const int t = blockIdx.x, mt = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long Ng = (long)g.n_tiles * g.kc_pad / R;
+  const int first = gemm_group_owner(Ng, g.G, (long)t * g.kc_pad / R);
+  const int n_c = gemm_group_owner(Ng, g.G, (long)(t + 1) * g.kc_pad / R - 1) - first + 1;
+
+  [[maybe_unused]] float ssv[16];
+  if constexpr (KIND != GEMM_RESID) rs_request<16>(g, mt * 16, ssv);
+  EpiOperands<KIND, 1> eo;
+  epi_request<KIND, 1>(g, t, mt, eo);
+
+  // U contributors' partials are requested together (one round trip), then
+  // added in order
+  constexpr int U = 8;
+  floatx4 acc[2][1];
+  acc[0][0] = acc[1][0] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < n_c; c0 += U) {
+    floatx4 buf[U][2];
+#pragma unroll
+    for (int v = 0; v < U; ++v) {
+      const floatx4 *src = partial_of(g, t, min(c0 + v, n_c - 1));
+#pragma unroll
+      for (int q = 0; q < 2; ++q) buf[v][q] = src[((wave * 2 + q) * g.MT + mt) * 64 + lane];
+    }
+#pragma unroll
+    for (int v = 0; v < U; ++v)
+      if (c0 + v < n_c) {
+        acc[0][0] += buf[v][0];
+        acc[1][0] += buf[v][1];
+      }
+  }
+  if constexpr (KIND != GEMM_RESID) rs_finish<16>(g, mt * 16, ssv, &red_s[0][0][0], rs_s);
+  __syncthreads();  // red_s (used by rs_finish) is reused by the epilogue
+  epilogue<KIND, 1>(g, t, mt, acc, eo, rs_s, red_s);
+}
+
+template <int KIND>
+hipError_t launch_kind(const GemmLaunch &g, hipStream_t s) {
+  const dim3 grid(g.G), block(256);
+  hipEvent_t ev0 = (hipEvent_t)g.ev_start, ev1 = (hipEvent_t)g.ev_stop;
+  // timed: from the GEMM dispatch's start to the last dispatch's end
+  hipEvent_t gemm_stop = g.split ? nullptr : ev1;
   switch (g.MT) {
-#define PPD_CASE(M) \
-  case M:                                                                                   \
-    if (g.ev_start)                                                                         \
-      hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND>), grid, block, 0, s,                 \
-                            (hipEvent_t)g.ev_start, (hipEvent_t)g.ev_stop, 0, g);           \
-    else                                                                                    \
-      hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND>), grid, block, 0, s, g);                \
+#define PPD_CASE(M)                                                                          \
+  case M:                                                                                    \
+    if (g.split) {                                                                           \
+      if (ev0)                                                                               \
+        hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND, true>), grid, block, 0, s, ev0,     \
+                              gemm_stop, 0, g);                                              \
+      else                                                                                   \
+        hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND, true>), grid, block, 0, s, g);         \
+    } else {                                                                                 \
+      if (ev0)                                                                               \
+        hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND, false>), grid, block, 0, s, ev0,    \
+                              gemm_stop, 0, g);                                              \
+      else                                                                                   \
+        hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND, false>), grid, block, 0, s, g);        \
+    }                                                                                        \
     break;
     PPD_CASE(1) PPD_CASE(2) PPD_CASE(3) PPD_CASE(4) PPD_CASE(5) PPD_CASE(6) PPD_CASE(7) PPD_CASE(8)
 #undef PPD_CASE
     default: return hipErrorInvalidValue;
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !g.split) return e;
+  const dim3 fgrid(g.n_tiles, g.MT);
+  if (ev1)
+    hipExtLaunchKernelGGL(gemm_finish_kernel<KIND>, fgrid, block, 0, s, nullptr, ev1, 0, g);
+  else
+    hipLaunchKernelGGL(gemm_finish_kernel<KIND>, fgrid, block, 0, s, g);
+  return hipGetLastError();
+}
+
+// ---- weight packing.  Packed 16-byte item (tile, chunk, sub-tile q < 8,
+// k-step s < 2, lane l < 64) holds the 8 bf16 of weight row
+// tile_row(tile, 16 q + l % 16) at columns 64 chunk + 32 s + 8 (l / 16) ..
+// + 7; rows and columns past the matrix (padding) are zero.
+template <int KIND>
+__global__ __launch_bounds__(256) void pack_kernel(const bf16_t *__restrict__ src, u32x4 *__restrict__ dst,
+                                                   int N, int K, int rows_total, int kc_pad, long n_items) {
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_items;
+       i += (long)gridDim.x * blockDim.x) {
+    const int l = (int)(i & 63);
+    const long f = i >> 6;  // fragment ((tile kc_pad + chunk) 8 + q) 2 + s
+    const int s = (int)(f & 1), q = (int)((f >> 1) & 7);
+    const long tc = f >> 4;
+    const int chunk = (int)(tc % kc_pad), tile = (int)(tc / kc_pad);
+    const int row = tile_row<KIND>(tile, 16 * q + (l & 15), N);
+    const int col = chunk * KC + 32 * s + 8 * (l >> 4);
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (row < rows_total && col < K) v = *(const u32x4 *)(src + (size_t)row * K + col);
+    dst[i] = v;
+  }
+}
+
+template <int KIND>
+hipError_t launch_pack_kind(int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s) {
+  const int n_tiles = gemm_tiles_of(KIND, N), kc_pad = gemm_kc_pad_of(K);
+  const long n_items = (long)n_tiles * kc_pad * UNIT;
+  const int rows_total = KIND == GEMM_SWIGLU ? 2 * N : N;
+  const dim3 grid((unsigned)std::min<long>(8192, (n_items + 255) / 256)), block(256);
+  hipLaunchKernelGGL(pack_kernel<KIND>, grid, block, 0, s, src, (u32x4 *)dst, N, K, rows_total,
+                     kc_pad, n_items);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int gemm_tile_rows(int kind) { return kind == GEMM_RESID ? 64 : 128; }
+int gemm_tiles_of(int kind, int N) { return kind == GEMM_SWIGLU ? N / 64 : (N + BN - 1) / BN; }
 
-hipError_t launch_gemm_bf16(const GemmLaunch &g, int n_tiles, hipStream_t s) {
+int gemm_kc_pad_of(int K) { return ((K / KC + R - 1) / R) * R; }
+
+hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s) {
+  switch (kind) {
+    case GEMM_QKV: return launch_pack_kind<GEMM_QKV>(N, K, src, dst, s);
+    case GEMM_RESID: return launch_pack_kind<GEMM_RESID>(N, K, src, dst, s);
+    case GEMM_SWIGLU: return launch_pack_kind<GEMM_SWIGLU>(N, K, src, dst, s);
+    case GEMM_LOGITS: return launch_pack_kind<GEMM_LOGITS>(N, K, src, dst, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_bf16(const GemmLaunch &g, hipStream_t s) {
   switch (g.kind) {
-    case GEMM_QKV: return launch_kind<GEMM_QKV>(g, n_tiles, s);
-    case GEMM_RESID: return launch_kind<GEMM_RESID>(g, n_tiles, s);
-    case GEMM_SWIGLU: return launch_kind<GEMM_SWIGLU>(g, n_tiles, s);
-    case GEMM_LOGITS: return launch_kind<GEMM_LOGITS>(g, n_tiles, s);
+    case GEMM_QKV: return launch_kind<GEMM_QKV>(g, s);
+    case GEMM_RESID: return launch_kind<GEMM_RESID>(g, s);
+    case GEMM_SWIGLU: return launch_kind<GEMM_SWIGLU>(g, s);
+    case GEMM_LOGITS: return launch_kind<GEMM_LOGITS>(g, s);
   }
   return hipErrorInvalidValue;
 }

@@ -75,12 +75,14 @@ ppd_status check_model(const ppd_model *m) {
   if (m->dtype != PPD_F32 && m->dtype != PPD_BF16) return fail(PPD_EINVAL, "unknown dtype");
   if (m->dtype == PPD_BF16) {
     if (m->head_dim != 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need head_dim 128");
-    if (m->hidden % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need hidden % 64 == 0");
+    if (m->hidden % 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need hidden %% 128 == 0");
     if (m->ffn % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need ffn %% 64 == 0");
     if (m->n_heads * 8 > PPD_MAX_COUNTERS - kAttnCounterBase)
       return fail(PPD_EUNSUPPORTED, "too many heads (max %d)", (PPD_MAX_COUNTERS - kAttnCounterBase) / 8);
     if ((m->vocab + 127) / 128 > kAttnCounterBase)
       return fail(PPD_EUNSUPPORTED, "vocab too large (max %d)", 128 * kAttnCounterBase);
+    if (m->ffn / 64 > kAttnCounterBase)
+      return fail(PPD_EUNSUPPORTED, "ffn too large (max %d)", 64 * kAttnCounterBase);
   }
   if (!m->tok_emb || !m->lm_head || !m->final_norm || (m->n_prompt > 0 && !m->prompt_emb))
     return fail(PPD_EINVAL, "embedding, LM head and final norm pointers must be set");
@@ -96,30 +98,43 @@ ppd_status check_model(const ppd_model *m) {
 
 int qkv_rows(const ppd_model *m) { return (m->n_heads + 2 * m->n_kv_heads) * m->head_dim; }
 
-// ---- launch-shape heuristics (also used to size the workspace)
+// ---- launch shapes (also used to size the workspace)
 
-// split-K factor: about one workgroup per compute unit, each split at least
-// 4 chunks of 64
-int choose_sk(int n_tiles, int K) {
-  const int nks = K / 32;
-  // more splits cost partial traffic and fixups, fewer leave compute units
-  // without a weight stream (measured on 7B shapes)
-  int sk = std::max(1, kCUs / n_tiles);
-  sk = std::min(sk, std::max(1, nks / 8));
-  return std::max(1, std::min(sk, 16));
-}
+// Partition of one skinny GEMM (see GemmLaunch).  A compute unit's load path
+// streams ~35 GB/s, so one whole 128-row tile per workgroup reaches the HBM
+// rate only with at least ~160 tiles; smaller GEMMs are split over all CUs.
+constexpr int kWholeTileMin = 160;
 
 struct GemmShape {
-  int n_tiles, K, rows;  // rows per tile
+  int kind, N, K;
+  int n_tiles, kc_pad, G, maxc, split;
 };
 
-void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
-  out[0] = {qkv_rows(m) / 128, m->hidden, 128};          // QKV: one head per tile
-  out[1] = {m->hidden / 64, m->n_heads * 128, 64};       // output projection
-  out[2] = {m->ffn / 64, m->hidden, 128};                // gate/up: 64 features per tile
-  out[3] = {m->hidden / 64, m->ffn, 64};                 // down projection
-  out[4] = {(m->vocab + 127) / 128, m->hidden, 128};     // LM head
+GemmShape gemm_shape(int kind, int N, int K) {
+  GemmShape g{kind, N, K, gemm_tiles_of(kind, N), gemm_kc_pad_of(K), 0, 1, 0};
+  const long Ng = (long)g.n_tiles * g.kc_pad / PPD_GEMM_RING;
+  g.split = g.n_tiles < kWholeTileMin;
+  g.G = g.split ? (int)std::min<long>(kCUs, Ng) : g.n_tiles;
+  for (int t = 0; t < g.n_tiles; ++t) {
+    const long x0 = (long)t * g.kc_pad / PPD_GEMM_RING, x1 = (long)(t + 1) * g.kc_pad / PPD_GEMM_RING;
+    g.maxc = std::max(g.maxc, gemm_group_owner(Ng, g.G, x1 - 1) - gemm_group_owner(Ng, g.G, x0) + 1);
+  }
+  if (g.G == g.n_tiles) g.split = 0;  // one whole tile per workgroup
+  return g;
 }
+
+enum { SH_QKV = 0, SH_O = 1, SH_GATE_UP = 2, SH_DOWN = 3, SH_LM = 4 };
+
+void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
+  out[SH_QKV] = gemm_shape(GEMM_QKV, qkv_rows(m), m->hidden);        // one head per tile
+  out[SH_O] = gemm_shape(GEMM_RESID, m->hidden, m->n_heads * 128);  // output projection
+  out[SH_GATE_UP] = gemm_shape(GEMM_SWIGLU, m->ffn, m->hidden);     // 64 features per tile
+  out[SH_DOWN] = gemm_shape(GEMM_RESID, m->hidden, m->ffn);         // down projection
+  out[SH_LM] = gemm_shape(GEMM_LOGITS, m->vocab, m->hidden);        // LM head
+}
+
+// bytes of a tile partial of T_pad tokens: 128 rows x T_pad fp32
+size_t tile_partial_floats(int Tp) { return (size_t)128 * Tp; }
 
 constexpr int kAttnMaxSplits = 8;
 
@@ -162,7 +177,7 @@ WsLayout layout_of(const ppd_model *m, int T) {
   w.counters = take(sizeof(uint32_t) * PPD_MAX_COUNTERS);
   w.x = take(sizeof(float) * Tp * H);
   w.xg = take(es * Tp * H + sizeof(float) * Tp);
-  w.max_ss = std::max(1, H / 64);
+  w.max_ss = std::max(1, H / PPD_GEMM_BN);
   w.ss = take(sizeof(float) * w.max_ss * Tp);
   w.q = take(es * Tp * nh * d);
   w.attn_o = take(es * Tp * nh * d);
@@ -179,10 +194,9 @@ WsLayout layout_of(const ppd_model *m, int T) {
   if (m->dtype == PPD_BF16) {
     GemmShape gs[5];
     gemm_shapes(m, gs);
-    for (int i = 0; i < 5; ++i) {
-      const int sk = choose_sk(gs[i].n_tiles, gs[i].K);
-      if (sk > 1) part = std::max(part, (size_t)gs[i].n_tiles * sk * 16 * gs[i].rows * (Tp / 16));
-    }
+    for (int i = 0; i < 5; ++i)
+      if (gs[i].split)
+        part = std::max(part, (size_t)gs[i].n_tiles * gs[i].maxc * tile_partial_floats(Tp));
   }
   w.max_part_floats = part;
   w.gemm_part = take(sizeof(float) * part);
@@ -209,7 +223,7 @@ ppd_status check_kv(const ppd_model *m, const ppd_kv *kv) {
 ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const int32_t *ids,
                      const int32_t *depth, const uint64_t *mask, void *ws, const WsLayout &w,
                      float *logits, int32_t *pred, hipStream_t s) {
-  const int H = m->hidden, F = m->ffn, nh = m->n_heads, nkv = m->n_kv_heads;
+  const int H = m->hidden, nh = m->n_heads, nkv = m->n_kv_heads;
   const int Tp = t_pad_of(T), MT = Tp / 16;
   const int cap = kv->capacity;
   uint32_t *status = at<uint32_t>(ws, w.status);
@@ -225,8 +239,16 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
   float2 *rope = at<float2>(ws, w.rope);
   GemmShape gs[5];
   gemm_shapes(m, gs);
-  int sk[5];
-  for (int i = 0; i < 5; ++i) sk[i] = choose_sk(gs[i].n_tiles, gs[i].K);
+  auto shape = [&](GemmLaunch &g, const GemmShape &sh) {
+    g.kind = sh.kind;
+    g.N = sh.N;
+    g.K = sh.K;
+    g.n_tiles = sh.n_tiles;
+    g.kc_pad = sh.kc_pad;
+    g.G = sh.G;
+    g.maxc = sh.maxc;
+    g.split = sh.split;
+  };
 
   PPD_TRY_HIP(launch_rope_table(depth, T, L, m->head_dim, m->rope_base, rope, s));
   PPD_TRY_HIP(launch_embed(PPD_BF16, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
@@ -243,18 +265,14 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     g.T = T;
     g.MT = MT;
     g.part = part;
-    g.counters = counters;
     g.inv_h = inv_h;
     g.eps = m->rms_eps;
     g.status = status;
     g.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
     // QKV + RoPE + cache stores
-    g.kind = GEMM_QKV;
+    shape(g, gs[SH_QKV]);
     g.W = (const bf16_t *)m->w_qkv[l];
     g.A = xg;
-    g.N = qkv_rows(m);
-    g.K = H;
-    g.sk = sk[0];
     g.ss = ss;
     g.n_ss = n_ss;
     g.rope = rope;
@@ -266,7 +284,7 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     g.cap = cap;
     g.L = L;
     timer_events(TK_QKV, &g.ev_start, &g.ev_stop);
-    PPD_TRY_HIP(launch_gemm_bf16(g, gs[0].n_tiles, s));
+    PPD_TRY_HIP(launch_gemm_bf16(g, s));
     // tree attention
     AttnLaunch a{};
     a.q = q;
@@ -290,60 +308,47 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     PPD_TRY_HIP(launch_attn_bf16(a, s));
     // O projection + residual; operand of the MLP norm
     GemmLaunch o = g;
-    o.kind = GEMM_RESID;
+    shape(o, gs[SH_O]);
     o.W = (const bf16_t *)m->w_o[l];
     o.A = attn_o;
-    o.N = H;
-    o.K = nh * 128;
-    o.sk = sk[1];
     o.x = x;
     o.xg = xg;
     o.gain = (const bf16_t *)m->mlp_norm[l];
     o.ss_out = ss;
     timer_events(TK_O, &o.ev_start, &o.ev_stop);
-    PPD_TRY_HIP(launch_gemm_bf16(o, gs[1].n_tiles, s));
-    n_ss = gs[1].n_tiles;
+    PPD_TRY_HIP(launch_gemm_bf16(o, s));
+    n_ss = gs[SH_O].n_tiles;
     // gate/up + SwiGLU
     GemmLaunch u = g;
-    u.kind = GEMM_SWIGLU;
+    shape(u, gs[SH_GATE_UP]);
     u.W = (const bf16_t *)m->w_gate_up[l];
     u.A = xg;
-    u.N = F;
-    u.K = H;
-    u.sk = sk[2];
     u.ss = ss;
     u.n_ss = n_ss;
     u.act = act;
     timer_events(TK_GATEUP, &u.ev_start, &u.ev_stop);
-    PPD_TRY_HIP(launch_gemm_bf16(u, gs[2].n_tiles, s));
+    PPD_TRY_HIP(launch_gemm_bf16(u, s));
     // down projection + residual; operand of the next norm
     GemmLaunch dn = g;
-    dn.kind = GEMM_RESID;
+    shape(dn, gs[SH_DOWN]);
     dn.W = (const bf16_t *)m->w_down[l];
     dn.A = act;
-    dn.N = H;
-    dn.K = F;
-    dn.sk = sk[3];
     dn.x = x;
     dn.xg = xg;
     dn.gain = (const bf16_t *)(l + 1 < m->n_layers ? m->attn_norm[l + 1] : m->final_norm);
     dn.ss_out = ss;
     timer_events(TK_DOWN, &dn.ev_start, &dn.ev_stop);
-    PPD_TRY_HIP(launch_gemm_bf16(dn, gs[3].n_tiles, s));
-    n_ss = gs[3].n_tiles;
+    PPD_TRY_HIP(launch_gemm_bf16(dn, s));
+    n_ss = gs[SH_DOWN].n_tiles;
   }
   // final norm + LM head + greedy partials
   GemmLaunch lm{};
-  lm.kind = GEMM_LOGITS;
+  shape(lm, gs[SH_LM]);
   lm.W = (const bf16_t *)m->lm_head;
   lm.A = xg;
-  lm.N = m->vocab;
-  lm.K = H;
   lm.T = T;
   lm.MT = MT;
-  lm.sk = sk[4];
   lm.part = part;
-  lm.counters = counters;
   lm.ss = ss;
   lm.n_ss = n_ss;
   lm.inv_h = inv_h;
@@ -353,8 +358,8 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
   lm.status = status;
   lm.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
   timer_events(TK_LM, &lm.ev_start, &lm.ev_stop);
-  PPD_TRY_HIP(launch_gemm_bf16(lm, gs[4].n_tiles, s));
-  PPD_TRY_HIP(launch_argmax_final(amax, gs[4].n_tiles, T, Tp, pred, status, s));
+  PPD_TRY_HIP(launch_gemm_bf16(lm, s));
+  PPD_TRY_HIP(launch_argmax_final(amax, gs[SH_LM].n_tiles, T, Tp, pred, status, s));
   return PPD_OK;
 }
 
@@ -399,6 +404,32 @@ ppd_status step_f32(const ppd_model *m, const ppd_kv *kv, int L, int T, const in
   PPD_TRY_HIP(launch_f32_matmul_scaled(xg, (const float *)m->lm_head, T, m->vocab, H, r, lg, s));
   PPD_TRY_HIP(launch_f32_argmax(lg, T, m->vocab, pred, status, s));
   return PPD_OK;
+}
+
+// GEMM kind and output-row count of a weight given as a row-major
+// [rows][cols] matrix
+ppd_status pack_args(int kind, int rows, int cols, int *gk, int *N) {
+  if (rows < 1 || cols < 1) return fail(PPD_EINVAL, "weight sizes must be positive");
+  if (cols % 64) return fail(PPD_EUNSUPPORTED, "packed weights need cols %% 64 == 0");
+  switch (kind) {
+    case PPD_W_QKV:
+      if (rows % 128) return fail(PPD_EUNSUPPORTED, "w_qkv needs rows %% 128 == 0 (head_dim 128)");
+      *gk = GEMM_QKV, *N = rows;
+      return PPD_OK;
+    case PPD_W_O:
+    case PPD_W_DOWN:
+      if (rows % 128) return fail(PPD_EUNSUPPORTED, "w_o / w_down need rows (hidden) %% 128 == 0");
+      *gk = GEMM_RESID, *N = rows;
+      return PPD_OK;
+    case PPD_W_GATE_UP:
+      if (rows % 128) return fail(PPD_EUNSUPPORTED, "w_gate_up needs rows (2 ffn) %% 128 == 0");
+      *gk = GEMM_SWIGLU, *N = rows / 2;
+      return PPD_OK;
+    case PPD_W_LM_HEAD:
+      *gk = GEMM_LOGITS, *N = rows;
+      return PPD_OK;
+  }
+  return fail(PPD_EINVAL, "unknown weight kind %d", kind);
 }
 
 }  // namespace
@@ -521,5 +552,22 @@ ppd_status ppd_set_kernel_timer(int32_t kind, void *const *start_events, void *c
 }
 
 const char *ppd_last_error(void) { return g_err.c_str(); }
+
+size_t ppd_packed_weight_bytes(int32_t kind, int32_t rows, int32_t cols) {
+  int gk, N;
+  if (pack_args(kind, rows, cols, &gk, &N) != PPD_OK) return 0;
+  return (size_t)gemm_tiles_of(gk, N) * gemm_kc_pad_of(cols) * PPD_GEMM_BN * 64 * sizeof(bf16_t);
+}
+
+ppd_status ppd_pack_weight(int32_t kind, int32_t rows, int32_t cols, const void *src, void *dst,
+                           void *stream) {
+  int gk, N;
+  ppd_status st = pack_args(kind, rows, cols, &gk, &N);
+  if (st != PPD_OK) return st;
+  if (!src || !dst) return fail(PPD_EINVAL, "NULL weight pointer");
+  PPD_TRY_HIP(launch_pack_weight(gk, N, cols, (const bf16_t *)src, (bf16_t *)dst,
+                                 (hipStream_t)stream));
+  return PPD_OK;
+}
 
 }  // extern "C"

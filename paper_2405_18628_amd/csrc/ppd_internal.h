@@ -79,22 +79,40 @@ struct WsLayout {
 };
 
 #define PPD_MAX_COUNTERS 8192
-#define PPD_GEMM_BN 64         // output rows per GEMM tile
 #define PPD_ATTN_MAX_SPLITS 64
 
 // ---------------------------------------------------------------------------
 // kernel launchers (defined in the .hip files, called by the host driver)
 
+// Skinny GEMM partition.  Tiles of 128 output rows; each tile's K is cut in
+// 64-column chunks, padded with zero chunks to kc_pad, a multiple of
+// PPD_GEMM_RING; a group is PPD_GEMM_RING consecutive chunks of one tile.
+// Unit u = tile * kc_pad + chunk.  Workgroup w of G owns the contiguous
+// groups [Ng w / G, Ng (w + 1) / G), Ng = n_tiles * kc_pad / PPD_GEMM_RING,
+// so every workgroup streams an equal share and tile boundaries fall between
+// groups.  G = n_tiles: one whole tile per workgroup, finished in place;
+// otherwise (split) every workgroup stores the partial sums of its tile
+// segments and a finish kernel adds them in workgroup order.
+#ifndef PPD_GEMM_RING
+#define PPD_GEMM_RING 4
+#endif
+#define PPD_GEMM_BN 128
+__host__ __device__ inline long gemm_group_lo(long Ng, int G, int w) { return Ng * w / G; }
+// workgroup owning group x
+__host__ __device__ inline int gemm_group_owner(long Ng, int G, long x) {
+  return (int)(((x + 1) * G - 1) / Ng);
+}
+
 struct GemmLaunch {
   // operands
-  const bf16_t *W;  // [N][K] (SwiGLU: gate rows then up rows, 2F x K)
-  const bf16_t *A;  // [T_pad][K]
+  const bf16_t *W;      // packed weight (ppd_pack_weight)
+  const bf16_t *A;      // [T_pad][K]
   const bf16_t *zeros;  // 16 zero bytes in global memory
-  int N, K, T, MT;  // N = output rows (SwiGLU: F), MT = T_pad / 16
-  int kind;         // GemmKind
-  int sk;           // split-K factor
-  float *part;
-  uint32_t *counters;
+  int N, K, T, MT;      // N = output rows (SwiGLU: F), MT = T_pad / 16
+  int kind;             // GemmKind
+  int n_tiles, kc_pad, G, maxc;  // partition (see above); maxc: max workgroups per tile
+  int split;            // G != n_tiles: partial sums + finish kernel
+  float *part;          // split: [n_tiles][maxc][8 MT 64][4] partial sums
   // epilogue inputs
   const float *ss;  // norm partials for row scaling (QKV, SwiGLU, LOGITS)
   int n_ss;
@@ -115,12 +133,17 @@ struct GemmLaunch {
   float *logits;       // [T][N] or null
   float2 *amax;        // [n_tiles][T_pad]
   uint32_t *status;
-  void *ev_start, *ev_stop;  // optional events at the dispatch's start / end
+  void *ev_start, *ev_stop;  // optional events at the first dispatch's start / last one's end
 };
 
 enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_SWIGLU = 2, GEMM_LOGITS = 3 };
 
-hipError_t launch_gemm_bf16(const GemmLaunch &g, int n_tiles, hipStream_t s);
+// packed layout of a weight for GEMM kind `kind` with N output rows (SwiGLU:
+// F features, 2F rows) and K columns
+int gemm_tiles_of(int kind, int N);
+int gemm_kc_pad_of(int K);
+hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s);
+hipError_t launch_gemm_bf16(const GemmLaunch &g, hipStream_t s);
 
 struct AttnLaunch {
   const bf16_t *q;      // [T_pad][nh][d]

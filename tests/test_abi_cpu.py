@@ -118,3 +118,27 @@ def test_accept_and_compact_reject_before_enqueue():
     assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 256, f, f, None) == ppd.PPD_ECAPACITY
     assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 10, None, f, None) == ppd.PPD_EINVAL
     assert L.ppd_workspace_init(None, 0, None) == ppd.PPD_EWORKSPACE
+
+
+def test_packed_weight_sizes_and_rejections():
+    """Packed size = tiles x (64-column chunks rounded up to a multiple of 4)
+    x 128 rows x 64 columns x 2 bytes; rows past the matrix (the LM head's
+    last tile) and padding chunks are counted, nothing else."""
+    L = ppd.lib()
+    unit = 128 * 64 * 2
+    cases = [(ppd.PPD_W_QKV, 3 * 4096, 4096, 96 * 64), (ppd.PPD_W_O, 4096, 4096, 32 * 64),
+             (ppd.PPD_W_GATE_UP, 2 * 11008, 4096, 172 * 64), (ppd.PPD_W_DOWN, 4096, 11008, 32 * 172),
+             (ppd.PPD_W_LM_HEAD, 32000, 4096, 250 * 64), (ppd.PPD_W_LM_HEAD, 1000, 512, 8 * 8),
+             (ppd.PPD_W_DOWN, 512, 1344, 4 * 24), (ppd.PPD_W_GATE_UP, 2 * 1344, 512, 21 * 8)]
+    for kind, rows, cols, units in cases:
+        assert ppd.ppd_packed_weight_bytes(kind, rows, cols) == units * unit, (kind, rows, cols)
+    for kind, rows, cols in [(ppd.PPD_W_QKV, 3 * 4096, 4000), (ppd.PPD_W_QKV, 3 * 4096 - 64, 4096),
+                             (ppd.PPD_W_O, 4000, 4096), (ppd.PPD_W_GATE_UP, 2 * 1000, 512),
+                             (ppd.PPD_W_LM_HEAD, 0, 512), (5, 128, 128), (-1, 128, 128)]:
+        assert L.ppd_packed_weight_bytes(kind, rows, cols) == 0
+        assert ppd.ppd_last_error()
+    f = 0x4000
+    assert L.ppd_pack_weight(ppd.PPD_W_O, 512, 512, None, f, None) == ppd.PPD_EINVAL
+    assert L.ppd_pack_weight(ppd.PPD_W_O, 512, 512, f, None, None) == ppd.PPD_EINVAL
+    assert L.ppd_pack_weight(ppd.PPD_W_O, 500, 512, f, f, None) == ppd.PPD_EUNSUPPORTED
+    assert L.ppd_pack_weight(9, 512, 512, f, f, None) == ppd.PPD_EINVAL

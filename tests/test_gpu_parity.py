@@ -210,3 +210,49 @@ def test_tiny_multistep_lossless(tiny_case):
     assert emitted == ref
     case.k.copy_(k0)
     case.v.copy_(v0)
+
+
+def _expected_packing(w, kind):
+    """The packed layout of include/ppd.h, written out with numpy indexing:
+    item (tile, chunk, q, s, lane) = row r(tile, 16 q + lane % 16), columns
+    64 chunk + 32 s + 8 (lane // 16) .. + 7; zeros past the matrix."""
+    rows, cols = w.shape
+    kc = -(-(cols // 64) // 4) * 4
+    if kind == ppd.PPD_W_GATE_UP:
+        F = rows // 2
+        n_tiles = F // 64
+        tr = np.concatenate([np.arange(64), F + np.arange(64)])[None, :] + 64 * np.arange(n_tiles)[:, None]
+    else:
+        n_tiles = -(-rows // 128)
+        tr = np.arange(128)[None, :] + 128 * np.arange(n_tiles)[:, None]
+    wp = np.zeros((n_tiles * 128 + rows, kc * 64), dtype=w.dtype)
+    wp[:rows, :cols] = w
+    tr = np.where(tr < rows, tr, rows + 1)          # padding rows read the zero block
+    lane = np.arange(64)
+    out = np.zeros((n_tiles, kc, 8, 2, 64, 8), dtype=w.dtype)
+    for q in range(8):
+        rr = tr[:, 16 * q + lane % 16]              # [tiles][64]
+        for s in range(2):
+            for c in range(kc):
+                col = 64 * c + 32 * s + 8 * (lane // 16)
+                idx = col[:, None] + np.arange(8)[None, :]      # [64][8]
+                out[:, c, q, s] = wp[rr[:, :, None], idx[None, :, :]]
+    return out
+
+
+@pytest.mark.parametrize("kind,rows,cols", [(ppd.PPD_W_LM_HEAD, 1000, 512),
+                                            (ppd.PPD_W_GATE_UP, 2 * 1344, 512),
+                                            (ppd.PPD_W_DOWN, 512, 1344),
+                                            (ppd.PPD_W_QKV, 6 * 128, 256)])
+def test_pack_weight_layout(kind, rows, cols):
+    say(f"[pack] kind={kind} {rows}x{cols}")
+    g = torch.Generator().manual_seed(rows * 7 + cols)
+    w = torch.randint(0, 1 << 16, (rows, cols), generator=g, dtype=torch.int32)
+    w = (w & 0x7F7F).to(torch.int16)                    # finite bf16 bit patterns
+    src = w.view(torch.bfloat16).cuda()
+    packed = ppd.ppd_pack_weight(kind, src)
+    torch.cuda.synchronize()
+    got = packed.cpu().view(torch.int16).numpy()
+    exp = _expected_packing(w.numpy(), kind).reshape(-1)
+    assert got.shape == exp.shape
+    assert np.array_equal(got, exp)
