@@ -158,8 +158,10 @@ typedef struct {
  * nodes and caches of up to max_len positions.  0 on invalid input. */
 size_t ppd_workspace_bytes(const ppd_model *model, int32_t t_max, int32_t max_len);
 
-/* Zero the workspace's counters and status word (enqueued on `stream`).  Call
- * once after allocating a workspace; later calls keep it consistent. */
+/* Zero the workspace's header -- the status word and a line of zeros the
+ * kernels read in place of padding (enqueued on `stream`).  Call once after
+ * allocating a workspace; later calls never write the header except for
+ * status bits. */
 ppd_status ppd_workspace_init(void *ws, size_t ws_bytes, void *stream);
 
 /*

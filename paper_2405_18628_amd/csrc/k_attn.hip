@@ -6,20 +6,19 @@
 // (written at L + i by the QKV epilogue), visible to node t iff bit i of its
 // ancestor mask is set.  The key range is cut into 32-key blocks.
 //
-// Work decomposition.  A workgroup owns one head h, one tile of 16 queries
-// and one of KS contiguous key splits; its four waves cut that split again
-// into four contiguous runs and each keeps its own online softmax.  A wave
-// streams its run through a private two-slot LDS ring with direct-to-LDS
-// transfers (global_load_lds_dwordx4), so waves never wait on each other
-// inside the loop: block i+1 is requested before block i is waited for.
-// At the end the four waves are merged through LDS; with KS > 1 the merged
-// (O, m, l) of each split is published and the last split of the (head,
-// query tile) to finish (atomic ticket) merges the splits in split order.
-// The query tiles of one (head, split) get workgroup ids congruent mod 8,
-// which the dispatcher places on one XCD, so they share its L2 and the
-// keys/values cross HBM about once.
+// Work decomposition.  The step is bound by reading the keys and values, and
+// a compute unit's load path sustains only ~35 GB/s, so the kernel reads
+// each key/value block once per compute unit and spreads the blocks over all
+// CUs: a workgroup owns one head h and one of KS contiguous key splits, and
+// all T queries.  The four waves load each block cooperatively (16-byte
+// non-temporal loads into a register ring up to 8 blocks ahead), stage
+// it in a double-buffered LDS slot, and each wave multiplies it with its own
+// 16-query tiles (tiles w and w + 4), keeping one online softmax per query.
+// With KS > 1 each wave stores its tiles' (O, m, l) and a merge kernel adds
+// the splits in split order; with KS = 1 the waves finish in place.
 //
-// Per 32-key block, on the matrix cores (v_mfma_f32_16x16x32_bf16):
+// Per 32-key block and query tile, on the matrix cores
+// (v_mfma_f32_16x16x32_bf16):
 //   S^T[key][query] = K Q^T      keys are the 16-row A operand (LDS),
 //                                queries the B operand (registers)
 //   O^T[d][query]  += V^T P^T    values (stored position-minor, so V^T rows
@@ -29,21 +28,18 @@
 //                                8 (m / 4) + 4 kt + (m % 4), so each lane's 8
 //                                probabilities are 8 consecutive keys, i.e. a
 //                                valid B operand.
-// Softmax runs in fp32 in the log2 domain; P enters the PV product as the sum
-// of two bf16 parts (hi, lo), i.e. to about 16 significant bits.
+// Softmax runs in fp32 in the log2 domain against a lazily moved reference
+// (rescaling only when a block's maximum exceeds it by more than 2^8); P
+// enters the PV product as the sum of two bf16 parts (hi, lo), i.e. to about
+// 16 significant bits.
 #include "ppd_internal.h"
 
 namespace {
 
-constexpr int KSLOT = 8192;               // 32 keys x 256 bytes
-constexpr int VSLOT = 8192;               // 128 dims x 64 bytes (32 keys)
-constexpr int SLOT = KSLOT + VSLOT;       // one block in LDS
-constexpr int WAVE_LDS = SLOT;            // per wave (also holds its merge rows)
-constexpr int OROW = 132;                 // merge row: 128 dims + padding (floats)
-#ifndef PPD_ATTN_RING
-#define PPD_ATTN_RING 2
-#endif
-constexpr int RING = PPD_ATTN_RING;       // blocks in flight per wave (registers)
+constexpr int KSLOT = 8192;          // 32 keys x 256 bytes
+constexpr int VSLOT = 8192;          // 128 dims x 64 bytes (32 keys)
+constexpr int SLOT = KSLOT + VSLOT;  // one block in LDS
+constexpr int OROW = PPD_ATTN_OROW;  // partial row: 128 dims, m, l, padding (floats)
 
 // LDS row of the K slot holding key j (j < 32) of a block: MFMA row m of key
 // tile kt holds key 8 (m / 4) + 4 kt + (m % 4)
@@ -52,315 +48,371 @@ __device__ __forceinline__ int row_of_key(int j) {
   return kt * 16 + a * 4 + e;
 }
 
-__global__ __launch_bounds__(256, 1) void attn_bf16_kernel(AttnLaunch p) {
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[4 * WAVE_LDS];
-  __shared__ float ml_s[4][16][2];
-  __shared__ int last_s;
+// s_waitcnt immediate for "at most n vector-memory operations outstanding"
+// (expcnt and lgkmcnt left at their maxima, i.e. not waited on)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+// one wave's state for one 16-query tile
+struct QTile {
+  u32x4 qf[4];   // queries (B operand), dims 32 ds + 8 (lane / 16) .. + 7
+  uint64_t mk0, mk1;
+  floatx4 o[8];  // O^T tiles: dims 16 dt + 4 (lane / 16) + e, query lane % 16
+  float m_run;   // reference of the exponentials (log2 domain, scaled)
+  float l_run;
+};
+
+// Eight waves: wave w works on query tiles (w % 4) + 4 i (i < NQ) and on the
+// blocks of parity w / 4, so two waves share each SIMD and hide each other's
+// latencies; the two parities are merged at the end.  RING: block pairs
+// requested ahead.
+template <int NQ, int RING>
+__global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[4 * SLOT];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qw = wave & 3, par = wave >> 2;
   const int lr = lane & 15, lg = lane >> 4;
   const int KS = p.splits;
-  const int G = p.nh * KS;
-  // workgroup id -> (group g = (head, split), query tile qt)
-  const int x8 = blockIdx.x & 7, rr = blockIdx.x >> 3;
-  const int qt = rr % p.MT;
-  const int g = (rr / p.MT) * 8 + x8;
-  if (g >= G) return;
-  const int h = g / KS, ks = g % KS;
+  const int h = blockIdx.x / KS, ks = blockIdx.x % KS;
   const int kvh = h / (p.nh / p.nkv);
   const int n_keys = p.L + p.T;
   const int nblk = (n_keys + 31) >> 5;
   const int b0 = min(nblk, ks * p.chunk), b1 = min(nblk, b0 + p.chunk);
-  const int cpw = (b1 - b0 + 3) >> 2;
-  const int wvs = __builtin_amdgcn_readfirstlane(wave);  // wave index as a scalar
-  const int wb0 = min(b1, b0 + wvs * cpw), wb1 = min(b1, wb0 + cpw);
-  const int nw = wb1 - wb0;
+  const int nb = b1 - b0;
+  const int nsteps = (nb + 1) >> 1;  // block pairs
   const bf16_t *kbase = p.kc + (size_t)kvh * p.cap * 128;
   const bf16_t *vbase = p.vc + (size_t)kvh * 128 * p.cap;
   const u32x4 *zp = (const u32x4 *)p.zeros;
-  unsigned char *wl = lds + wave * WAVE_LDS;
 
-  // ---- this lane's queries (B operand) and ancestor masks
-  const int tq_l = qt * 16 + lr;
-  const bool qlive = tq_l < p.T;
-  u32x4 qf[4];
+  // ---- this wave's query tiles that exist
+  const int n_live = min(NQ, (p.MT - qw + 3) / 4);
+  QTile qt[NQ];
 #pragma unroll
-  for (int ds = 0; ds < 4; ++ds)
-    qf[ds] = *(qlive ? (const u32x4 *)(p.q + ((size_t)tq_l * p.nh + h) * 128 + ds * 32 + lg * 8) : zp);
-  const uint64_t mk0 = qlive ? p.mask[2 * tq_l] : 0ull;
-  const uint64_t mk1 = qlive ? p.mask[2 * tq_l + 1] : 0ull;
-
-  // ---- register ring.  A block is loaded with 16-byte non-temporal loads:
-  // K rows are contiguous (8 KB per block), lane + 64 i covers 16-byte chunk
-  // c of it (key c / 16, column c % 16); V^T chunk c is dim row c / 4, keys
-  // 8 (c % 4) .. + 7 of the block.
-  u32x4 kr[RING][8], vr[RING][8];
-  // Past its run a wave re-reads its last block (any in-bounds block does:
-  // the data is never staged), so every iteration issues the same loads.
-  const int b_last = wb1 > 0 ? wb1 - 1 : 0;
-  auto load = [&](int b, u32x4 (&kd)[8], u32x4 (&vd)[8]) {
-    const int bb = min(b, b_last);
-    const u32x4 *kb = (const u32x4 *)(kbase + (size_t)bb * 32 * 128);
+  for (int i = 0; i < NQ; ++i) {
+    const int tq = (qw + 4 * i) * 16 + lr;
+    const bool qlive = tq < p.T;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) kd[i] = __builtin_nontemporal_load(kb + lane + 64 * i);
+    for (int ds = 0; ds < 4; ++ds)
+      qt[i].qf[ds] = *(qlive ? (const u32x4 *)(p.q + ((size_t)tq * p.nh + h) * 128 + ds * 32 + lg * 8) : zp);
+    qt[i].mk0 = qlive ? p.mask[2 * tq] : 0ull;
+    qt[i].mk1 = qlive ? p.mask[2 * tq + 1] : 0ull;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = lane + 64 * i;
-      vd[i] = __builtin_nontemporal_load(
-          (const u32x4 *)(vbase + (size_t)(c >> 2) * p.cap + bb * 32 + (c & 3) * 8));
-    }
-  };
-  // Block b -> this wave's LDS slot, swizzled (K: physical 16-byte column =
-  // logical ^ (row % 16); V^T: logical ^ ((row / 4) % 4)); keys past the
-  // last valid one are cleared (value groups; key rows are masked anyway)
-  // LDS byte offsets of this lane's chunks (the same for every block)
-  int kofs[8], vofs[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int c = lane + 64 * i;
-    const int R = row_of_key(c >> 4);
-    kofs[i] = R * 256 + (((c & 15) ^ (R & 15)) * 16);
-    const int r = c >> 2, cv = c & 3;
-    vofs[i] = KSLOT + r * 64 + ((cv ^ ((r >> 2) & 3)) * 16);
+    for (int dt = 0; dt < 8; ++dt) qt[i].o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    qt[i].m_run = -INFINITY;
+    qt[i].l_run = 0.f;
   }
-  const int vkey = (lane & 3) * 8;  // first key of this lane's value chunks
-  auto stage = [&](int b, const u32x4 (&kd)[8], const u32x4 (&vd)[8]) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) *(u32x4 *)(wl + kofs[i]) = kd[i];
-    const int nv = n_keys - b * 32;  // valid keys in this block (may exceed 32)
-    if (nv >= 32) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) *(u32x4 *)(wl + vofs[i]) = vd[i];
-    } else {
-      const int keep_n = nv - vkey;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        u32x4 v = vd[i];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const uint32_t keep = (2 * w < keep_n ? 0xffffu : 0u) | (2 * w + 1 < keep_n ? 0xffff0000u : 0u);
-          v[w] &= keep;
-        }
-        *(u32x4 *)(wl + vofs[i]) = v;
-      }
-    }
-  };
-
-  floatx4 o[8];
-#pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
-
-#pragma unroll
-  for (int j = 0; j < RING; ++j) load(wb0 + j, kr[j], vr[j]);
   __builtin_amdgcn_sched_barrier(0);
 
-  for (int c0 = 0; c0 < nw; c0 += RING) {
+  // ---- cooperative loads of a block pair (64 keys), whole 128-byte lines:
+  // K chunk c = tid + 512 i (i < 2) of the pair's 16 KB is key c / 16,
+  // column c % 16; V^T chunk c is dim row c / 8, keys 8 (c % 8) .. + 7 of the
+  // pair.  Key rows past the cache capacity are clamped into it (such keys
+  // are never visible, and their values are cleared when staged).  Past the
+  // split the last pair is re-read, so every iteration issues the same loads.
+  const int b_last = nb > 0 ? b1 - 1 : 0;
+  u32x4 kr[RING][2], vr[RING][2];
+  auto request = [&](int st, u32x4(&kd)[2], u32x4(&vd)[2]) {
+    const int kp0 = min(b0 + 2 * st, b_last) * 32;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + 512 * i;
+      const int key = min(kp0 + (c >> 4), p.cap - 1);
+      kd[i] = __builtin_nontemporal_load((const u32x4 *)(kbase + (size_t)key * 128 + (c & 15) * 8));
+      const int g0 = min(kp0 + (c & 7) * 8, p.cap - 8);
+      vd[i] = __builtin_nontemporal_load((const u32x4 *)(vbase + (size_t)(c >> 3) * p.cap + g0));
+    }
+  };
+  // LDS destinations of this thread's chunks: block parity and byte offset
+  // within the block slot.  K row R = row_of_key(key % 32), physical 16-byte
+  // column = logical ^ (R % 16); V^T row = dim, physical column = logical ^
+  // ((dim / 4) % 4)
+  int kofs[2], vofs[2], kpar[2], vpar[2], vgrp[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = tid + 512 * i;
+    const int k = c >> 4, R = row_of_key(k & 31);
+    kpar[i] = k >> 5;
+    kofs[i] = R * 256 + (((c & 15) ^ (R & 15)) * 16);
+    const int d = c >> 3, g = c & 7;
+    vpar[i] = g >> 2;
+    vgrp[i] = g & 3;
+    vofs[i] = KSLOT + d * 64 + (((g & 3) ^ ((d >> 2) & 3)) * 16);
+  }
+  // block index of pair st, parity q (past the split: beyond the last key)
+  auto block_of = [&](int st, int q) { return 2 * st + q < nb ? b0 + 2 * st + q : nblk + 1; };
+  auto stage = [&](int st, const u32x4(&kd)[2], const u32x4(&vd)[2]) {
+    unsigned char *base = lds + (st & 1) * 2 * SLOT;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      *(u32x4 *)(base + kpar[i] * SLOT + kofs[i]) = kd[i];
+      *(u32x4 *)(base + vpar[i] * SLOT + vofs[i]) = vd[i];
+    }
+    // a pair reaching past the last key: clear the values of keys >= n_keys
+    // in LDS (their probabilities are 0, but the cache there may hold
+    // anything); each thread rewrites only its own chunks
+    if (n_keys - block_of(st, 0) * 32 < 64) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int keep_n = n_keys - block_of(st, vpar[i]) * 32 - vgrp[i] * 8;
+        if (keep_n < 8) {
+          u32x4 v = vd[i];
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t keep =
+                (2 * w < keep_n ? 0xffffu : 0u) | (2 * w + 1 < keep_n ? 0xffff0000u : 0u);
+            v[w] &= keep;
+          }
+          *(u32x4 *)(base + vpar[i] * SLOT + vofs[i]) = v;
+        }
+      }
+    }
+  };
+
+#pragma unroll
+  for (int j = 0; j < RING; ++j) request(j, kr[j], vr[j]);
+  __builtin_amdgcn_sched_barrier(0);
+  // the query loads (issued first) have landed; the ring may still fly
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * RING));
+
+  // one block for one query tile
+  auto compute = [&](QTile &Q, const unsigned char *sl, int key0) {
+    const unsigned char *ks_l = sl;
+    const unsigned char *vs_l = sl + KSLOT;
+    // S^T for the two 16-key tiles
+    floatx4 s[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      s[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) {
+        const u32x4 ka = *(const u32x4 *)(ks_l + (kt * 16 + lr) * 256 + (((ds * 4 + lg) ^ lr) * 16));
+        s[kt] = mfma16x16x32(as_bf16x8(ka), as_bf16x8(Q.qf[ds]), s[kt]);
+      }
+    }
+    // mask and block max: this lane holds keys key0 + 8 lg + 4 kt + e of its
+    // query; scores stay unscaled here (the scale c > 0 keeps the order)
+    float sv[8];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sv[kt * 4 + e] = s[kt][e];
+    if (key0 + 32 > p.L) {
+      // this lane's 8 keys key0 + 8 lg .. + 7 (bit u = key j0 + u): visible
+      // if in the cached prefix, or a tree key (j - L < T) whose bit j - L of
+      // the ancestor mask is set; blocks wholly in the prefix skip this
+      const int j0 = key0 + lg * 8;
+      const int sh = j0 - p.L;  // ancestor-mask bit of key j0
+      const uint32_t pre = (1u << min(8, max(0, -sh))) - 1u;
+      const uint32_t valid = (1u << min(8, max(0, n_keys - j0))) - 1u;
+      uint64_t win;  // mask bits sh .. sh + 7 in its low byte (0 below bit 0)
+      if (sh >= 128)
+        win = 0ull;
+      else if (sh >= 64)
+        win = Q.mk1 >> (sh - 64);
+      else if (sh >= 0)
+        win = (Q.mk0 >> sh) | (sh > 56 ? Q.mk1 << (64 - sh) : 0ull);
+      else
+        win = sh > -8 ? Q.mk0 << -sh : 0ull;
+      const uint32_t vis = pre | ((uint32_t)win & valid & 0xffu);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sv[u] = (vis >> u) & 1u ? sv[u] : -INFINITY;
+    }
+    float bmax = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                       fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    const float c = p.scale_log2;
+    bmax *= c;
+    // Lazy rescaling: the exponentials are taken against a reference m_ref
+    // that moves only when a block's maximum exceeds it by more than 8 (log2
+    // units), so probabilities stay below 2^8 and the accumulators are
+    // rescaled only then (a branch the whole wave takes together).
+    const bool need = bmax > Q.m_run + 8.f;  // m_run: the reference
+    if (__ballot(need)) {
+      // 0 when leaving -inf (nothing accumulated yet), 1 where kept
+      const float alpha = need ? __builtin_amdgcn_exp2f(Q.m_run - bmax) : 1.f;
+      const float m_new = need ? bmax : Q.m_run;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) Q.o[dt] *= alpha;
+      Q.l_run *= alpha;
+      Q.m_run = m_new;
+    }
+    // a query with nothing visible yet keeps reference -inf: use 0 so that
+    // its probabilities are exactly 0
+    const float m_eff = Q.m_run == -INFINITY ? 0.f : Q.m_run;
+    float pv[8];
+    float psum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pv[e] = __builtin_amdgcn_exp2f(fmaf(sv[e], c, -m_eff));
+      psum += pv[e];
+    }
+    Q.l_run += psum;
+    // P = hi + lo, both bf16: the PV product then carries P to ~16
+    // significant bits (two MFMAs per tile; the kernel is bound by loads)
+    float plo[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) plo[e] = pv[e] - bf16_to_f32(f32_to_bf16(pv[e]));
+    const u32x4 pb = u32x4{pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                           pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
+    const u32x4 pl = u32x4{pack_bf16x2(plo[0], plo[1]), pack_bf16x2(plo[2], plo[3]),
+                           pack_bf16x2(plo[4], plo[5]), pack_bf16x2(plo[6], plo[7])};
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      const int r = dt * 16 + lr;
+      const u32x4 va = *(const u32x4 *)(vs_l + r * 64 + ((lg ^ ((lr >> 2) & 3)) * 16));
+      Q.o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pb), Q.o[dt]);
+      Q.o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pl), Q.o[dt]);
+    }
+  };
+
+  // ---- main loop, RING pairs per trip.  Pair st: stage it (requested RING
+  // pairs ago) into LDS slots 2 (st & 1) + parity and request pair st + RING
+  // into the freed registers; barrier; every wave multiplies its query tiles
+  // with the block of its parity.  The slots staged here were last read for
+  // pair st - 2, which every wave finished before pair st - 1's barrier.  The
+  // last trip runs whole: its blocks past the split lie beyond the last key
+  // (values cleared, nothing visible), so the loop body has no branch around
+  // its loads.
+  for (int c0 = 0; c0 < nsteps; c0 += RING) {
 #pragma unroll
     for (int j = 0; j < RING; ++j) {
-      const int i = c0 + j;
-      const bool live = i < nw;
-      // stage block i (its loads were issued RING blocks ago), then reuse
-      // the registers for block i + RING; the wave's own LDS operations run
-      // in order, so block i-1's reads precede these writes
-      if (live) stage(wb0 + i, kr[j], vr[j]);
+      const int st = c0 + j;
+      stage(st, kr[j], vr[j]);
       __builtin_amdgcn_sched_barrier(0);
-      load(wb0 + i + RING, kr[j], vr[j]);
+      request(st + RING, kr[j], vr[j]);
       __builtin_amdgcn_sched_barrier(0);
-      if (!live) continue;
-      const unsigned char *ks_l = wl;
-      const unsigned char *vs_l = wl + KSLOT;
-      const int key0 = (wb0 + i) * 32;
-      // S^T for the two 16-key tiles
-      floatx4 s[2];
+      __syncthreads();
+      const unsigned char *sl = lds + ((st & 1) * 2 + par) * SLOT;
+      const int kb = block_of(st, par);
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        s[kt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ds = 0; ds < 4; ++ds) {
-          const u32x4 ka = *(const u32x4 *)(ks_l + (kt * 16 + lr) * 256 + (((ds * 4 + lg) ^ lr) * 16));
-          s[kt] = mfma16x16x32(as_bf16x8(ka), as_bf16x8(qf[ds]), s[kt]);
-        }
-      }
-      // scale, mask, block max: this lane holds keys key0 + 8 lg + 4 kt + e
-      float sv[8];
-      float bmax = -INFINITY;
-      if (key0 + 32 <= p.L) {
-        // the whole block is cached prefix: visible to every node
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float x = s[kt][e] * p.scale_log2;
-            sv[kt * 4 + e] = x;
-            bmax = fmaxf(bmax, x);
-          }
-      } else {
-        // this lane's 8 keys key0 + 8 lg .. + 7: visibility bits from the
-        // prefix bound and the ancestor mask (bit j - L for tree keys)
-        const int j0 = key0 + lg * 8;
-        uint32_t visb = 0;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j = j0 + u;
-          const int jj = j - p.L;
-          const uint64_t word = jj < 64 ? mk0 : mk1;
-          const uint32_t anc = (uint32_t)((word >> (jj & 63)) & 1ull);
-          visb |= ((uint32_t)(j < p.L) | ((uint32_t)(j < n_keys) & anc)) << u;
-        }
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float x = (visb >> (kt * 4 + e)) & 1u ? s[kt][e] * p.scale_log2 : -INFINITY;
-            sv[kt * 4 + e] = x;
-            bmax = fmaxf(bmax, x);
-          }
-      }
-      bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
-      bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
-      // no divergence around the MFMAs: a query with nothing visible yet uses
-      // a finite reference so that every probability and alpha is exactly 0
-      const float m_new = fmaxf(m_run, bmax);
-      const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_ref);
-      m_run = m_new;
-      float pv[8];
-      float psum = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pv[e] = exp2f(sv[e] - m_ref);
-        psum += pv[e];
-      }
-      l_run = l_run * alpha + psum;
-      // P = hi + lo, both bf16: the PV product then carries P to ~16
-      // significant bits (two MFMAs per tile; the kernel is bound by HBM)
-      float plo[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) plo[e] = pv[e] - bf16_to_f32(f32_to_bf16(pv[e]));
-      const u32x4 pb = u32x4{pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
-                             pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
-      const u32x4 pl = u32x4{pack_bf16x2(plo[0], plo[1]), pack_bf16x2(plo[2], plo[3]),
-                             pack_bf16x2(plo[4], plo[5]), pack_bf16x2(plo[6], plo[7])};
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const int r = dt * 16 + lr;
-        const u32x4 va = *(const u32x4 *)(vs_l + r * 64 + ((lg ^ ((lr >> 2) & 3)) * 16));
-        o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pb), o[dt] * alpha);
-        o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pl), o[dt]);
-      }
+      for (int qi = 0; qi < NQ; ++qi)
+        if (qi < n_live) compute(qt[qi], sl, kb * 32);
     }
   }
-  // per-query l over the 4 lane groups (m is already uniform)
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
 
-  // ---- merge the four waves through LDS (this wave's ring is free now)
-  float *ow = (float *)wl;  // [16][OROW]
+  // ---- merge the two parities (waves w and w + 4) through LDS, one query
+  // tile slot at a time, then the output (KS = 1) or this split's partial
+  // row [16 queries][OROW]
+  float *mrow = (float *)lds + (size_t)qw * 16 * OROW + lr * OROW;
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) *(floatx4 *)(ow + lr * OROW + dt * 16 + lg * 4) = o[dt];
-  if (lg == 0) {
-    ml_s[wave][lr][0] = m_run;
-    ml_s[wave][lr][1] = l_run;
+  for (int qi = 0; qi < NQ; ++qi) {
+    __syncthreads();  // the LDS ring (or the previous round) is free
+    QTile &Q = qt[qi];
+    float l = Q.l_run;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const bool live = qi < n_live;
+    if (par == 1 && live) {
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) *(floatx4 *)(mrow + dt * 16 + lg * 4) = Q.o[dt];
+      if (lg == 0) *(float2 *)(mrow + 128) = float2{Q.m_run, l};
+    }
+    __syncthreads();
+    if (par == 1 || !live) continue;
+    const float2 ml1 = *(const float2 *)(mrow + 128);
+    const float M = fmaxf(Q.m_run, ml1.x);
+    const float s0 = Q.m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(Q.m_run - M);
+    const float s1 = ml1.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml1.x - M);
+    floatx4 o[8];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[dt] = Q.o[dt] * s0 + *(const floatx4 *)(mrow + dt * 16 + lg * 4) * s1;
+    l = l * s0 + ml1.y * s1;
+    const int tile = qw + 4 * qi;
+    if (KS == 1) {
+      const int t = tile * 16 + lr;
+      if (t < p.T) {
+        const float inv = 1.f / l;
+        bf16_t *dst = p.out + (size_t)t * p.nh * 128 + h * 128 + lg * 4;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+          const floatx4 v = o[dt] * inv;
+          *(u32x2 *)(dst + dt * 16) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        }
+      }
+    } else {
+      float *row = p.part + (((size_t)h * KS + ks) * p.MT + tile) * 16 * OROW + lr * OROW;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) *(floatx4 *)(row + dt * 16 + lg * 4) = o[dt];
+      if (lg == 0) *(float2 *)(row + 128) = float2{M, l};
+    }
   }
-  __syncthreads();
-  // thread -> query tq = tid / 16, dims 8 (tid % 16) .. + 7
+}
+
+// ---- merge of the KS splits: workgroup (head h, query tile qt); thread ->
+// query tq = tid / 16, dims 8 (tid % 16) .. + 7.  The splits' rows are read
+// 8 at a time (one round trip per batch) and added in split order, scaled to
+// the running maximum.
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
+  const int h = blockIdx.x, qt = blockIdx.y;
   const int tq = threadIdx.x >> 4, d8 = (threadIdx.x & 15) * 8;
-  float M = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) M = fmaxf(M, ml_s[w][tq][0]);
-  floatx4 acc0 = floatx4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
-  float lsum = 0.f;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const float mw = ml_s[w][tq][0];
-    const float sc = mw == -INFINITY ? 0.f : exp2f(mw - M);
-    lsum += sc * ml_s[w][tq][1];
-    const float *src = (const float *)(lds + w * WAVE_LDS) + tq * OROW + d8;
-    acc0 += sc * *(const floatx4 *)src;
-    acc1 += sc * *(const floatx4 *)(src + 4);
-  }
   const int t = qt * 16 + tq;
-  auto store_out = [&](floatx4 v0, floatx4 v1) {
-    bf16_t *dst = p.out + (size_t)t * p.nh * 128 + h * 128 + d8;
-    *(u32x4 *)dst = u32x4{pack_bf16x2(v0[0], v0[1]), pack_bf16x2(v0[2], v0[3]),
-                          pack_bf16x2(v1[0], v1[1]), pack_bf16x2(v1[2], v1[3])};
+  if (t >= p.T) return;
+  const int KS = p.splits;
+  auto row_of = [&](int s) {
+    return p.part + (((size_t)h * KS + s) * p.MT + qt) * 16 * OROW + tq * OROW;
   };
-  if (KS == 1) {
-    if (t < p.T) {
-      const float inv = 1.f / lsum;
-      store_out(acc0 * inv, acc1 * inv);
+  constexpr int B = 8;
+  float M = -INFINITY, lsum = 0.f;
+  floatx4 acc0 = floatx4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
+  for (int s0 = 0; s0 < KS; s0 += B) {
+    float2 ml[B];
+    floatx4 r0[B], r1[B];
+#pragma unroll
+    for (int v = 0; v < B; ++v) {
+      const float *row = row_of(min(s0 + v, KS - 1));
+      ml[v] = *(const float2 *)(row + 128);
+      r0[v] = *(const floatx4 *)(row + d8);
+      r1[v] = *(const floatx4 *)(row + d8 + 4);
     }
-    return;
-  }
-
-  // ---- publish this split's (O, m, l), rows of OROW floats.  Agent-scope
-  // relaxed atomic stores write through to memory that every XCD sees,
-  // without the L2 write-back and invalidate that a device fence costs; the
-  // ticket is taken only after they have completed, and the last split
-  // reads them back with agent-scope atomic loads (never a stale L2 copy).
-  const int tile = h * p.MT + qt;
-  uint64_t *part = (uint64_t *)(p.part + (size_t)tile * KS * 16 * OROW);
-  {
-    uint64_t *row = part + ((size_t)ks * 16 + tq) * (OROW / 2);
-    const floatx4 v0 = acc0, v1 = acc1;
-    __hip_atomic_store(row + d8 / 2, __builtin_bit_cast(uint64_t, float2{v0[0], v0[1]}),
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(row + d8 / 2 + 1, __builtin_bit_cast(uint64_t, float2{v0[2], v0[3]}),
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(row + d8 / 2 + 2, __builtin_bit_cast(uint64_t, float2{v1[0], v1[1]}),
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(row + d8 / 2 + 3, __builtin_bit_cast(uint64_t, float2{v1[2], v1[3]}),
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (d8 == 0)
-      __hip_atomic_store(row + 64, __builtin_bit_cast(uint64_t, float2{M, lsum}), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const unsigned prev =
-        __hip_atomic_fetch_add(&p.counters[tile], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int last = prev == (unsigned)(KS - 1);
-    if (last) __hip_atomic_store(&p.counters[tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    last_s = last;
-  }
-  __syncthreads();
-  if (!last_s || t >= p.T) return;
-
-  auto ld2 = [](const uint64_t *a) {
-    return __builtin_bit_cast(float2, __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-  };
-  float Mt = -INFINITY;
-  for (int s2 = 0; s2 < KS; ++s2) Mt = fmaxf(Mt, ld2(part + ((size_t)s2 * 16 + tq) * (OROW / 2) + 64).x);
-  acc0 = floatx4{0.f, 0.f, 0.f, 0.f};
-  acc1 = acc0;
-  lsum = 0.f;
-  for (int s2 = 0; s2 < KS; ++s2) {
-    const uint64_t *row = part + ((size_t)s2 * 16 + tq) * (OROW / 2);
-    const float2 ml = ld2(row + 64);
-    const float2 a = ld2(row + d8 / 2), b = ld2(row + d8 / 2 + 1);
-    const float2 c = ld2(row + d8 / 2 + 2), d = ld2(row + d8 / 2 + 3);
-    const float sc = ml.x == -INFINITY ? 0.f : exp2f(ml.x - Mt);
-    lsum += sc * ml.y;
-    acc0 += sc * floatx4{a.x, a.y, b.x, b.y};
-    acc1 += sc * floatx4{c.x, c.y, d.x, d.y};
+    float mb = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < B; ++v)
+      if (s0 + v < KS) mb = fmaxf(mb, ml[v].x);
+    if (mb > M) {
+      const float f = exp2f(M - mb);  // 0 while M = -inf (nothing accumulated)
+      acc0 *= f;
+      acc1 *= f;
+      lsum *= f;
+      M = mb;
+    }
+#pragma unroll
+    for (int v = 0; v < B; ++v) {
+      if (s0 + v < KS) {
+        const float sc = ml[v].x == -INFINITY ? 0.f : exp2f(ml[v].x - M);
+        lsum += sc * ml[v].y;
+        acc0 += sc * r0[v];
+        acc1 += sc * r1[v];
+      }
+    }
   }
   const float inv = 1.f / lsum;
-  store_out(acc0 * inv, acc1 * inv);
+  acc0 *= inv;
+  acc1 *= inv;
+  bf16_t *dst = p.out + (size_t)t * p.nh * 128 + h * 128 + d8;
+  *(u32x4 *)dst = u32x4{pack_bf16x2(acc0[0], acc0[1]), pack_bf16x2(acc0[2], acc0[3]),
+                        pack_bf16x2(acc1[0], acc1[1]), pack_bf16x2(acc1[2], acc1[3])};
 }
 
 }  // namespace
 
-int attn_grid_size(int nh, int splits, int MT) { return ((nh * splits + 7) / 8) * 8 * MT; }
-
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
-  dim3 grid(attn_grid_size(a.nh, a.splits, a.MT)), block(256);
-  if (a.ev_start)
-    hipExtLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, (hipEvent_t)a.ev_start,
-                          (hipEvent_t)a.ev_stop, 0, a);
+  const dim3 grid(a.nh * a.splits), block(512), mblock(256);
+  hipEvent_t ev0 = (hipEvent_t)a.ev_start, ev1 = (hipEvent_t)a.ev_stop;
+  hipEvent_t main_stop = a.splits > 1 ? nullptr : ev1;
+  auto kernel = a.MT > 4 ? attn_bf16_kernel<2, 2> : attn_bf16_kernel<1, 4>;
+  if (ev0)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev0, main_stop, 0, a);
   else
-    hipLaunchKernelGGL(attn_bf16_kernel, grid, block, 0, s, a);
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  const dim3 mgrid(a.nh, a.MT);
+  if (ev1)
+    hipExtLaunchKernelGGL(attn_merge_kernel, mgrid, mblock, 0, s, nullptr, ev1, 0, a);
+  else
+    hipLaunchKernelGGL(attn_merge_kernel, mgrid, mblock, 0, s, a);
   return hipGetLastError();
 }

@@ -57,7 +57,6 @@ ppd_status fail(ppd_status s, const char *fmt, ...) {
 
 constexpr int kCUs = 256;          // MI355X compute units
 constexpr size_t kAlign = 256;
-constexpr int kAttnCounterBase = 4096;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
 int t_pad_of(int T) { return (T + 15) & ~15; }
@@ -77,12 +76,6 @@ ppd_status check_model(const ppd_model *m) {
     if (m->head_dim != 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need head_dim 128");
     if (m->hidden % 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need hidden %% 128 == 0");
     if (m->ffn % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need ffn %% 64 == 0");
-    if (m->n_heads * 8 > PPD_MAX_COUNTERS - kAttnCounterBase)
-      return fail(PPD_EUNSUPPORTED, "too many heads (max %d)", (PPD_MAX_COUNTERS - kAttnCounterBase) / 8);
-    if ((m->vocab + 127) / 128 > kAttnCounterBase)
-      return fail(PPD_EUNSUPPORTED, "vocab too large (max %d)", 128 * kAttnCounterBase);
-    if (m->ffn / 64 > kAttnCounterBase)
-      return fail(PPD_EUNSUPPORTED, "ffn too large (max %d)", 64 * kAttnCounterBase);
   }
   if (!m->tok_emb || !m->lm_head || !m->final_norm || (m->n_prompt > 0 && !m->prompt_emb))
     return fail(PPD_EINVAL, "embedding, LM head and final norm pointers must be set");
@@ -136,27 +129,16 @@ void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
 // bytes of a tile partial of T_pad tokens: 128 rows x T_pad fp32
 size_t tile_partial_floats(int Tp) { return (size_t)128 * Tp; }
 
-constexpr int kAttnMaxSplits = 8;
-
-// Key splits of the attention: the workgroups (heads x query tiles x splits,
-// one per compute unit at a time) should fill whole waves of the 256 CUs;
-// each split costs a partial round trip, and every wave keeps at least two
+// Key splits of the attention: a workgroup per (head, split) reads each
+// key/value block once, so the splits spread the cache over the compute
+// units -- about one workgroup per CU, each keeping at least 4 of the
 // 32-key blocks.
+int attn_max_splits(int nh) { return std::min(PPD_ATTN_MAX_SPLITS, (kCUs + nh - 1) / nh); }
+
 void attn_splits(const ppd_model *m, int L, int T, int *splits, int *chunk) {
   const int nblk = (L + T + 31) / 32;
-  const int wgs = m->n_heads * (t_pad_of(T) / 16);
-  const int ks_max = std::max(1, std::min(kAttnMaxSplits, nblk / 8));
-  int best = 1;
-  double best_cost = 1e30;
-  for (int ks = 1; ks <= ks_max; ++ks) {
-    const int rounds = (wgs * ks + kCUs - 1) / kCUs;
-    const double cost = (double)rounds / ks + 0.02 * ks;
-    if (cost < best_cost - 1e-9) {
-      best_cost = cost;
-      best = ks;
-    }
-  }
-  const int c = (nblk + best - 1) / best;
+  const int ks = std::max(1, std::min(attn_max_splits(m->n_heads), nblk / 4));
+  const int c = ((nblk + ks - 1) / ks + 1) & ~1;  // even: splits start on 64-key pairs
   *splits = (nblk + c - 1) / c;
   *chunk = c;
 }
@@ -172,9 +154,7 @@ WsLayout layout_of(const ppd_model *m, int T) {
     off = align_up(off + bytes);
     return o;
   };
-  w.n_counters = PPD_MAX_COUNTERS;
   w.status = take(16);
-  w.counters = take(sizeof(uint32_t) * PPD_MAX_COUNTERS);
   w.x = take(sizeof(float) * Tp * H);
   w.xg = take(es * Tp * H + sizeof(float) * Tp);
   w.max_ss = std::max(1, H / PPD_GEMM_BN);
@@ -188,8 +168,8 @@ WsLayout layout_of(const ppd_model *m, int T) {
   } else {
     w.tmp = take(0);
   }
-  w.max_splits = m->dtype == PPD_BF16 ? kAttnMaxSplits : 0;
-  w.attn_part = take(sizeof(float) * (size_t)nh * w.max_splits * Tp * 132);
+  w.max_splits = m->dtype == PPD_BF16 ? attn_max_splits(nh) : 0;
+  w.attn_part = take(sizeof(float) * (size_t)nh * w.max_splits * Tp * PPD_ATTN_OROW);
   size_t part = 0;
   if (m->dtype == PPD_BF16) {
     GemmShape gs[5];
@@ -227,7 +207,6 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
   const int Tp = t_pad_of(T), MT = Tp / 16;
   const int cap = kv->capacity;
   uint32_t *status = at<uint32_t>(ws, w.status);
-  uint32_t *counters = at<uint32_t>(ws, w.counters);
   float *x = at<float>(ws, w.x);
   bf16_t *xg = at<bf16_t>(ws, w.xg);
   float *ss = at<float>(ws, w.ss);
@@ -293,7 +272,6 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     a.mask = mask;
     a.out = attn_o;
     a.part = at<float>(ws, w.attn_part);
-    a.counters = counters + kAttnCounterBase;
     a.zeros = g.zeros;
     a.T = T;
     a.MT = MT;
@@ -446,7 +424,7 @@ size_t ppd_workspace_bytes(const ppd_model *model, int32_t t_max, int32_t max_le
 }
 
 ppd_status ppd_workspace_init(void *ws, size_t ws_bytes, void *stream) {
-  const size_t need = align_up(16) + sizeof(uint32_t) * PPD_MAX_COUNTERS;
+  const size_t need = align_up(16);  // status word and the line of zeros
   if (!ws || ws_bytes < need) return fail(PPD_EWORKSPACE, "workspace needs at least %zu bytes", need);
   PPD_TRY_HIP(launch_ws_init(ws, need / 4, (hipStream_t)stream));
   return PPD_OK;

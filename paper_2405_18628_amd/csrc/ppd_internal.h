@@ -61,7 +61,6 @@ __device__ __forceinline__ float wave_max(float v) {
 
 struct WsLayout {
   size_t status;      // uint32 [4]
-  size_t counters;    // uint32 [n_counters]
   size_t x;           // float  [T_pad][H]        residual stream
   size_t xg;          // act    [T_pad][H]        x * gain (next norm's operand)
   size_t ss;          // float  [max_ss][T_pad]   sum-of-squares partials
@@ -74,11 +73,10 @@ struct WsLayout {
   size_t amax;        // float2 [max_amax_tiles][T_pad]
   size_t rope;        // float2 [T_pad][d/2]      (cos, sin)
   size_t total;
-  int n_counters, max_ss, max_splits, max_amax_tiles;
+  int max_ss, max_splits, max_amax_tiles;
   size_t max_part_floats;
 };
 
-#define PPD_MAX_COUNTERS 8192
 #define PPD_ATTN_MAX_SPLITS 64
 
 // ---------------------------------------------------------------------------
@@ -145,20 +143,20 @@ int gemm_kc_pad_of(int K);
 hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s);
 hipError_t launch_gemm_bf16(const GemmLaunch &g, hipStream_t s);
 
+#define PPD_ATTN_OROW 132  // floats per partial row: 128 dims, m, l, padding
+
 struct AttnLaunch {
   const bf16_t *q;      // [T_pad][nh][d]
   const bf16_t *kc;     // [nkv][cap][d]
   const bf16_t *vc;     // [nkv][d][cap]
   const uint64_t *mask;
   bf16_t *out;          // [T_pad][nh d]
-  float *part;          // [nh][MT][splits][16][d + 4]
-  uint32_t *counters;   // nh * MT tickets, zero between launches
+  float *part;          // [nh][splits][MT][16][PPD_ATTN_OROW] (splits > 1)
   const bf16_t *zeros;  // >= 16 zero bytes
   int T, MT, L, cap, nh, nkv, splits, chunk;  // chunk: 32-key blocks per split
   float scale_log2;     // log2(e) / sqrt(d)
-  void *ev_start, *ev_stop;  // optional events at the dispatch's start / end
+  void *ev_start, *ev_stop;  // optional events at the first dispatch's start / last one's end
 };
-int attn_grid_size(int nh, int splits, int MT);
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s);
 
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
