@@ -341,13 +341,13 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
   }
 }
 
-// ---- merge of the KS splits: workgroup (head h, query tile qt); thread ->
-// query tq = tid / 16, dims 8 (tid % 16) .. + 7.  The splits' rows are read
-// 8 at a time (one round trip per batch) and added in split order, scaled to
-// the running maximum.
+// ---- merge of the KS splits: workgroup (head h, query tile qt, 32-dim
+// quarter dq); thread -> query tq = tid / 16, dims 32 dq + 2 (tid % 16) and
+// + 1.  The splits' rows are read 8 at a time (one round trip per batch) and
+// added in split order, scaled to the running maximum.
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
-  const int h = blockIdx.x, qt = blockIdx.y;
-  const int tq = threadIdx.x >> 4, d8 = (threadIdx.x & 15) * 8;
+  const int h = blockIdx.x, qt = blockIdx.y, dq = blockIdx.z;
+  const int tq = threadIdx.x >> 4, d2 = dq * 32 + (threadIdx.x & 15) * 2;
   const int t = qt * 16 + tq;
   if (t >= p.T) return;
   const int KS = p.splits;
@@ -356,16 +356,14 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
   };
   constexpr int B = 8;
   float M = -INFINITY, lsum = 0.f;
-  floatx4 acc0 = floatx4{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
+  float2 acc = float2{0.f, 0.f};
   for (int s0 = 0; s0 < KS; s0 += B) {
-    float2 ml[B];
-    floatx4 r0[B], r1[B];
+    float2 ml[B], r[B];
 #pragma unroll
     for (int v = 0; v < B; ++v) {
       const float *row = row_of(min(s0 + v, KS - 1));
       ml[v] = *(const float2 *)(row + 128);
-      r0[v] = *(const floatx4 *)(row + d8);
-      r1[v] = *(const floatx4 *)(row + d8 + 4);
+      r[v] = *(const float2 *)(row + d2);
     }
     float mb = -INFINITY;
 #pragma unroll
@@ -373,8 +371,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
       if (s0 + v < KS) mb = fmaxf(mb, ml[v].x);
     if (mb > M) {
       const float f = exp2f(M - mb);  // 0 while M = -inf (nothing accumulated)
-      acc0 *= f;
-      acc1 *= f;
+      acc.x *= f;
+      acc.y *= f;
       lsum *= f;
       M = mb;
     }
@@ -383,17 +381,13 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
       if (s0 + v < KS) {
         const float sc = ml[v].x == -INFINITY ? 0.f : exp2f(ml[v].x - M);
         lsum += sc * ml[v].y;
-        acc0 += sc * r0[v];
-        acc1 += sc * r1[v];
+        acc.x += sc * r[v].x;
+        acc.y += sc * r[v].y;
       }
     }
   }
   const float inv = 1.f / lsum;
-  acc0 *= inv;
-  acc1 *= inv;
-  bf16_t *dst = p.out + (size_t)t * p.nh * 128 + h * 128 + d8;
-  *(u32x4 *)dst = u32x4{pack_bf16x2(acc0[0], acc0[1]), pack_bf16x2(acc0[2], acc0[3]),
-                        pack_bf16x2(acc1[0], acc1[1]), pack_bf16x2(acc1[2], acc1[3])};
+  *(uint32_t *)(p.out + (size_t)t * p.nh * 128 + h * 128 + d2) = pack_bf16x2(acc.x * inv, acc.y * inv);
 }
 
 }  // namespace
@@ -409,7 +403,7 @@ hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
     hipLaunchKernelGGL(kernel, grid, block, 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  const dim3 mgrid(a.nh, a.MT);
+  const dim3 mgrid(a.nh, a.MT, 4);
   if (ev1)
     hipExtLaunchKernelGGL(attn_merge_kernel, mgrid, mblock, 0, s, nullptr, ev1, 0, a);
   else
