@@ -52,6 +52,23 @@ __device__ __forceinline__ int row_of_key(int j) {
 // (expcnt and lgkmcnt left at their maxima, i.e. not waited on)
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
+// Reductions over the four 16-lane groups of a wave (lanes l, l ^ 16,
+// l ^ 32, l ^ 48) with the gfx950 lane-swap instructions: swapping a value
+// with itself across 16-lane (32-lane) halves gives each lane its partner's
+// value in one of the two results and its own in the other.
+__device__ __forceinline__ float quad_max(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float quad_sum(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // one wave's state for one 16-query tile
 struct QTile {
   u32x4 qf[4];   // queries (B operand), dims 32 ds + 8 (lane / 16) .. + 7
@@ -138,7 +155,9 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
     const int d = c >> 3, g = c & 7;
     vpar[i] = g >> 2;
     vgrp[i] = g & 3;
-    vofs[i] = KSLOT + d * 64 + (((g & 3) ^ ((d >> 2) & 3)) * 16);
+    // the odd block's V^T rows are stored as row d ^ 2, so that the two
+    // blocks' stores from one 16-lane group fall into different banks
+    vofs[i] = KSLOT + (d ^ (vpar[i] << 1)) * 64 + (((g & 3) ^ ((d >> 2) & 3)) * 16);
   }
   // block index of pair st, parity q (past the split: beyond the last key)
   auto block_of = [&](int st, int q) { return 2 * st + q < nb ? b0 + 2 * st + q : nblk + 1; };
@@ -219,25 +238,27 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) sv[u] = (vis >> u) & 1u ? sv[u] : -INFINITY;
     }
-    float bmax = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
-                       fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    // this lane's maximum over its 8 keys (scaled; the scale c > 0 keeps
+    // the order)
     const float c = p.scale_log2;
-    bmax *= c;
-    // Lazy rescaling: the exponentials are taken against a reference m_ref
+    const float lmax = c * fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                                 fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+    // Lazy rescaling: the exponentials are taken against a reference (m_run)
     // that moves only when a block's maximum exceeds it by more than 8 (log2
     // units), so probabilities stay below 2^8 and the accumulators are
-    // rescaled only then (a branch the whole wave takes together).
-    const bool need = bmax > Q.m_run + 8.f;  // m_run: the reference
-    if (__ballot(need)) {
+    // rescaled only then.  The common case needs no exchange between lanes:
+    // only when some lane's own maximum exceeds the reference does the wave
+    // (all together) reduce the block maximum over each query's four lane
+    // groups and move the reference of the queries that need it.
+    if (__ballot(lmax > Q.m_run + 8.f)) {
+      const float bmax = quad_max(lmax);
+      const bool need = bmax > Q.m_run + 8.f;  // the same in a query's four lanes
       // 0 when leaving -inf (nothing accumulated yet), 1 where kept
       const float alpha = need ? __builtin_amdgcn_exp2f(Q.m_run - bmax) : 1.f;
-      const float m_new = need ? bmax : Q.m_run;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) Q.o[dt] *= alpha;
       Q.l_run *= alpha;
-      Q.m_run = m_new;
+      Q.m_run = need ? bmax : Q.m_run;
     }
     // a query with nothing visible yet keeps reference -inf: use 0 so that
     // its probabilities are exactly 0
@@ -262,7 +283,7 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
       const int r = dt * 16 + lr;
-      const u32x4 va = *(const u32x4 *)(vs_l + r * 64 + ((lg ^ ((lr >> 2) & 3)) * 16));
+      const u32x4 va = *(const u32x4 *)(vs_l + (r ^ (par << 1)) * 64 + ((lg ^ ((lr >> 2) & 3)) * 16));
       Q.o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pb), Q.o[dt]);
       Q.o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pl), Q.o[dt]);
     }
@@ -301,9 +322,7 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
   for (int qi = 0; qi < NQ; ++qi) {
     __syncthreads();  // the LDS ring (or the previous round) is free
     QTile &Q = qt[qi];
-    float l = Q.l_run;
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    float l = quad_sum(Q.l_run);
     const bool live = qi < n_live;
     if (par == 1 && live) {
 #pragma unroll
