@@ -316,7 +316,7 @@ def kv_compact(k_cache: List[np.ndarray], v_cache: List[np.ndarray], tree_k, tre
     """Commit the accepted nodes' keys/values: cache[L + k] = tree[path[k]].
 
     Prompt-token keys/values are never committed: one shared cache (Section
-    5.4).  Returns the new cache length L + len(path)."""
+    5.3).  Returns the new cache length L + len(path)."""
     for l in range(len(k_cache)):
         for kk, node in enumerate(path):
             k_cache[l][:, L + kk, :] = tree_k[l][:, node, :]
@@ -421,3 +421,108 @@ def path_tokens(parent: Sequence[int], ids: Sequence[int], node: int) -> List[in
         seq.append(int(ids[j]))
         j = int(parent[j])
     return seq[::-1]
+
+
+# ----------------------------------------------------------------------------
+# candidate generation for the next step (Section 3, step (1); Section 3.1;
+# Section 4 and the tree-construction appendix)
+#
+# The next step's tree is a fixed sparse-tree template whose token ids are
+# filled from this step's outputs: its root is the bonus token (the accepted
+# node's greedy token) and a candidate at depth d with rank r takes the r-th
+# best token of the logits of the d-th prompt token attached to the accepted
+# node -- that prompt token stands d positions past the accepted node, i.e.
+# at the position of the bonus token's (d-1)-th successor, so its output
+# predicts the token at depth d of the next tree (Section 3.1).  Prompt nodes
+# of the template carry fixed prompt ids.
+
+TOPK_MAX = 16  # largest rank + 1 a template may use per depth
+
+
+def prompt_chain(parent: Sequence[int], ids: Sequence[int], vocab: int, node: int) -> List[int]:
+    """The prompt tokens attached to `node`: p_1 is its child with prompt id 0
+    (token vocab + 0), p_j the child of p_{j-1} with prompt id j - 1 (the chain
+    position j uses prompt embedding j - 1).  Returns [p_1, p_2, ...] (empty if
+    the node carries none); the first such child is taken if several match."""
+    T = len(parent)
+    chain = []
+    cur = int(node)
+    while True:
+        want = vocab + len(chain)
+        nxt = -1
+        for i in range(T):
+            if int(parent[i]) == cur and int(ids[i]) == want:
+                nxt = i
+                break
+        if nxt < 0:
+            return chain
+        chain.append(nxt)
+        cur = nxt
+
+
+def rank_order(row: np.ndarray) -> np.ndarray:
+    """Vocabulary indices of one logits row from best to worst: larger value
+    first, equal values by smaller index; NaN ranks below every number."""
+    v = np.asarray(row, np.float64)
+    key = np.where(np.isnan(v), -np.inf, v)
+    nan_last = np.isnan(v).astype(np.int64)
+    # lexsort sorts by the last key first
+    return np.lexsort((np.arange(v.shape[0]), -key, nan_last)).astype(np.int64)
+
+
+def template_depths(tpl_parent: Sequence[int]) -> np.ndarray:
+    depth, _ = build_mask(tpl_parent)
+    return depth
+
+
+def validate_template(tpl_parent: Sequence[int], tpl_kind: Sequence[int], n_prompt: int) -> None:
+    """A template is a topological tree (tpl_parent) with a kind per node:
+    kind >= 0 is a candidate of that rank (< TOPK_MAX) whose parent is the root
+    or a candidate; kind < 0 is prompt token -kind - 1 (< n_prompt), attached
+    to a candidate (prompt id 0) or to the prompt token one id lower.  Node 0
+    is the root (its kind is ignored)."""
+    validate_tree(tpl_parent)
+    T = len(tpl_parent)
+    for i in range(1, T):
+        k, p = int(tpl_kind[i]), int(tpl_parent[i])
+        pk = int(tpl_kind[p]) if p > 0 else 0
+        if k >= 0:
+            if k >= TOPK_MAX or (p > 0 and pk < 0):
+                raise ValueError(f"template node {i}: bad candidate")
+        else:
+            j = -k - 1
+            if j >= n_prompt:
+                raise ValueError(f"template node {i}: prompt id {j} >= {n_prompt}")
+            if (j == 0 and p > 0 and pk < 0) or (j > 0 and (p == 0 or pk != -j)):
+                raise ValueError(f"template node {i}: prompt chain out of order")
+
+
+def next_tree_ids(parent: Sequence[int], ids: Sequence[int], vocab: int, path: Sequence[int],
+                  next_tok: int, logits: np.ndarray, tpl_parent: Sequence[int],
+                  tpl_kind: Sequence[int]) -> np.ndarray:
+    """Token ids of the next step's tree (template tpl_parent / tpl_kind).
+
+    Root: next_tok, the bonus token.  Candidate at template depth d with rank
+    r: rank_order(logits[src])[r], where src is the accepted node's d-th prompt
+    token; for d beyond its prompt chain, the chain's deepest node (or the
+    accepted node itself when it carries none) -- a reading of this build:
+    the template stays fixed, and exact-match verification keeps the output
+    lossless whatever the guesses.  Prompt nodes: vocab + prompt id."""
+    a = int(path[-1])
+    chain = prompt_chain(parent, ids, vocab, a)
+    depth = template_depths(tpl_parent)
+    T = len(tpl_parent)
+    out = np.zeros(T, np.int64)
+    out[0] = int(next_tok)
+    order_of = {}
+    for i in range(1, T):
+        k = int(tpl_kind[i])
+        if k < 0:
+            out[i] = vocab + (-k - 1)
+            continue
+        d = int(depth[i])
+        src = chain[d - 1] if d <= len(chain) else (chain[-1] if chain else a)
+        if src not in order_of:
+            order_of[src] = rank_order(logits[src])
+        out[i] = int(order_of[src][k])
+    return out

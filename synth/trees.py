@@ -132,3 +132,52 @@ def tree_from_parents(parent, ids, vocab: int) -> Tree:
     parent = np.asarray(parent, np.int32)
     ids = np.asarray(ids, np.int32)
     return Tree(parent, ids, int(np.sum(ids < vocab)))
+
+
+# ---------------------------------------------------------------------------
+# sparse-tree templates for the next step's tree (candidate generation)
+
+# candidate rank paths of a 15-candidate template (depth <= 3): rank r at
+# depth d means "the r-th best guess for the token at depth d"
+RANK_PATHS_15 = [(0,), (1,), (2,), (3,), (4,), (5,),
+                 (0, 0), (0, 1), (0, 2), (1, 0), (1, 1), (2, 0),
+                 (0, 0, 0), (0, 0, 1), (0, 1, 0)]
+
+
+@dataclass
+class Template:
+    parent: np.ndarray  # int32 [T]
+    kind: np.ndarray    # int32 [T]: rank (>= 0) of a candidate, or -1 - prompt id
+
+    @property
+    def T(self) -> int:
+        return int(self.parent.shape[0])
+
+
+def make_template(rank_paths=RANK_PATHS_15, n_prompt: int = 3) -> Template:
+    """Root, then the candidates of `rank_paths` (each path's prefix must come
+    earlier), then a chain of n_prompt prompt tokens under the root and under
+    every candidate, in node order.  Every node carries a chain, so whichever
+    node is accepted, the next tree's guesses come from its own prompt tokens.
+    Default: 1 + 15 candidates, 16 chains of 3 -> T = 64."""
+    parent, kind = [-1], [0]
+    node_of = {(): 0}
+    for path in rank_paths:
+        path = tuple(path)
+        parent.append(node_of[path[:-1]])
+        kind.append(path[-1])
+        node_of[path] = len(parent) - 1
+    n_cand = len(parent)
+    for c in range(n_cand):
+        prev = c
+        for j in range(n_prompt):
+            parent.append(prev)
+            kind.append(-1 - j)
+            prev = len(parent) - 1
+    return Template(np.asarray(parent, np.int32), np.asarray(kind, np.int32))
+
+
+def template_tree(tpl: Template, ids) -> Tree:
+    """The tree of a template with the given token ids."""
+    n_cand = int(np.sum(tpl.kind[1:] >= 0)) + 1
+    return Tree(tpl.parent.copy(), np.asarray(ids, np.int32), n_cand)

@@ -400,3 +400,109 @@ def test_kv_compact_commits_path_rows(tiny):
     for l in range(sh.n_layers):
         assert np.abs(kc[l][:, :L2] - kr[l][:, :L2]).max() < 1e-12
         assert np.abs(vc[l][:, :L2] - vr[l][:, :L2]).max() < 1e-12
+
+
+# ------------------------------------------------ next-step candidate generation
+
+def _brute_rank(row, t):
+    """Definition of a rank: the number of entries that beat entry t (a larger
+    number, or an equal one at a smaller index; NaN beats nothing and loses to
+    every number, NaNs among themselves by index)."""
+    v = [float(x) for x in row]
+    def beats(j, i):
+        if math.isnan(v[i]):
+            return (not math.isnan(v[j])) or j < i
+        if math.isnan(v[j]):
+            return False
+        return v[j] > v[i] or (v[j] == v[i] and j < i)
+    return sum(1 for j in range(len(v)) if j != t and beats(j, t))
+
+
+def test_rank_order_matches_definition():
+    rng = np.random.default_rng(11)
+    for trial in range(40):
+        n = int(rng.integers(1, 60))
+        row = rng.integers(-3, 4, n).astype(np.float64)   # many ties
+        if trial % 3 == 0:
+            row[rng.integers(0, n, max(1, n // 5))] = np.nan
+        order = O.rank_order(row)
+        assert sorted(order.tolist()) == list(range(n))
+        for r, t in enumerate(order):
+            assert _brute_rank(row, int(t)) == r
+        if not np.isnan(row).any():
+            assert order[0] == O.argmax_first(row[None, :])[0]
+
+
+def test_prompt_chain_handmade():
+    V = 10
+    # node 0 root; 1 candidate; 2,4,6 = root's chain (prompt ids 0, 1, 2);
+    # 3,5,7 = candidate 1's chain; 8 = a stray prompt id 1 directly under 1
+    parent = [-1, 0, 0, 1, 2, 3, 4, 5, 1]
+    ids = [5, 7, V + 0, V + 0, V + 1, V + 1, V + 2, V + 2, V + 1]
+    assert O.prompt_chain(parent, ids, V, 0) == [2, 4, 6]
+    assert O.prompt_chain(parent, ids, V, 1) == [3, 5, 7]
+    assert O.prompt_chain(parent, ids, V, 6) == []
+    # a chain cut short: only prompt id 0 present
+    assert O.prompt_chain([-1, 0, 1], [3, V, V + 5], V, 0) == [1]
+
+
+def test_next_tree_ids_handmade():
+    """Hand-computed: accepted node 1 with chain (3, 5); template root, ranks
+    (0), (1), (0, 0), (0, 1) and one chain of 2 under the root."""
+    V = 6
+    parent = [-1, 0, 0, 1, 2, 3, 4]
+    ids = [2, 4, V + 0, V + 0, V + 1, V + 1, 1]
+    logits = np.zeros((7, V))
+    logits[3] = [0.1, 0.9, 0.3, 0.9, -1.0, 0.2]   # depth-1 source: order 1, 3, 2, 5, 0, 4
+    logits[5] = [2.0, 1.0, 3.0, 0.0, 3.0, -5.0]   # depth-2 source: order 2, 4, 0, 1, 3, 5
+    tpl_parent = [-1, 0, 0, 1, 1, 0, 5]
+    tpl_kind = [0, 0, 1, 0, 1, -1, -2]
+    O.validate_template(tpl_parent, tpl_kind, 2)
+    out = O.next_tree_ids(parent, ids, V, [0, 1], 4, logits, tpl_parent, tpl_kind)
+    assert out.tolist() == [4, 1, 3, 2, 4, V + 0, V + 1]
+    # accepted node without prompt tokens: every depth falls back to its own row
+    logits[2] = [0, 0, 0, 0, 0, 9.0]
+    out = O.next_tree_ids([-1, 0, 0], [2, 3, 5], V, [0, 2], 5, np.vstack([logits[:2], logits[2:3]]),
+                          tpl_parent, tpl_kind)
+    assert out.tolist() == [5, 5, 0, 5, 0, V + 0, V + 1]
+
+
+@pytest.mark.parametrize("tpl_parent,tpl_kind", [
+    ([-1, 0, 1], [0, -1, 0]),          # candidate under a prompt token
+    ([-1, 0, 0], [0, 0, -2]),          # prompt id 1 directly under the root
+    ([-1, 0, 1], [0, 0, -3]),          # prompt id 2 after a candidate
+    ([-1, 0], [0, 16]),                # rank beyond the top-k limit
+    ([-1, 0], [0, -4]),                # prompt id >= n_prompt
+])
+def test_validate_template_rejects(tpl_parent, tpl_kind):
+    with pytest.raises(ValueError):
+        O.validate_template(tpl_parent, tpl_kind, 3)
+
+
+def test_closed_loop_with_generated_candidates_is_lossless(tiny):
+    """Section 3's full guess-and-verify loop: each step's tree is the template
+    filled from the previous step's outputs (bonus root, top-k of the accepted
+    node's prompt tokens); the emitted tokens are the vanilla greedy sequence
+    (Section 5.1: output identical to the original model)."""
+    from synth.trees import make_template
+    sh, W, m, kc0, vc0, L0, root = tiny
+    tpl = make_template([(0,), (1,), (2,), (0, 0), (0, 1), (1, 0), (0, 0, 0)], 3)
+    O.validate_template(tpl.parent, tpl.kind, sh.n_prompt)
+    kc, vc = O.copy_cache(kc0, vc0)
+    rng = np.random.default_rng(5)
+    ids = rng.integers(0, sh.vocab, tpl.T)
+    ids[0] = root
+    ids[tpl.kind < 0] = sh.vocab + (-tpl.kind[tpl.kind < 0] - 1)
+    L, emitted, accepted = L0, [], 0
+    for s in range(6):
+        res = O.verify_forward(m, kc, vc, L, ids, tpl.parent, "f32")
+        pred = O.argmax_first(res["logits"])
+        path, n_path, nxt = O.accept(tpl.parent, ids, pred, sh.vocab)
+        L = O.kv_compact(kc, vc, res["tree_k"], res["tree_v"], L, path)
+        emitted += [int(ids[j]) for j in path[1:]] + [nxt]
+        accepted += n_path - 1
+        ids = O.next_tree_ids(tpl.parent, ids, sh.vocab, path, nxt, res["logits"], tpl.parent,
+                              tpl.kind)
+        assert ids[0] == nxt
+    ref = O.greedy_decode(m, kc0, vc0, L0, root, len(emitted), "f32")
+    assert emitted == ref
