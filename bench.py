@@ -91,7 +91,7 @@ def main():
     import paper_2405_18628_amd as ppd
     from synth import workload
     from synth.model import empty_kv, fill_kv_normal, make_weights
-    from synth.trees import make_tree
+    from synth.trees import make_template, make_tree
 
     wl = workload(args.workload)
     sh = wl.shape
@@ -179,6 +179,24 @@ def main():
         del keep
         kernels[kind] = tot / cnt * 1e3  # us per launch
 
+    # next-step candidate generation (ppd_next_tree) on this step's outputs,
+    # with the 15-candidate template (1 + 15 candidates, 3 prompt tokens each)
+    tpl = make_template()
+    nids = torch.empty(tpl.T, dtype=torch.int32, device=dev)
+
+    def next_tree():
+        ppd.ppd_next_tree(T, par_d, ids_d, sh.vocab, sh.n_prompt, logits, path, n_path, nxt,
+                          tpl.parent, tpl.kind, nids, ws)
+    for _ in range(3):
+        next_tree()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        next_tree()
+    e1.record()
+    torch.cuda.synchronize()
+    next_us = e0.elapsed_time(e1) / args.steps * 1e3
+
     alg = step_bytes(sh, L, T, n_acc)
     flops = step_flops(sh, L, T)
     gu_us = kernels["gate_up"]
@@ -208,6 +226,7 @@ def main():
         "tree_tokens_per_s": round(T / (ms * 1e-3), 1),
         "emitted_tokens_per_s": round(n_acc / (ms * 1e-3), 1),
         "kernel_us": {k2: round(v2, 2) for k2, v2 in kernels.items()},
+        "next_tree_us": round(next_us, 2),
         "device_status": status,
         "roofline": {"bound": "hbm", "kernel": "gate_up GEMM + SwiGLU",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

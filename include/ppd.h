@@ -15,6 +15,8 @@
  *                        accepted root path, bonus token (Section 3)
  *   ppd_kv_compact       device: commit the accepted nodes' keys/values to
  *                        the single shared KV cache (Section 5.3)
+ *   ppd_next_tree        device: the next step's candidate tree from this
+ *                        step's outputs (Section 3, step (1))
  *
  * Conventions shared by every call
  * --------------------------------
@@ -215,6 +217,44 @@ ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids,
  */
 ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
                           const int32_t *path, const int32_t *n_path, void *stream);
+
+/*
+ * Candidate generation for the next step (Section 3, step (1); Section 3.1;
+ * Section 4 with the tree-construction appendix), so that the decode loop
+ * verify -> accept -> compact -> next tree runs without a host round trip.
+ * The next tree has the fixed shape of a template (tpl_parent, a topological
+ * parent array with tpl_parent[0] = -1) whose token ids are written to
+ * next_ids:
+ *   node 0 (root)           *next_tok, the bonus token from ppd_accept;
+ *   tpl_kind[i] = r >= 0     a candidate of rank r: the r-th best token of the
+ *                            logits of the accepted node's d-th prompt token,
+ *                            d = the node's depth in the template (the
+ *                            accepted node's prompt chain: its child with id
+ *                            vocab + 0, that node's child with id vocab + 1,
+ *                            ...; past the chain's end its deepest node, or
+ *                            the accepted node itself when it has none);
+ *   tpl_kind[i] = -1 - j     prompt token j (id vocab + j).
+ * Ranks order larger logits first, equal logits by smaller index, NaN last
+ * (a NaN among the selected ranks sets PPD_DEV_NAN_LOGIT).  The template's
+ * parent/depth/mask are the caller's (ppd_build_tree_mask on tpl_parent).
+ *   T, parent, ids    this step's tree (device int32[T])
+ *   logits            device float32[T][vocab] written by ppd_verify_step
+ *   path, n_path, next_tok   device, as written by ppd_accept
+ *   tpl_T, tpl_parent, tpl_kind   HOST arrays of tpl_T entries (copied into
+ *                     the launch; the call keeps no pointer to them)
+ *   next_ids          device int32[tpl_T] (output)
+ *   ws                the workspace (status word)
+ * Template rules (else PPD_EINVAL, nothing enqueued): 1 <= tpl_T <= PPD_T_MAX;
+ * a candidate's parent is the root or a candidate, rank < PPD_TOPK_MAX and <
+ * vocab, depth <= 15; prompt token 0 hangs under the root or a candidate,
+ * prompt token j > 0 under prompt token j - 1, j < n_prompt.
+ */
+#define PPD_TOPK_MAX 16
+ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, int32_t vocab,
+                         int32_t n_prompt, const float *logits, const int32_t *path,
+                         const int32_t *n_path, const int32_t *next_tok, int32_t tpl_T,
+                         const int32_t *tpl_parent, const int32_t *tpl_kind, int32_t *next_ids,
+                         void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Profiling aid, not needed for correctness.  While set, every

@@ -75,10 +75,12 @@ def lib() -> C.CDLL:
         L.ppd_device_status.argtypes = [vp, sz, P(C.c_uint32), i32, vp]
         L.ppd_set_kernel_timer.argtypes = [i32, vp, vp, i32]
         L.ppd_last_error.restype = C.c_char_p
+        L.ppd_next_tree.argtypes = [i32, vp, vp, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, vp, sz,
+                                    vp]
         L.ppd_packed_weight_bytes.argtypes = [i32, i32, i32]
         L.ppd_packed_weight_bytes.restype = sz
         L.ppd_pack_weight.argtypes = [i32, i32, i32, vp, vp, vp]
-        for f in ("ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
+        for f in ("ppd_next_tree", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
                   "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -247,6 +249,26 @@ def ppd_accept(T: int, parent, ids, pred, vocab: int, path, n_path, next_tok, ws
                             _stream(stream)))
 
 
+def ppd_next_tree(T: int, parent, ids, vocab: int, n_prompt: int, logits, path, n_path,
+                  next_tok, tpl_parent: Sequence[int], tpl_kind: Sequence[int], next_ids, ws,
+                  stream=None):
+    """Token ids of the next step's tree (template tpl_parent / tpl_kind, host
+    sequences) into the device tensor next_ids."""
+    import torch
+    for t, n in ((parent, "parent"), (ids, "ids"), (path, "path"), (n_path, "n_path"),
+                 (next_tok, "next_tok"), (next_ids, "next_ids")):
+        _dev(t, torch.int32, n)
+    _dev(logits, torch.float32, "logits")
+    tp = np.ascontiguousarray(np.asarray(tpl_parent, dtype=np.int32))
+    tk = np.ascontiguousarray(np.asarray(tpl_kind, dtype=np.int32))
+    if tp.shape != tk.shape:
+        raise ValueError("tpl_parent and tpl_kind differ in length")
+    _check(lib().ppd_next_tree(int(T), _ptr(parent), _ptr(ids), int(vocab), int(n_prompt),
+                               _ptr(logits), _ptr(path), _ptr(n_path), _ptr(next_tok),
+                               int(tp.shape[0]), tp.ctypes.data, tk.ctypes.data, _ptr(next_ids),
+                               _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
 def ppd_kv_compact(model: Model, kv: KVCache, L: int, path, n_path, stream=None):
     _check(lib().ppd_kv_compact(C.byref(model.desc), C.byref(kv.desc), int(L), _ptr(path),
                                 _ptr(n_path), _stream(stream)))
@@ -280,6 +302,6 @@ def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):
     return st, sp
 
 
-__all__ = ["ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
+__all__ = ["ppd_next_tree", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
            "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept", "ppd_kv_compact",
            "ppd_device_status", "ppd_last_error"]

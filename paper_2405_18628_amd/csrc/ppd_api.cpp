@@ -503,6 +503,67 @@ ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
   return PPD_OK;
 }
 
+ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, int32_t vocab,
+                         int32_t n_prompt, const float *logits, const int32_t *path,
+                         const int32_t *n_path, const int32_t *next_tok, int32_t tpl_T,
+                         const int32_t *tpl_parent, const int32_t *tpl_kind, int32_t *next_ids,
+                         void *ws, size_t ws_bytes, void *stream) {
+  if (T < 1 || T > PPD_T_MAX) return fail(PPD_EINVAL, "T=%d outside [1, %d]", T, PPD_T_MAX);
+  if (tpl_T < 1 || tpl_T > PPD_T_MAX)
+    return fail(PPD_EINVAL, "template size %d outside [1, %d]", tpl_T, PPD_T_MAX);
+  if (vocab < 1 || n_prompt < 0) return fail(PPD_EINVAL, "vocab must be positive, n_prompt >= 0");
+  if (!parent || !ids || !logits || !path || !n_path || !next_tok || !tpl_parent || !tpl_kind ||
+      !next_ids)
+    return fail(PPD_EINVAL, "NULL argument");
+  if (!ws || ws_bytes < 16) return fail(PPD_EWORKSPACE, "workspace (status word) required");
+  NextTreeLaunch p{};
+  p.parent = parent;
+  p.ids = ids;
+  p.T = T;
+  p.vocab = vocab;
+  p.logits = logits;
+  p.path = path;
+  p.n_path = n_path;
+  p.next_tok = next_tok;
+  p.next_ids = next_ids;
+  p.status = (uint32_t *)ws;
+  p.tpl_T = tpl_T;
+  // the template: topological, candidates under the root or candidates,
+  // prompt chains in prompt-id order under candidates
+  if (tpl_parent[0] != -1) return fail(PPD_EINVAL, "template: tpl_parent[0] must be -1");
+  int n_depths = 0;
+  for (int i = 0; i < tpl_T; ++i) {
+    const int par = tpl_parent[i], kind = tpl_kind[i];
+    int depth = 0;
+    if (i > 0) {
+      if (par < 0 || par >= i)
+        return fail(PPD_EINVAL, "template: tpl_parent[%d]=%d is not an earlier node", i, par);
+      const int pk = par > 0 ? tpl_kind[par] : 0;  // the root counts as a candidate
+      depth = p.tpl_depth[par] + 1;
+      if (kind >= 0) {
+        if (pk < 0) return fail(PPD_EINVAL, "template: candidate %d under a prompt token", i);
+        if (kind >= PPD_TOPK_MAX || kind >= vocab)
+          return fail(PPD_EINVAL, "template: rank %d of node %d too large", kind, i);
+        if (depth > PPD_NEXT_MAX_DEPTH)
+          return fail(PPD_EINVAL, "template: candidate depth %d > %d", depth, PPD_NEXT_MAX_DEPTH);
+        p.k_of_depth[depth] = std::max(p.k_of_depth[depth], kind + 1);
+        n_depths = std::max(n_depths, depth);
+      } else {
+        const int j = -kind - 1;
+        if (j >= n_prompt || j > 32766)
+          return fail(PPD_EINVAL, "template: prompt id %d >= n_prompt", j);
+        if (j == 0 ? pk < 0 : pk != -j)
+          return fail(PPD_EINVAL, "template: prompt token %d of node %d out of chain order", j, i);
+      }
+    }
+    if (depth > 127) return fail(PPD_EINVAL, "template too deep");
+    p.tpl_depth[i] = (int8_t)depth;
+    p.tpl_kind[i] = (int16_t)(i == 0 ? 0 : std::max(kind, -32768));
+  }
+  PPD_TRY_HIP(launch_next_tree(p, n_depths, (hipStream_t)stream));
+  return PPD_OK;
+}
+
 ppd_status ppd_device_status(void *ws, size_t ws_bytes, uint32_t *status_out, int32_t clear,
                              void *stream) {
   if (!ws || ws_bytes < 16 || !status_out) return fail(PPD_EINVAL, "NULL or short workspace");

@@ -159,6 +159,22 @@ struct AttnLaunch {
 };
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s);
 
+// next-step candidate generation (k_next.hip)
+#define PPD_NEXT_MAX_DEPTH 15
+struct NextTreeLaunch {
+  const int32_t *parent, *ids;  // this step's tree
+  int T, vocab;
+  const float *logits;          // [T][vocab]
+  const int32_t *path, *n_path, *next_tok;
+  int32_t *next_ids;            // [tpl_T]
+  uint32_t *status;
+  int tpl_T;
+  int8_t tpl_depth[PPD_T_MAX];  // template node depth (root 0)
+  int16_t tpl_kind[PPD_T_MAX];  // rank of a candidate, or -1 - prompt id
+  int k_of_depth[PPD_NEXT_MAX_DEPTH + 1];  // ranks needed at each depth (0: none)
+};
+hipError_t launch_next_tree(const NextTreeLaunch &p, int n_depths, hipStream_t s);
+
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
                         int T, int vocab, int n_prompt, int H, const void *gain, float *x,
                         void *xg, float *ss, uint32_t *status, hipStream_t s);

@@ -142,3 +142,32 @@ def test_packed_weight_sizes_and_rejections():
     assert L.ppd_pack_weight(ppd.PPD_W_O, 512, 512, f, None, None) == ppd.PPD_EINVAL
     assert L.ppd_pack_weight(ppd.PPD_W_O, 500, 512, f, f, None) == ppd.PPD_EUNSUPPORTED
     assert L.ppd_pack_weight(9, 512, 512, f, f, None) == ppd.PPD_EINVAL
+
+
+def test_next_tree_rejects_before_enqueue():
+    """Template and argument checks of ppd_next_tree (host side, nothing is
+    enqueued on failure)."""
+    import numpy as np
+    L = ppd.lib()
+    f = 0x4000
+
+    def call(tp, tk, T=8, vocab=100, n_prompt=3, ws=f, wsb=64, logits=f):
+        tp = np.asarray(tp, np.int32)
+        tk = np.asarray(tk, np.int32)
+        return L.ppd_next_tree(T, f, f, vocab, n_prompt, logits, f, f, f, len(tp),
+                               tp.ctypes.data, tk.ctypes.data, f, ws, wsb, None)
+    assert call([0, 0], [0, 0]) == ppd.PPD_EINVAL                  # root not -1
+    assert call([-1, 1], [0, 0]) == ppd.PPD_EINVAL                 # not topological
+    assert call([-1, 0, 1], [0, -1, 0]) == ppd.PPD_EINVAL          # candidate under prompt
+    assert call([-1, 0, 0], [0, 0, -2]) == ppd.PPD_EINVAL          # prompt 1 under root
+    assert call([-1, 0], [0, 16]) == ppd.PPD_EINVAL                # rank >= PPD_TOPK_MAX
+    assert call([-1, 0], [0, 5], vocab=5) == ppd.PPD_EINVAL        # rank >= vocab
+    assert call([-1, 0], [0, -4]) == ppd.PPD_EINVAL                # prompt id >= n_prompt
+    deep = [-1] + list(range(16))
+    assert call(deep, [0] * 17) == ppd.PPD_EINVAL                  # depth 16 > 15
+    assert call([-1, 0], [0, 0], T=0) == ppd.PPD_EINVAL
+    assert call([-1, 0], [0, 0], T=129) == ppd.PPD_EINVAL
+    assert call([-1, 0], [0, 0], ws=None) == ppd.PPD_EWORKSPACE
+    assert call([-1, 0], [0, 0], logits=None) == ppd.PPD_EINVAL
+    assert call(list(range(-1, 128)), [0] * 129) == ppd.PPD_EINVAL  # template > PPD_T_MAX
+    assert "template" in ppd.ppd_last_error()

@@ -1,0 +1,129 @@
+"""GPU parity of next-step candidate generation (ppd_next_tree) and the
+device-only decode loop verify -> accept -> compact -> next tree.
+
+The ids are integer selections: compared bit-exactly with the oracle's
+`next_tree_ids` on the same float32 logits.  The closed loop on the fp32 tiny
+decoder must emit exactly the vanilla greedy sequence (lossless)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2405_18628_amd as ppd
+from gpu_cases import make_case, say, tree_tensors, workspace
+from synth import workload
+from synth.trees import RANK_PATHS_15, Tree, make_template, make_tree
+
+pytestmark = pytest.mark.gpu
+
+
+def _with_chains(tree: Tree, vocab: int, n_prompt: int, rng) -> Tree:
+    """Add a prompt chain under every candidate that has none (so that any
+    accepted node carries one), keeping topological order; some chains are
+    cut short to exercise the fallback."""
+    parent, ids = tree.parent.tolist(), tree.ids.tolist()
+    has = set(parent[i] for i in range(len(parent)) if ids[i] == vocab)
+    for c in range(tree.n_candidates):
+        if c in has or len(parent) + n_prompt > 128:
+            continue
+        m = int(rng.integers(0, n_prompt + 1))
+        prev = c
+        for j in range(m):
+            parent.append(prev)
+            ids.append(vocab + j)
+            prev = len(parent) - 1
+    return Tree(np.asarray(parent, np.int32), np.asarray(ids, np.int32), tree.n_candidates)
+
+
+def _synthetic_logits(T, V, rng, nan_rows=()):
+    x = rng.integers(-20, 21, (T, V)).astype(np.float32) * 0.25   # many ties
+    for r in nan_rows:
+        x[r, rng.integers(0, V, 7)] = np.nan
+    return x
+
+
+@pytest.mark.parametrize("V,spec,tpl_paths,seed", [
+    (1000, "candidates:10", RANK_PATHS_15, 1),
+    (32000, "total:40", RANK_PATHS_15, 2),
+    (37, "candidates:6", [(0,), (15,), (2,), (0, 3), (2, 0), (2, 0, 1)], 3),
+    (32000, "chain:1", [(0,), (1,), (0, 0)], 4),
+])
+def test_next_tree_ids_bit_exact(V, spec, tpl_paths, seed):
+    rng = np.random.default_rng(seed)
+    n_prompt = 3
+    if spec.startswith("chain"):
+        tree = Tree(np.asarray([-1], np.int32), np.asarray([5], np.int32), 1)
+    else:
+        tree = make_tree(spec, V, n_prompt, 4, 100 + seed, 3)
+    tree = _with_chains(tree, V, n_prompt, rng)
+    tpl = make_template(tpl_paths, n_prompt)
+    O.validate_template(tpl.parent, tpl.kind, n_prompt)
+    T = tree.T
+    tt = tree_tensors(tree)
+    ws = torch.zeros(256, dtype=torch.uint8, device="cuda")
+    for trial in range(6):
+        a = int(rng.integers(0, tree.n_candidates))
+        path = O.path_tokens(tree.parent, list(range(T)), a)
+        logits = _synthetic_logits(T, V, rng, nan_rows=[trial % T] if trial % 2 else [])
+        nxt = int(rng.integers(0, V))
+        say(f"[next] V={V} T={T} tpl={tpl.T} accepted={a} trial={trial}")
+        path_d = torch.tensor(path + [0] * (T - len(path)), dtype=torch.int32, device="cuda")
+        n_path = torch.tensor([len(path)], dtype=torch.int32, device="cuda")
+        nxt_d = torch.tensor([nxt], dtype=torch.int32, device="cuda")
+        out = torch.full((tpl.T,), -9, dtype=torch.int32, device="cuda")
+        ppd.ppd_next_tree(T, tt["parent"], tt["ids"], V, n_prompt, torch.from_numpy(logits).cuda(),
+                          path_d, n_path, nxt_d, tpl.parent, tpl.kind, out, ws)
+        torch.cuda.synchronize()
+        ref = O.next_tree_ids(tree.parent, tree.ids, V, path, nxt, logits.astype(np.float64),
+                              tpl.parent, tpl.kind)
+        assert out.cpu().numpy().tolist() == ref.tolist()
+
+
+def test_closed_loop_on_device_is_lossless():
+    """Six decode steps with nothing but device calls between them (the
+    template's parent, depth and mask are uploaded once): the emitted tokens
+    equal the oracle's vanilla greedy continuation."""
+    case = make_case(workload("tiny"))
+    sh = case.shape
+    tpl = make_template([(0,), (1,), (2,), (0, 0), (0, 1), (1, 0), (0, 0, 0)], 3)
+    T = tpl.T
+    depth, mask = ppd.ppd_build_tree_mask(tpl.parent)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    parent_d, depth_d, mask_d = dev(tpl.parent.astype(np.int32)), dev(depth), dev(mask.view(np.int64))
+    rng = np.random.default_rng(5)
+    ids0 = rng.integers(0, sh.vocab, T).astype(np.int32)
+    ids0[0] = case.root
+    ids0[tpl.kind < 0] = sh.vocab + (-tpl.kind[tpl.kind < 0] - 1)
+    ids = dev(ids0)
+    ws = workspace(case, T)
+    logits = torch.empty((T, sh.vocab), dtype=torch.float32, device="cuda")
+    pred = torch.empty(T, dtype=torch.int32, device="cuda")
+    path = torch.zeros(T, dtype=torch.int32, device="cuda")
+    n_path = torch.zeros(1, dtype=torch.int32, device="cuda")
+    nxt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    nids = torch.zeros(T, dtype=torch.int32, device="cuda")
+    len_dev = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kv = ppd.KVCache(case.k, case.v, len_dev)
+    k0, v0 = case.k.clone(), case.v.clone()
+    L, emitted = case.L, []
+    for s in range(6):
+        ppd.ppd_verify_step(case.model, kv, L, T, ids, depth_d, mask_d, ws, logits, pred)
+        ppd.ppd_accept(T, parent_d, ids, pred, sh.vocab, path, n_path, nxt, ws)
+        ppd.ppd_kv_compact(case.model, kv, L, path, n_path)
+        ppd.ppd_next_tree(T, parent_d, ids, sh.vocab, sh.n_prompt, logits, path, n_path, nxt,
+                          tpl.parent, tpl.kind, nids, ws)
+        torch.cuda.synchronize()          # the test reads the tokens; the loop does not need to
+        n = int(n_path.item())
+        p = path[:n].cpu().tolist()
+        cur = ids.cpu().tolist()
+        emitted += [cur[j] for j in p[1:]] + [int(nxt.item())]
+        say(f"[loop] step {s}: accepted {n - 1}, L={L}")
+        L += n
+        assert int(len_dev.item()) == L
+        ids.copy_(nids)
+    assert ppd.ppd_device_status(ws) == 0
+    ref = O.greedy_decode(case.oracle_model, case.kc_host, case.vc_host, case.L, case.root,
+                          len(emitted), "f32")
+    assert emitted == ref
+    case.k.copy_(k0)
+    case.v.copy_(v0)
