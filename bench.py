@@ -190,12 +190,15 @@ def main():
     for _ in range(3):
         next_tree()
     torch.cuda.synchronize()
-    e0.record()
+    next_us = 0.0
+    st, sp = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    keep = ppd.ppd_set_kernel_timer("next_tree", [st], [sp])
     for _ in range(args.steps):
         next_tree()
-    e1.record()
-    torch.cuda.synchronize()
-    next_us = e0.elapsed_time(e1) / args.steps * 1e3
+        torch.cuda.synchronize()
+        next_us += st.elapsed_time(sp) * 1e3 / args.steps
+    ppd.ppd_set_kernel_timer("next_tree")
+    del keep
 
     alg = step_bytes(sh, L, T, n_acc)
     flops = step_flops(sh, L, T)

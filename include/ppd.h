@@ -235,11 +235,13 @@ ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
  *                            the accepted node itself when it has none);
  *   tpl_kind[i] = -1 - j     prompt token j (id vocab + j).
  * Ranks order larger logits first, equal logits by smaller index, NaN last
- * (a NaN among the selected ranks sets PPD_DEV_NAN_LOGIT).  The template's
+ * (a NaN among the selected ranks sets PPD_DEV_NAN_LOGIT).  One workgroup
+ * per candidate depth reads one logits row.  The template's
  * parent/depth/mask are the caller's (ppd_build_tree_mask on tpl_parent).
  *   T, parent, ids    this step's tree (device int32[T])
  *   logits            device float32[T][vocab] written by ppd_verify_step
- *   path, n_path, next_tok   device, as written by ppd_accept
+ *   path, n_path, next_tok   device, as written by ppd_accept (path holds
+ *                     T entries, all read)
  *   tpl_T, tpl_parent, tpl_kind   HOST arrays of tpl_T entries (copied into
  *                     the launch; the call keeps no pointer to them)
  *   next_ids          device int32[tpl_T] (output)
@@ -262,7 +264,8 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
  * `kind` in the step (i < n_events) with start_events[i] / stop_events[i]
  * attached to the dispatch itself (hipExtLaunchKernelGGL), so they take the
  * kernel's own start and end times on the step's stream.  kind: 0 QKV GEMM, 1 tree attention, 2 output
- * projection, 3 gate/up GEMM, 4 down projection, 5 LM head.  The arrays are
+ * projection, 3 gate/up GEMM, 4 down projection, 5 LM head; kind 6 times
+ * the one kernel of each ppd_next_tree call instead (with the first events).  The arrays are
  * host arrays of hipEvent_t and must stay valid while set; n_events = 0
  * disables.  Thread-local setting.
  */

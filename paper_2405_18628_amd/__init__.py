@@ -281,7 +281,8 @@ def ppd_device_status(ws, clear: bool = False, stream=None) -> int:
     return int(out.value)
 
 
-KERNEL_KINDS = {"qkv": 0, "attention": 1, "o_proj": 2, "gate_up": 3, "down": 4, "lm_head": 5}
+KERNEL_KINDS = {"qkv": 0, "attention": 1, "o_proj": 2, "gate_up": 3, "down": 4, "lm_head": 5,
+                "next_tree": 6}
 
 
 def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):

@@ -12,73 +12,131 @@
 // nodes carry fixed prompt ids.  Ranks order larger logits first, equal ones
 // by smaller index, NaN last.
 //
-// One workgroup per candidate depth: it walks the accepted node's prompt
-// chain, selects the top kd of one logits row (each thread keeps a sorted
-// list of the K best of its strided elements, K >= kd; kd rounds of a
-// workgroup-wide maximum over the lists' heads then emit the ranks in
-// order), and writes the template's candidates at its depth.  Workgroup 0 also writes the root and the prompt
-// nodes.
+// One workgroup of 1024 threads per candidate depth.  It walks the accepted
+// node's prompt chain, then selects the top kd of one logits row:
+//   1. every thread holds 32 strided elements of the row in registers (all
+//      loads in flight at once) and takes its best one;
+//   2. the kd-th best of the 16 wave maxima (kd <= 16) is reached by at
+//      least kd elements, so every element of the top kd reaches it;
+//   3. the elements that reach it (only threads whose best does) go to a
+//      list in LDS, and each is ranked by counting the list entries that
+//      beat it.
+// Comparisons use one 64-bit key per element that orders (value, index) as
+// the ranks do, so selection is integer max / compare without branches.
+// If the list would overflow, kd rounds of a workgroup-wide maximum over the
+// elements below the previous pick select the ranks instead.
 #include "ppd_internal.h"
 
 namespace {
 
-// (value, index) ordered as in the rank definition: a NaN loses to every
-// number, numbers compare by value, then by smaller index
-struct Cand {
-  float v;
-  int i;  // INT_MAX: empty
-};
+constexpr int kThreads = 1024;
+constexpr int kPer = 32;                    // row elements per thread per chunk
+constexpr int kChunk = kThreads * kPer;     // row elements per chunk
+constexpr int kListCap = 2048;              // candidate list capacity
 
-__device__ __forceinline__ bool beats(const Cand &a, const Cand &b) {
-  if (a.i == INT_MAX) return false;
-  if (b.i == INT_MAX) return true;
-  const bool an = a.v != a.v, bn = b.v != b.v;
-  if (an != bn) return bn;
-  if (an) return a.i < b.i;
-  return a.v > b.v || (a.v == b.v && a.i < b.i);
+// Rank key of (value, index): a larger key ranks first.  The high word maps
+// the float monotonically onto unsigned order (-0 as +0, every NaN to 0,
+// below all numbers), the low word is ~index, so equal values rank the
+// smaller index first.  Key 0 is "no element": every element's low word
+// is at least 2^31.
+__device__ __forceinline__ uint32_t value_word(float v) {
+  uint32_t b = __float_as_uint(v);
+  const uint32_t mag = b & 0x7fffffffu;
+  b = mag == 0 ? 0u : b;
+  const uint32_t k = b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+  return mag > 0x7f800000u ? 0u : k;
+}
+__device__ __forceinline__ uint64_t make_key(uint32_t hi, int idx) {
+  return ((uint64_t)hi << 32) | (uint32_t)~idx;
+}
+__device__ __forceinline__ int key_index(uint64_t key) { return (int)~(uint32_t)key; }
+__device__ __forceinline__ bool key_is_nan(uint64_t key) { return (uint32_t)(key >> 32) == 0; }
+
+__device__ __forceinline__ uint64_t lane_key(uint64_t k, int j) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)k, j);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(k >> 32), j);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-// K: list length, a power of two >= every depth's rank count kd
-template <int K>
-__global__ __launch_bounds__(256) void next_tree_kernel(NextTreeLaunch p) {
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_key(uint64_t k) {
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)k, CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(k >> 32), CTRL, 0xf, 0xf, false);
+  return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+// maximum key over the wave, in every lane: lane pairs within quads (DPP
+// quad permutations), 8-lane halves (half-row mirror), 16-lane rows (row
+// mirror), row pairs and wave halves (permlane swaps)
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+  k = umax64(k, dpp_key<0xb1>(k));   // quad_perm [1,0,3,2]
+  k = umax64(k, dpp_key<0x4e>(k));   // quad_perm [2,3,0,1]
+  k = umax64(k, dpp_key<0x141>(k));  // row_half_mirror
+  k = umax64(k, dpp_key<0x140>(k));  // row_mirror
+  uint32_t lo = (uint32_t)k, hi = (uint32_t)(k >> 32);
+  auto l16 = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+  auto h16 = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+  k = umax64(((uint64_t)h16[0] << 32) | l16[0], ((uint64_t)h16[1] << 32) | l16[1]);
+  lo = (uint32_t)k;
+  hi = (uint32_t)(k >> 32);
+  auto l32 = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+  auto h32 = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  return umax64(((uint64_t)h32[0] << 32) | l32[0], ((uint64_t)h32[1] << 32) | l32[1]);
+}
+
+// MULTI: the row spans several register chunks (reloaded in each pass);
+// VEC: rows are 16-byte aligned, read in float4 (a thread's elements are
+// then runs of 4)
+template <bool MULTI, bool VEC>
+__global__ __launch_bounds__(kThreads) void next_tree_kernel(NextTreeLaunch p) {
   __shared__ int chain_s[PPD_NEXT_MAX_DEPTH + 1];
-  __shared__ int found_s;
-  __shared__ Cand wave_best[4];
+  __shared__ int found_s, count_s, nan_s;
+  __shared__ uint64_t wave_s[kThreads / 64];
+  __shared__ uint64_t list_s[kListCap];
   __shared__ int top_s[PPD_TOPK_MAX];
-  __shared__ int nan_s;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = blockIdx.x + 1;  // candidate depth handled here
   const int kd = p.k_of_depth[d];
+  const int V = p.vocab;
+
+  // this step's tree and accepted path, one node per thread
+  int my_par = -2, my_id = -1, my_path = 0;
+  if (tid < p.T) {
+    my_par = p.parent[tid];
+    my_id = p.ids[tid];
+    my_path = p.path[tid];
+  }
 
   // ---- root and prompt nodes (workgroup 0)
   if (blockIdx.x == 0) {
-    for (int i = tid; i < p.tpl_T; i += blockDim.x) {
+    for (int i = tid; i < p.tpl_T; i += kThreads) {
       const int kind = p.tpl_kind[i];
       if (i == 0)
         p.next_ids[0] = *p.next_tok;
       else if (kind < 0)
-        p.next_ids[i] = p.vocab + (-kind - 1);
+        p.next_ids[i] = V + (-kind - 1);
     }
   }
   if (kd == 0) return;  // no candidate at this depth
 
   // ---- the accepted node and its prompt chain, up to depth d
   if (tid == 0) {
-    const int n = min(max(*p.n_path, 1), p.T);
-    int a = p.path[n - 1];
-    a = min(max(a, 0), p.T - 1);
-    chain_s[0] = a;
+    found_s = min(max(*p.n_path, 1), p.T) - 1;  // the accepted node's place on the path
     nan_s = 0;
+    count_s = 0;
   }
+  __syncthreads();
+  if (tid == found_s) chain_s[0] = min(max(my_path, 0), p.T - 1);
   __syncthreads();
   int src = chain_s[0];
   for (int j = 0; j < d; ++j) {
     const int cur = chain_s[j];
     if (tid == 0) found_s = INT_MAX;
     __syncthreads();
-    for (int i = tid; i < p.T; i += blockDim.x)
-      if (p.parent[i] == cur && p.ids[i] == p.vocab + j) atomicMin(&found_s, i);
+    if (my_par == cur && my_id == V + j) atomicMin(&found_s, tid);
     __syncthreads();
     const int f = found_s;
     if (f == INT_MAX) break;  // uniform: the chain ends here
@@ -87,53 +145,136 @@ __global__ __launch_bounds__(256) void next_tree_kernel(NextTreeLaunch p) {
     __syncthreads();
   }
 
-  // ---- per-thread sorted lists of the kd best strided elements of the row
-  const float *row = p.logits + (size_t)src * p.vocab;
-  Cand lst[K];
+  // ---- 1. the row in registers (as value words), each thread's best
+  const float *row = p.logits + (size_t)src * V;
+  const int n_chunks = MULTI ? (V + kChunk - 1) / kChunk : 1;
+  // row index of this thread's element e of chunk c (grows with e)
+  auto eidx = [&](int c, int e) {
+    return VEC ? c * kChunk + 4 * ((e >> 2) * kThreads + tid) + (e & 3)
+               : c * kChunk + e * kThreads + tid;
+  };
+  uint32_t h[kPer];
+  auto load = [&](int c) {
+    float x[kPer];
+    if (VEC) {
+      const float4 *row4 = (const float4 *)row;
+      const int V4 = V >> 2;
 #pragma unroll
-  for (int k = 0; k < K; ++k) lst[k] = Cand{0.f, INT_MAX};
-  for (int v = tid; v < p.vocab; v += blockDim.x) {
-    Cand c{row[v], v};
-    if (!beats(c, lst[K - 1])) continue;
-    // sorted insertion: walking from the best, c takes the first slot it
-    // beats and the displaced entry moves on (the worst falls off)
+      for (int j = 0; j < kPer / 4; ++j) {
+        const float4 v = row4[min(c * (kChunk / 4) + j * kThreads + tid, V4 - 1)];
+        x[4 * j] = v.x;
+        x[4 * j + 1] = v.y;
+        x[4 * j + 2] = v.z;
+        x[4 * j + 3] = v.w;
+      }
+    } else {
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-      if (beats(c, lst[k])) {
-        const Cand t = lst[k];
-        lst[k] = c;
-        c = t;
+      for (int e = 0; e < kPer; ++e) x[e] = row[min(eidx(c, e), V - 1)];
+    }
+    __builtin_amdgcn_sched_barrier(0);  // all loads in flight before the first use
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) h[e] = value_word(x[e]);
+  };
+  auto key_of = [&](int c, int e) -> uint64_t {
+    const int idx = eidx(c, e);
+    return idx < V ? make_key(h[e], idx) : 0;
+  };
+  uint64_t best = 0;
+  for (int c = 0; c < n_chunks; ++c) {
+    load(c);
+    // indices grow with e: the first maximal word has the smallest index
+    uint32_t bh = h[0];
+    int be = 0;
+#pragma unroll
+    for (int e = 1; e < kPer; ++e) {
+      const bool take = (h[e] > bh) & (eidx(c, e) < V);
+      bh = take ? h[e] : bh;
+      be = take ? e : be;
+    }
+    const int bi = eidx(c, be);
+    best = umax64(best, bi < V ? make_key(bh, bi) : 0);
+  }
+
+  // ---- 2. threshold: the kd-th best of the 16 wave maxima (kd <= 16)
+  const uint64_t wmax = wave_max_key(best);
+  if (lane == 0) wave_s[wave] = wmax;
+  __syncthreads();
+  uint64_t tau = 0;
+  {
+    const uint64_t mine = lane < kThreads / 64 ? wave_s[lane] : 0;
+    int rank = 0;
+#pragma unroll
+    for (int q = 0; q < kThreads / 64; ++q) rank += wave_s[q] > mine ? 1 : 0;
+    const unsigned long long sel = __ballot(lane < kThreads / 64 && rank == kd - 1 && mine != 0);
+    if (sel) tau = lane_key(mine, __builtin_ctzll(sel));
+  }
+  // tau == 0 (no threshold) only when fewer than kd waves hold elements,
+  // so the row is shorter than the list
+
+  // ---- 3. the elements reaching the threshold, ranked by counting
+  const uint64_t t1 = tau == 0 ? 1 : tau;  // empty keys (0) never reach it
+  if (best >= t1) {
+    for (int c = 0; c < n_chunks; ++c) {
+      if (MULTI) load(c);
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) {
+        const uint64_t k = key_of(c, e);
+        if (k >= t1) {
+          const int slot = atomicAdd(&count_s, 1);
+          if (slot < kListCap) list_s[slot] = k;
+        }
       }
     }
   }
-
-  // ---- kd rounds: the workgroup's best head is rank r; its owner pops it
-  for (int r = 0; r < kd; ++r) {
-    Cand b = lst[0];
+  __syncthreads();
+  const int n = count_s;
+  if (n <= kListCap) {
+    for (int i = tid; i < n; i += kThreads) {
+      const uint64_t c = list_s[i];
+      int r = 0;
+      for (int j = 0; j < n; ++j) r += list_s[j] > c ? 1 : 0;
+      if (r < kd) {
+        top_s[r] = key_index(c);
+        if (key_is_nan(c)) nan_s = 1;
+      }
+    }
+  } else {
+    // kd rounds of a workgroup maximum over the keys below the previous
+    // pick (the row has more than kListCap > kd elements)
+    uint64_t last = ~0ull;
+    for (int r = 0; r < kd; ++r) {
+      uint64_t b = 0;
+      for (int c = 0; c < n_chunks; ++c) {
+        if (MULTI) load(c);
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      Cand o{__shfl_xor(b.v, off, 64), __shfl_xor(b.i, off, 64)};
-      if (beats(o, b)) b = o;
-    }
-    if (lane == 0) wave_best[wave] = b;
-    __syncthreads();
-    Cand w = wave_best[0];
-    for (int q = 1; q < 4; ++q)
-      if (beats(wave_best[q], w)) w = wave_best[q];
-    if (tid == 0) {
-      top_s[r] = w.i == INT_MAX ? 0 : w.i;
-      if (w.i == INT_MAX || w.v != w.v) nan_s = 1;
-    }
-    if (lst[0].i == w.i && w.i != INT_MAX) {  // the owner: drop its head
+        for (int e = 0; e < kPer; ++e) {
+          const uint64_t k = key_of(c, e);
+          b = umax64(b, k < last ? k : 0);
+        }
+      }
 #pragma unroll
-      for (int k = 0; k < K - 1; ++k) lst[k] = lst[k + 1];
-      lst[K - 1] = Cand{0.f, INT_MAX};
+      for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)b, off, 64);
+        const uint32_t hi = __shfl_xor((uint32_t)(b >> 32), off, 64);
+        b = umax64(b, ((uint64_t)hi << 32) | lo);
+      }
+      __syncthreads();  // wave_s is still read above / in the last round
+      if (lane == 0) wave_s[wave] = b;
+      __syncthreads();
+      uint64_t w = 0;
+#pragma unroll
+      for (int q = 0; q < kThreads / 64; ++q) w = umax64(w, wave_s[q]);
+      if (tid == 0) {
+        top_s[r] = key_index(w);
+        if (key_is_nan(w)) nan_s = 1;
+      }
+      last = w;
     }
-    __syncthreads();  // wave_best is rewritten next round
   }
+  __syncthreads();
 
   // ---- the template's candidates at depth d
-  for (int i = tid; i < p.tpl_T; i += blockDim.x)
+  for (int i = tid; i < p.tpl_T; i += kThreads)
     if (i > 0 && p.tpl_depth[i] == d && p.tpl_kind[i] >= 0) p.next_ids[i] = top_s[p.tpl_kind[i]];
   if (tid == 0 && nan_s) atomicOr(p.status, PPD_DEV_NAN_LOGIT);
 }
@@ -141,18 +282,14 @@ __global__ __launch_bounds__(256) void next_tree_kernel(NextTreeLaunch p) {
 }  // namespace
 
 hipError_t launch_next_tree(const NextTreeLaunch &p, int n_depths, hipStream_t s) {
-  int kmax = 1;
-  for (int d = 1; d <= PPD_NEXT_MAX_DEPTH; ++d) kmax = max(kmax, p.k_of_depth[d]);
-  const dim3 grid(max(1, n_depths)), block(256);
-  if (kmax <= 1)
-    hipLaunchKernelGGL(next_tree_kernel<1>, grid, block, 0, s, p);
-  else if (kmax <= 2)
-    hipLaunchKernelGGL(next_tree_kernel<2>, grid, block, 0, s, p);
-  else if (kmax <= 4)
-    hipLaunchKernelGGL(next_tree_kernel<4>, grid, block, 0, s, p);
-  else if (kmax <= 8)
-    hipLaunchKernelGGL(next_tree_kernel<8>, grid, block, 0, s, p);
+  const dim3 grid(max(1, n_depths)), block(kThreads);
+  const bool vec = p.vocab % 4 == 0 && (uintptr_t)p.logits % 16 == 0;
+  auto kernel = p.vocab > kChunk ? (vec ? next_tree_kernel<true, true> : next_tree_kernel<true, false>)
+                                 : (vec ? next_tree_kernel<false, true> : next_tree_kernel<false, false>);
+  if (p.ev_start)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, (hipEvent_t)p.ev_start,
+                          (hipEvent_t)p.ev_stop, 0, p);
   else
-    hipLaunchKernelGGL(next_tree_kernel<16>, grid, block, 0, s, p);
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, p);
   return hipGetLastError();
 }

@@ -26,7 +26,7 @@ struct KernelTimer {
 };
 thread_local KernelTimer g_timer;
 
-enum TimedKind { TK_QKV = 0, TK_ATTN = 1, TK_O = 2, TK_GATEUP = 3, TK_DOWN = 4, TK_LM = 5 };
+enum TimedKind { TK_QKV = 0, TK_ATTN = 1, TK_O = 2, TK_GATEUP = 3, TK_DOWN = 4, TK_LM = 5, TK_NEXT = 6 };
 
 // Events of the next timed launch of `kind` (both null when not timed).  The
 // kernel is then launched with hipExtLaunchKernelGGL, which records them at
@@ -560,6 +560,8 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
     p.tpl_depth[i] = (int8_t)depth;
     p.tpl_kind[i] = (int16_t)(i == 0 ? 0 : std::max(kind, -32768));
   }
+  if (g_timer.kind == TK_NEXT) g_timer.next = 0;  // one timed launch per call
+  timer_events(TK_NEXT, &p.ev_start, &p.ev_stop);
   PPD_TRY_HIP(launch_next_tree(p, n_depths, (hipStream_t)stream));
   return PPD_OK;
 }
@@ -580,7 +582,7 @@ ppd_status ppd_set_kernel_timer(int32_t kind, void *const *start_events, void *c
     g_timer = KernelTimer{};
     return PPD_OK;
   }
-  if (kind < TK_QKV || kind > TK_LM || !start_events || !stop_events)
+  if (kind < TK_QKV || kind > TK_NEXT || !start_events || !stop_events)
     return fail(PPD_EINVAL, "bad kernel timer arguments");
   g_timer.kind = kind;
   g_timer.start = start_events;

@@ -172,6 +172,7 @@ struct NextTreeLaunch {
   int8_t tpl_depth[PPD_T_MAX];  // template node depth (root 0)
   int16_t tpl_kind[PPD_T_MAX];  // rank of a candidate, or -1 - prompt id
   int k_of_depth[PPD_NEXT_MAX_DEPTH + 1];  // ranks needed at each depth (0: none)
+  void *ev_start, *ev_stop;     // optional events on the dispatch (profiling)
 };
 hipError_t launch_next_tree(const NextTreeLaunch &p, int n_depths, hipStream_t s);
 

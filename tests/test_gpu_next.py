@@ -35,20 +35,42 @@ def _with_chains(tree: Tree, vocab: int, n_prompt: int, rng) -> Tree:
     return Tree(np.asarray(parent, np.int32), np.asarray(ids, np.int32), tree.n_candidates)
 
 
-def _synthetic_logits(T, V, rng, nan_rows=()):
-    x = rng.integers(-20, 21, (T, V)).astype(np.float32) * 0.25   # many ties
+def _synthetic_logits(T, V, rng, nan_rows=(), kind="ties"):
+    if kind == "ties":
+        x = rng.integers(-20, 21, (T, V)).astype(np.float32) * 0.25   # many ties
+    elif kind == "normal":
+        x = rng.standard_normal((T, V)).astype(np.float32)
+    else:
+        # "crowded": element i sits with 1023 others in a group i mod 1024;
+        # groups whose number is below 15 mod 64 hold large values, those at
+        # 15 mod 64 middling ones, so that thousands of elements beat every
+        # 15th-best group maximum among 64 consecutive groups
+        g = np.arange(V) % 1024 % 64
+        x = rng.standard_normal((T, V)).astype(np.float32)
+        x[:, g < 15] += 50.0
+        x[:, g == 15] += 10.0
     for r in nan_rows:
         x[r, rng.integers(0, V, 7)] = np.nan
     return x
 
 
-@pytest.mark.parametrize("V,spec,tpl_paths,seed", [
-    (1000, "candidates:10", RANK_PATHS_15, 1),
-    (32000, "total:40", RANK_PATHS_15, 2),
-    (37, "candidates:6", [(0,), (15,), (2,), (0, 3), (2, 0), (2, 0, 1)], 3),
-    (32000, "chain:1", [(0,), (1,), (0, 0)], 4),
+@pytest.mark.parametrize("V,spec,tpl_paths,seed,kind", [
+    (1000, "candidates:10", RANK_PATHS_15, 1, "ties"),
+    (32000, "total:40", RANK_PATHS_15, 2, "ties"),
+    (37, "candidates:6", [(0,), (15,), (2,), (0, 3), (2, 0), (2, 0, 1)], 3, "ties"),
+    (32000, "chain:1", [(0,), (1,), (0, 0)], 4, "ties"),
+    (32000, "candidates:8", [(0,), (15,), (1,), (0, 15), (0, 3)], 5, "crowded"),
+    (70001, "candidates:8", [(0,), (15,), (1,), (0, 15), (0, 3)], 6, "crowded"),
+    (70001, "total:30", RANK_PATHS_15, 7, "normal"),
+    (1023, "candidates:5", [(0,), (15,), (0, 7)], 8, "normal"),
+    (40000, "total:30", RANK_PATHS_15, 9, "normal"),
+    (65536, "candidates:8", [(0,), (15,), (1,), (0, 15), (0, 3)], 10, "crowded"),
 ])
-def test_next_tree_ids_bit_exact(V, spec, tpl_paths, seed):
+def test_next_tree_ids_bit_exact(V, spec, tpl_paths, seed, kind):
+    """Ranks from rows with many ties and NaNs, Gaussian rows, and rows
+    crowded so that the candidate list overflows (then the ranks come from
+    repeated maxima); rows longer than one register chunk (32768), rows read
+    in float4 (vocab a multiple of 4) and element by element."""
     rng = np.random.default_rng(seed)
     n_prompt = 3
     if spec.startswith("chain"):
@@ -64,7 +86,7 @@ def test_next_tree_ids_bit_exact(V, spec, tpl_paths, seed):
     for trial in range(6):
         a = int(rng.integers(0, tree.n_candidates))
         path = O.path_tokens(tree.parent, list(range(T)), a)
-        logits = _synthetic_logits(T, V, rng, nan_rows=[trial % T] if trial % 2 else [])
+        logits = _synthetic_logits(T, V, rng, nan_rows=[trial % T] if trial % 2 else [], kind=kind)
         nxt = int(rng.integers(0, V))
         say(f"[next] V={V} T={T} tpl={tpl.T} accepted={a} trial={trial}")
         path_d = torch.tensor(path + [0] * (T - len(path)), dtype=torch.int32, device="cuda")
