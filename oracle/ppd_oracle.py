@@ -435,20 +435,38 @@ def path_tokens(parent: Sequence[int], ids: Sequence[int], node: int) -> List[in
 # at the position of the bonus token's (d-1)-th successor, so its output
 # predicts the token at depth d of the next tree (Section 3.1).  Prompt nodes
 # of the template carry fixed prompt ids.
+#
+# Ensemble prompt tokens (Section 3.2; the EPT appendix on masks and
+# aggregation): with n_ept EPTs per prompt token, the EPTs form n_ept
+# disjoint groups, and an EPT of group g sees, besides the input tokens, only
+# the EPTs of group g at earlier positions.  In a tree that is n_ept parallel
+# prompt chains under a node, chain g holding the group-g EPTs of token
+# distances 1, 2, ...; the ancestor mask is then exactly the ensemble mask.
+# The EPT of token distance j (1-based) in group g is prompt embedding
+# (j - 1) * n_ept + g.  The guess for a token distance averages the logits of
+# its n_ept EPTs (the text's "averaging the logits"; the printed formula
+# averages probabilities -- the text's reading is taken).
 
 TOPK_MAX = 16  # largest rank + 1 a template may use per depth
 
 
-def prompt_chain(parent: Sequence[int], ids: Sequence[int], vocab: int, node: int) -> List[int]:
-    """The prompt tokens attached to `node`: p_1 is its child with prompt id 0
-    (token vocab + 0), p_j the child of p_{j-1} with prompt id j - 1 (the chain
-    position j uses prompt embedding j - 1).  Returns [p_1, p_2, ...] (empty if
-    the node carries none); the first such child is taken if several match."""
+def ept_prompt_id(j: int, g: int, n_ept: int) -> int:
+    """Prompt embedding of the EPT of group g at token distance j + 1."""
+    return j * n_ept + g
+
+
+def prompt_chain(parent: Sequence[int], ids: Sequence[int], vocab: int, node: int,
+                 n_ept: int = 1, group: int = 0) -> List[int]:
+    """The prompt tokens of EPT group `group` attached to `node`: p_1 is its
+    child with prompt id ept_prompt_id(0, group), p_j the child of p_{j-1}
+    with prompt id ept_prompt_id(j - 1, group) (with one EPT: prompt id j - 1).
+    Returns [p_1, p_2, ...] (empty if the node carries none); the first such
+    child is taken if several match."""
     T = len(parent)
     chain = []
     cur = int(node)
     while True:
-        want = vocab + len(chain)
+        want = vocab + ept_prompt_id(len(chain), group, n_ept)
         nxt = -1
         for i in range(T):
             if int(parent[i]) == cur and int(ids[i]) == want:
@@ -458,6 +476,20 @@ def prompt_chain(parent: Sequence[int], ids: Sequence[int], vocab: int, node: in
             return chain
         chain.append(nxt)
         cur = nxt
+
+
+def ept_mean_row(rows: Sequence[np.ndarray]) -> np.ndarray:
+    """Average of the EPT groups' logits rows, in float32 as the logits are
+    stored: the rows added in group order, then divided by their count (a
+    single row is returned unchanged).  The ranks taken from it are integer
+    decisions, so both implementations take them on this same float32
+    value."""
+    acc = np.asarray(rows[0], np.float32).copy()
+    for r in rows[1:]:
+        acc = (acc + np.asarray(r, np.float32)).astype(np.float32)
+    if len(rows) > 1:
+        acc = (acc / np.float32(len(rows))).astype(np.float32)
+    return acc
 
 
 def rank_order(row: np.ndarray) -> np.ndarray:
@@ -475,12 +507,15 @@ def template_depths(tpl_parent: Sequence[int]) -> np.ndarray:
     return depth
 
 
-def validate_template(tpl_parent: Sequence[int], tpl_kind: Sequence[int], n_prompt: int) -> None:
+def validate_template(tpl_parent: Sequence[int], tpl_kind: Sequence[int], n_prompt: int,
+                      n_ept: int = 1) -> None:
     """A template is a topological tree (tpl_parent) with a kind per node:
     kind >= 0 is a candidate of that rank (< TOPK_MAX) whose parent is the root
-    or a candidate; kind < 0 is prompt token -kind - 1 (< n_prompt), attached
-    to a candidate (prompt id 0) or to the prompt token one id lower.  Node 0
-    is the root (its kind is ignored)."""
+    or a candidate; kind < 0 is prompt embedding q = -kind - 1, the EPT of
+    group q mod n_ept at token distance q // n_ept + 1 (< n_prompt token
+    distances), attached to a candidate (token distance 1) or to the same
+    group's EPT one token distance lower.  Node 0 is the root (its kind is
+    ignored)."""
     validate_tree(tpl_parent)
     T = len(tpl_parent)
     for i in range(1, T):
@@ -490,26 +525,30 @@ def validate_template(tpl_parent: Sequence[int], tpl_kind: Sequence[int], n_prom
             if k >= TOPK_MAX or (p > 0 and pk < 0):
                 raise ValueError(f"template node {i}: bad candidate")
         else:
-            j = -k - 1
+            j, g = divmod(-k - 1, n_ept)
             if j >= n_prompt:
-                raise ValueError(f"template node {i}: prompt id {j} >= {n_prompt}")
-            if (j == 0 and p > 0 and pk < 0) or (j > 0 and (p == 0 or pk != -j)):
+                raise ValueError(f"template node {i}: token distance {j + 1} > {n_prompt}")
+            if j == 0:
+                if p > 0 and pk < 0:
+                    raise ValueError(f"template node {i}: prompt chain out of order")
+            elif p == 0 or pk != -1 - ept_prompt_id(j - 1, g, n_ept):
                 raise ValueError(f"template node {i}: prompt chain out of order")
 
 
 def next_tree_ids(parent: Sequence[int], ids: Sequence[int], vocab: int, path: Sequence[int],
                   next_tok: int, logits: np.ndarray, tpl_parent: Sequence[int],
-                  tpl_kind: Sequence[int]) -> np.ndarray:
+                  tpl_kind: Sequence[int], n_ept: int = 1) -> np.ndarray:
     """Token ids of the next step's tree (template tpl_parent / tpl_kind).
 
     Root: next_tok, the bonus token.  Candidate at template depth d with rank
-    r: rank_order(logits[src])[r], where src is the accepted node's d-th prompt
-    token; for d beyond its prompt chain, the chain's deepest node (or the
+    r: rank_order(row)[r], where row is the logits of the accepted node's d-th
+    prompt token -- with n_ept > 1, ept_mean_row over the d-th EPT of every
+    group's chain.  For d beyond a chain, that chain's deepest node (or the
     accepted node itself when it carries none) -- a reading of this build:
     the template stays fixed, and exact-match verification keeps the output
     lossless whatever the guesses.  Prompt nodes: vocab + prompt id."""
     a = int(path[-1])
-    chain = prompt_chain(parent, ids, vocab, a)
+    chains = [prompt_chain(parent, ids, vocab, a, n_ept, g) for g in range(n_ept)]
     depth = template_depths(tpl_parent)
     T = len(tpl_parent)
     out = np.zeros(T, np.int64)
@@ -521,8 +560,9 @@ def next_tree_ids(parent: Sequence[int], ids: Sequence[int], vocab: int, path: S
             out[i] = vocab + (-k - 1)
             continue
         d = int(depth[i])
-        src = chain[d - 1] if d <= len(chain) else (chain[-1] if chain else a)
-        if src not in order_of:
-            order_of[src] = rank_order(logits[src])
-        out[i] = int(order_of[src][k])
+        srcs = tuple(ch[d - 1] if d <= len(ch) else (ch[-1] if ch else a) for ch in chains)
+        if srcs not in order_of:
+            row = logits[srcs[0]] if n_ept == 1 else ept_mean_row([logits[s] for s in srcs])
+            order_of[srcs] = rank_order(row)
+        out[i] = int(order_of[srcs][k])
     return out

@@ -154,12 +154,13 @@ class Template:
         return int(self.parent.shape[0])
 
 
-def make_template(rank_paths=RANK_PATHS_15, n_prompt: int = 3) -> Template:
+def make_template(rank_paths=RANK_PATHS_15, n_prompt: int = 3, n_ept: int = 1) -> Template:
     """Root, then the candidates of `rank_paths` (each path's prefix must come
-    earlier), then a chain of n_prompt prompt tokens under the root and under
-    every candidate, in node order.  Every node carries a chain, so whichever
-    node is accepted, the next tree's guesses come from its own prompt tokens.
-    Default: 1 + 15 candidates, 16 chains of 3 -> T = 64."""
+    earlier), then under the root and under every candidate n_ept parallel
+    chains of n_prompt prompt tokens (chain g: prompt ids j * n_ept + g for
+    j = 0 .. n_prompt - 1), in node order.  Every node carries chains, so
+    whichever node is accepted, the next tree's guesses come from its own
+    prompt tokens.  Default: 1 + 15 candidates, 16 chains of 3 -> T = 64."""
     parent, kind = [-1], [0]
     node_of = {(): 0}
     for path in rank_paths:
@@ -169,11 +170,12 @@ def make_template(rank_paths=RANK_PATHS_15, n_prompt: int = 3) -> Template:
         node_of[path] = len(parent) - 1
     n_cand = len(parent)
     for c in range(n_cand):
-        prev = c
-        for j in range(n_prompt):
-            parent.append(prev)
-            kind.append(-1 - j)
-            prev = len(parent) - 1
+        for g in range(n_ept):
+            prev = c
+            for j in range(n_prompt):
+                parent.append(prev)
+                kind.append(-1 - (j * n_ept + g))
+                prev = len(parent) - 1
     return Template(np.asarray(parent, np.int32), np.asarray(kind, np.int32))
 
 

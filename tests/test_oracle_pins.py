@@ -506,3 +506,136 @@ def test_closed_loop_with_generated_candidates_is_lossless(tiny):
         assert ids[0] == nxt
     ref = O.greedy_decode(m, kc0, vc0, L0, root, len(emitted), "f32")
     assert emitted == ref
+
+
+# ------------------------------------------------- ensemble prompt tokens (EPT)
+
+def test_ept_chains_realise_the_ensemble_mask():
+    """The EPT appendix's ensemble mask: an EPT of group g sees the input
+    tokens (here: the candidate path it hangs under) and the EPTs of group g
+    at smaller or equal positions, nothing else.  The ancestor mask of a
+    template with n_ept parallel chains per node is exactly that."""
+    from synth.trees import make_template
+    n_prompt, n_ept = 3, 3
+    tpl = make_template([(0,), (1,), (0, 0)], n_prompt, n_ept)
+    O.validate_template(tpl.parent, tpl.kind, n_prompt, n_ept)
+    depth, anc = O.build_mask(tpl.parent)
+    T = tpl.T
+    # owner candidate, group and token distance of every EPT node, from the
+    # template's kinds and the chain layout alone
+    owner, group, dist = {}, {}, {}
+    for i in range(1, T):
+        k = int(tpl.kind[i])
+        if k < 0:
+            j, g = divmod(-k - 1, n_ept)
+            group[i], dist[i] = g, j + 1
+            o = i
+            for _ in range(j + 1):
+                o = int(tpl.parent[o])
+            owner[i] = o
+
+    def cand_path(c):
+        out = {c}
+        while c > 0:
+            c = int(tpl.parent[c])
+            out.add(c)
+        return out
+
+    for v in range(T):
+        for u in range(T):
+            if v in group:
+                c = owner[v]
+                want = (u in cand_path(c)) or (u in group and owner[u] == c and group[u] == group[v]
+                                                and dist[u] <= dist[v])
+            else:
+                want = u in cand_path(v)
+            assert bool(anc[v, u]) == want, (v, u)
+        if v in group:
+            assert depth[v] == depth[owner[v]] + dist[v]   # position = the token it stands for
+
+
+def test_ept_mean_row_special_cases():
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal(50).astype(np.float32)
+    assert np.array_equal(O.ept_mean_row([x]), x)                      # one EPT: unchanged
+    assert np.array_equal(O.ept_mean_row([x, x]), x)                   # (x + x) / 2 is exact
+    a, b, c, d = (rng.integers(-1000, 1000, 50).astype(np.float32) for _ in range(4))
+    exact = (a.astype(np.float64) + b + c + d) / 4.0                   # small integers: exact sums
+    assert np.array_equal(O.ept_mean_row([a, b, c, d]).astype(np.float64), exact)
+    assert np.array_equal(O.ept_mean_row([d, c, b, a]), O.ept_mean_row([a, b, c, d]))
+    y = x.copy()
+    y[7] = np.nan
+    m = O.ept_mean_row([x, y])
+    assert np.isnan(m[7]) and not np.isnan(np.delete(m, 7)).any()
+
+
+def test_next_tree_ids_ept_handmade():
+    """Two EPT groups; the averaged row ranks differently from either group's
+    own row.  Accepted node 1 carries chains (3, 5) of group 0 and (4, 6) of
+    group 1 (prompt ids 0, 2 and 1, 3); template: ranks (0), (1), (0, 0) and
+    the two chains of length 2 under the root."""
+    V, n_ept = 4, 2
+    parent = [-1, 0, 0, 1, 1, 3, 4]
+    ids = [2, 1, 3, V + 0, V + 1, V + 2, V + 3]
+    logits = np.zeros((7, V), np.float32)
+    logits[3] = [4.0, 0.0, 1.0, 2.0]     # group 0, distance 1: order 0, 3, 2, 1
+    logits[4] = [-4.0, 2.0, 2.0, 0.0]    # group 1, distance 1: order 1, 2, 3, 0
+    # mean [0, 1, 1.5, 1]: order 2, 1, 3, 0
+    logits[5] = [1.0, 3.0, 0.0, 0.0]     # group 0, distance 2
+    logits[6] = [1.0, -3.0, 0.0, 5.0]    # group 1, distance 2; mean [1, 0, 0, 2.5]: order 3, 0, 1, 2
+    tpl_parent = [-1, 0, 0, 1, 0, 0, 4, 5]
+    tpl_kind = [0, 0, 1, 0, -1, -2, -3, -4]
+    O.validate_template(tpl_parent, tpl_kind, 2, n_ept)
+    out = O.next_tree_ids(parent, ids, V, [0, 1], 3, logits, tpl_parent, tpl_kind, n_ept)
+    assert out.tolist() == [3, 2, 1, 3, V + 0, V + 1, V + 2, V + 3]
+    # identical groups: the mean is each group's row, as with one EPT
+    logits[4], logits[6] = logits[3], logits[5]
+    out = O.next_tree_ids(parent, ids, V, [0, 1], 3, logits, tpl_parent, tpl_kind, n_ept)
+    one = O.next_tree_ids([-1, 0, 0, 1, 3], [2, 1, 3, V + 0, V + 1], V, [0, 1], 3,
+                          logits[[0, 1, 2, 3, 5]], [-1, 0, 0, 1, 0, 4], [0, 0, 1, 0, -1, -2])
+    assert out[:4].tolist() == one[:4].tolist()
+
+
+@pytest.mark.parametrize("tpl_parent,tpl_kind", [
+    ([-1, 0, 1], [0, -1, -4]),         # group 0 continued by group 1's distance-2 EPT
+    ([-1, 0, 1], [0, -2, -3]),         # group 1 continued by group 0's distance-2 EPT
+    ([-1, 0], [0, -7]),                # token distance 4 > 3
+    ([-1, 0, 0], [0, 0, -3]),          # distance-2 EPT directly under the root
+])
+def test_validate_template_rejects_ept(tpl_parent, tpl_kind):
+    O.validate_template([-1, 0, 1, 0, 3], [0, -1, -3, -2, -4], 3, 2)   # both groups, in order
+    with pytest.raises(ValueError):
+        O.validate_template(tpl_parent, tpl_kind, 3, 2)
+
+
+def test_closed_loop_with_ept_candidates_is_lossless(tiny):
+    """The guess-and-verify loop with two EPT groups per prompt token (each
+    token distance has two embeddings, guesses from the averaged logits)
+    still emits the vanilla greedy sequence."""
+    import dataclasses
+    from synth.trees import make_template
+    sh, W, m, kc0, vc0, L0, root = tiny
+    n_ept = 2
+    sh2 = dataclasses.replace(sh, n_prompt=sh.n_prompt * n_ept)
+    extra = np.random.default_rng(8).standard_normal((sh.n_prompt, sh.hidden)) * 0.02
+    W2 = dict(W)
+    W2["prompt_emb"] = np.vstack([O.to_f64(W["prompt_emb"]), extra])
+    m2 = O.Model(sh2, W2)
+    tpl = make_template([(0,), (1,), (2,), (0, 0), (0, 1), (1, 0), (0, 0, 0)], sh.n_prompt, n_ept)
+    O.validate_template(tpl.parent, tpl.kind, sh.n_prompt, n_ept)
+    kc, vc = O.copy_cache(kc0, vc0)
+    rng = np.random.default_rng(6)
+    ids = rng.integers(0, sh.vocab, tpl.T)
+    ids[0] = root
+    ids[tpl.kind < 0] = sh.vocab + (-tpl.kind[tpl.kind < 0] - 1)
+    L, emitted = L0, []
+    for s in range(5):
+        res = O.verify_forward(m2, kc, vc, L, ids, tpl.parent, "f32")
+        pred = O.argmax_first(res["logits"])
+        path, n_path, nxt = O.accept(tpl.parent, ids, pred, sh.vocab)
+        L = O.kv_compact(kc, vc, res["tree_k"], res["tree_v"], L, path)
+        emitted += [int(ids[j]) for j in path[1:]] + [nxt]
+        ids = O.next_tree_ids(tpl.parent, ids, sh.vocab, path, nxt,
+                              res["logits"].astype(np.float32), tpl.parent, tpl.kind, n_ept)
+    ref = O.greedy_decode(m, kc0, vc0, L0, root, len(emitted), "f32")
+    assert emitted == ref
