@@ -200,6 +200,35 @@ def main():
     ppd.ppd_set_kernel_timer("next_tree")
     del keep
 
+    # the same with two EPT groups per prompt token (Section 3.2): the
+    # 15-candidate template with two chains of 3 under every node (T = 112),
+    # used as this step's tree, Gaussian logits, accepted path root -> node 1
+    tpl2 = make_template(n_ept=2)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.seeds["tokens"])
+    logits2 = torch.randn((tpl2.T, sh.vocab), device=dev, generator=gen)
+    ids2 = np.where(tpl2.kind < 0, sh.vocab + (-tpl2.kind - 1), 1 + np.arange(tpl2.T)).astype(np.int32)
+    par2_d, ids2_d = todev(tpl2.parent.astype(np.int32)), todev(ids2)
+    path2 = torch.zeros(tpl2.T, dtype=torch.int32, device=dev)
+    path2[1] = 1
+    n_path2 = torch.tensor([2], dtype=torch.int32, device=dev)
+    nids2 = torch.empty(tpl2.T, dtype=torch.int32, device=dev)
+
+    def next_tree_ept():
+        ppd.ppd_next_tree(tpl2.T, par2_d, ids2_d, sh.vocab, sh.n_prompt, logits2, path2, n_path2,
+                          nxt, tpl2.parent, tpl2.kind, nids2, ws, n_ept=2)
+    for _ in range(3):
+        next_tree_ept()
+    torch.cuda.synchronize()
+    next_ept_us = 0.0
+    keep = ppd.ppd_set_kernel_timer("next_tree", [st], [sp])
+    for _ in range(args.steps):
+        next_tree_ept()
+        torch.cuda.synchronize()
+        next_ept_us += st.elapsed_time(sp) * 1e3 / args.steps
+    ppd.ppd_set_kernel_timer("next_tree")
+    del keep
+
     alg = step_bytes(sh, L, T, n_acc)
     flops = step_flops(sh, L, T)
     gu_us = kernels["gate_up"]
@@ -230,6 +259,7 @@ def main():
         "emitted_tokens_per_s": round(n_acc / (ms * 1e-3), 1),
         "kernel_us": {k2: round(v2, 2) for k2, v2 in kernels.items()},
         "next_tree_us": round(next_us, 2),
+        "next_tree_ept2_us": round(next_ept_us, 2),
         "device_status": status,
         "roofline": {"bound": "hbm", "kernel": "gate_up GEMM + SwiGLU",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

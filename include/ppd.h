@@ -233,12 +233,22 @@ ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
  *                            vocab + 0, that node's child with id vocab + 1,
  *                            ...; past the chain's end its deepest node, or
  *                            the accepted node itself when it has none);
- *   tpl_kind[i] = -1 - j     prompt token j (id vocab + j).
+ *   tpl_kind[i] = -1 - q     prompt embedding q (id vocab + q).
+ * Ensemble prompt tokens (Section 3.2, the EPT appendix): with n_ept EPTs per
+ * prompt token, prompt embedding q is the EPT of group q % n_ept at token
+ * distance q / n_ept + 1; a node carries one chain per group (group g: ids
+ * vocab + g, vocab + n_ept + g, ...), which under the ancestor mask is the
+ * ensemble mask, and the logits row behind a depth-d candidate is the mean of
+ * the groups' d-th chain nodes' rows (float32: added in group order, then
+ * divided by n_ept).  n_ept = 1 is the plain single chain (prompt id j at
+ * distance j + 1).
  * Ranks order larger logits first, equal logits by smaller index, NaN last
  * (a NaN among the selected ranks sets PPD_DEV_NAN_LOGIT).  One workgroup
  * per candidate depth reads one logits row.  The template's
  * parent/depth/mask are the caller's (ppd_build_tree_mask on tpl_parent).
  *   T, parent, ids    this step's tree (device int32[T])
+ *   n_prompt, n_ept   token distances per chain, EPT groups (1 <= n_ept <=
+ *                     PPD_EPT_MAX); prompt embeddings n_prompt * n_ept
  *   logits            device float32[T][vocab] written by ppd_verify_step
  *   path, n_path, next_tok   device, as written by ppd_accept (path holds
  *                     T entries, all read)
@@ -248,12 +258,14 @@ ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
  *   ws                the workspace (status word)
  * Template rules (else PPD_EINVAL, nothing enqueued): 1 <= tpl_T <= PPD_T_MAX;
  * a candidate's parent is the root or a candidate, rank < PPD_TOPK_MAX and <
- * vocab, depth <= 15; prompt token 0 hangs under the root or a candidate,
- * prompt token j > 0 under prompt token j - 1, j < n_prompt.
+ * vocab, depth <= 15; a distance-1 EPT hangs under the root or a candidate,
+ * a distance-(j+1) EPT of group g under the distance-j EPT of group g, and
+ * j < n_prompt.
  */
 #define PPD_TOPK_MAX 16
+#define PPD_EPT_MAX 64
 ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, int32_t vocab,
-                         int32_t n_prompt, const float *logits, const int32_t *path,
+                         int32_t n_prompt, int32_t n_ept, const float *logits, const int32_t *path,
                          const int32_t *n_path, const int32_t *next_tok, int32_t tpl_T,
                          const int32_t *tpl_parent, const int32_t *tpl_kind, int32_t *next_ids,
                          void *ws, size_t ws_bytes, void *stream);

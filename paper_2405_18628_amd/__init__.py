@@ -75,8 +75,8 @@ def lib() -> C.CDLL:
         L.ppd_device_status.argtypes = [vp, sz, P(C.c_uint32), i32, vp]
         L.ppd_set_kernel_timer.argtypes = [i32, vp, vp, i32]
         L.ppd_last_error.restype = C.c_char_p
-        L.ppd_next_tree.argtypes = [i32, vp, vp, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, vp, sz,
-                                    vp]
+        L.ppd_next_tree.argtypes = [i32, vp, vp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, vp,
+                                    sz, vp]
         L.ppd_packed_weight_bytes.argtypes = [i32, i32, i32]
         L.ppd_packed_weight_bytes.restype = sz
         L.ppd_pack_weight.argtypes = [i32, i32, i32, vp, vp, vp]
@@ -251,7 +251,7 @@ def ppd_accept(T: int, parent, ids, pred, vocab: int, path, n_path, next_tok, ws
 
 def ppd_next_tree(T: int, parent, ids, vocab: int, n_prompt: int, logits, path, n_path,
                   next_tok, tpl_parent: Sequence[int], tpl_kind: Sequence[int], next_ids, ws,
-                  stream=None):
+                  stream=None, n_ept: int = 1):
     """Token ids of the next step's tree (template tpl_parent / tpl_kind, host
     sequences) into the device tensor next_ids."""
     import torch
@@ -264,7 +264,7 @@ def ppd_next_tree(T: int, parent, ids, vocab: int, n_prompt: int, logits, path, 
     if tp.shape != tk.shape:
         raise ValueError("tpl_parent and tpl_kind differ in length")
     _check(lib().ppd_next_tree(int(T), _ptr(parent), _ptr(ids), int(vocab), int(n_prompt),
-                               _ptr(logits), _ptr(path), _ptr(n_path), _ptr(next_tok),
+                               int(n_ept), _ptr(logits), _ptr(path), _ptr(n_path), _ptr(next_tok),
                                int(tp.shape[0]), tp.ctypes.data, tk.ctypes.data, _ptr(next_ids),
                                _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 

@@ -25,6 +25,8 @@
 // the ranks do, so selection is integer max / compare without branches.
 // If the list would overflow, kd rounds of a workgroup-wide maximum over the
 // elements below the previous pick select the ranks instead.
+#include <type_traits>
+
 #include "ppd_internal.h"
 
 namespace {
@@ -88,11 +90,13 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
 
 // MULTI: the row spans several register chunks (reloaded in each pass);
 // VEC: rows are 16-byte aligned, read in float4 (a thread's elements are
-// then runs of 4)
-template <bool MULTI, bool VEC>
+// then runs of 4); EPT: several EPT groups, whose rows are averaged
+template <bool MULTI, bool VEC, bool EPT>
 __global__ __launch_bounds__(kThreads) void next_tree_kernel(NextTreeLaunch p) {
-  __shared__ int chain_s[PPD_NEXT_MAX_DEPTH + 1];
-  __shared__ int found_s, count_s, nan_s;
+  // per EPT group: the chain node reached so far (-2 - node once the chain
+  // has ended at that node), the next level's node, the logits row used
+  __shared__ int cur_s[PPD_EPT_MAX], find_s[PPD_EPT_MAX], src_s[PPD_EPT_MAX];
+  __shared__ int acc_s, count_s, nan_s;
   __shared__ uint64_t wave_s[kThreads / 64];
   __shared__ uint64_t list_s[kListCap];
   __shared__ int top_s[PPD_TOPK_MAX];
@@ -101,9 +105,10 @@ __global__ __launch_bounds__(kThreads) void next_tree_kernel(NextTreeLaunch p) {
   const int d = blockIdx.x + 1;  // candidate depth handled here
   const int kd = p.k_of_depth[d];
   const int V = p.vocab;
+  const int G = EPT ? p.n_ept : 1;
 
   // this step's tree and accepted path, one node per thread
-  int my_par = -2, my_id = -1, my_path = 0;
+  int my_par = INT_MIN, my_id = -1, my_path = 0;
   if (tid < p.T) {
     my_par = p.parent[tid];
     my_id = p.ids[tid];
@@ -122,46 +127,55 @@ __global__ __launch_bounds__(kThreads) void next_tree_kernel(NextTreeLaunch p) {
   }
   if (kd == 0) return;  // no candidate at this depth
 
-  // ---- the accepted node and its prompt chain, up to depth d
+  // ---- the accepted node and its prompt chains (one per EPT group), up to
+  // depth d; a chain stops at its first missing level
   if (tid == 0) {
-    found_s = min(max(*p.n_path, 1), p.T) - 1;  // the accepted node's place on the path
+    acc_s = min(max(*p.n_path, 1), p.T) - 1;  // the accepted node's place on the path
     nan_s = 0;
     count_s = 0;
   }
   __syncthreads();
-  if (tid == found_s) chain_s[0] = min(max(my_path, 0), p.T - 1);
-  __syncthreads();
-  int src = chain_s[0];
+  if (tid == acc_s)
+    for (int g = 0; g < G; ++g) cur_s[g] = min(max(my_path, 0), p.T - 1);
   for (int j = 0; j < d; ++j) {
-    const int cur = chain_s[j];
-    if (tid == 0) found_s = INT_MAX;
+    if (tid < G) find_s[tid] = INT_MAX;
     __syncthreads();
-    if (my_par == cur && my_id == V + j) atomicMin(&found_s, tid);
+    const int g = my_id - V - j * G;  // my node's group if it is a level-j EPT
+    if (g >= 0 && g < G && my_par == cur_s[g]) atomicMin(&find_s[g], tid);
     __syncthreads();
-    const int f = found_s;
-    if (f == INT_MAX) break;  // uniform: the chain ends here
-    if (tid == 0) chain_s[j + 1] = f;
-    src = f;
-    __syncthreads();
+    bool any = false;
+    for (int q = 0; q < G; ++q) any |= find_s[q] != INT_MAX;
+    if (!any) break;  // uniform: every chain ends here
+    if (tid < G) {
+      const int c = cur_s[tid];
+      if (c >= 0) cur_s[tid] = find_s[tid] != INT_MAX ? find_s[tid] : -2 - c;
+    }
+    __syncthreads();  // find_s is reset next
   }
+  __syncthreads();
+  if (tid < G) {
+    const int c = cur_s[tid];
+    src_s[tid] = c >= 0 ? c : -2 - c;
+  }
+  __syncthreads();
 
-  // ---- 1. the row in registers (as value words), each thread's best
-  const float *row = p.logits + (size_t)src * V;
+  // ---- 1. the row in registers (as value words), each thread's best; with
+  // EPT groups the row is their mean: added in group order, then divided
   const int n_chunks = MULTI ? (V + kChunk - 1) / kChunk : 1;
   // row index of this thread's element e of chunk c (grows with e)
   auto eidx = [&](int c, int e) {
     return VEC ? c * kChunk + 4 * ((e >> 2) * kThreads + tid) + (e & 3)
                : c * kChunk + e * kThreads + tid;
   };
-  uint32_t h[kPer];
-  auto load = [&](int c) {
-    float x[kPer];
+  // elements [E0, E0 + N) of this thread's chunk c of a row into x
+  auto load_part = [&](auto e0_tag, auto n_tag, const float *row, int c, float *x) {
+    constexpr int E0 = decltype(e0_tag)::value, N = decltype(n_tag)::value;
     if (VEC) {
       const float4 *row4 = (const float4 *)row;
       const int V4 = V >> 2;
 #pragma unroll
-      for (int j = 0; j < kPer / 4; ++j) {
-        const float4 v = row4[min(c * (kChunk / 4) + j * kThreads + tid, V4 - 1)];
+      for (int j = 0; j < N / 4; ++j) {
+        const float4 v = row4[min(c * (kChunk / 4) + (E0 / 4 + j) * kThreads + tid, V4 - 1)];
         x[4 * j] = v.x;
         x[4 * j + 1] = v.y;
         x[4 * j + 2] = v.z;
@@ -169,9 +183,33 @@ __global__ __launch_bounds__(kThreads) void next_tree_kernel(NextTreeLaunch p) {
       }
     } else {
 #pragma unroll
-      for (int e = 0; e < kPer; ++e) x[e] = row[min(eidx(c, e), V - 1)];
+      for (int e = 0; e < N; ++e) x[e] = row[min(eidx(c, E0 + e), V - 1)];
     }
     __builtin_amdgcn_sched_barrier(0);  // all loads in flight before the first use
+  };
+  using Z = std::integral_constant<int, 0>;
+  using Half = std::integral_constant<int, kPer / 2>;
+  using Full = std::integral_constant<int, kPer>;
+  uint32_t h[kPer];
+  auto load = [&](int c) {
+    float x[kPer];
+    // row bases are wave-uniform: scalar base + 32-bit lane offsets
+    load_part(Z(), Full(), p.logits + (size_t)__builtin_amdgcn_readfirstlane(src_s[0]) * V, c, x);
+    if (EPT) {
+      for (int g = 1; g < G; ++g) {
+        const float *row = p.logits + (size_t)__builtin_amdgcn_readfirstlane(src_s[g]) * V;
+        float y[kPer / 2];  // half a chunk at a time keeps the registers in bounds
+        load_part(Z(), Half(), row, c, y);
+#pragma unroll
+        for (int e = 0; e < kPer / 2; ++e) x[e] += y[e];
+        load_part(Half(), Half(), row, c, y);
+#pragma unroll
+        for (int e = 0; e < kPer / 2; ++e) x[kPer / 2 + e] += y[e];
+      }
+      const float n = (float)G;
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) x[e] = x[e] / n;
+    }
 #pragma unroll
     for (int e = 0; e < kPer; ++e) h[e] = value_word(x[e]);
   };
@@ -284,8 +322,14 @@ __global__ __launch_bounds__(kThreads) void next_tree_kernel(NextTreeLaunch p) {
 hipError_t launch_next_tree(const NextTreeLaunch &p, int n_depths, hipStream_t s) {
   const dim3 grid(max(1, n_depths)), block(kThreads);
   const bool vec = p.vocab % 4 == 0 && (uintptr_t)p.logits % 16 == 0;
-  auto kernel = p.vocab > kChunk ? (vec ? next_tree_kernel<true, true> : next_tree_kernel<true, false>)
-                                 : (vec ? next_tree_kernel<false, true> : next_tree_kernel<false, false>);
+  const bool multi = p.vocab > kChunk, ept = p.n_ept > 1;
+  void (*kernel)(NextTreeLaunch);
+  if (ept)
+    kernel = multi ? (vec ? next_tree_kernel<true, true, true> : next_tree_kernel<true, false, true>)
+                   : (vec ? next_tree_kernel<false, true, true> : next_tree_kernel<false, false, true>);
+  else
+    kernel = multi ? (vec ? next_tree_kernel<true, true, false> : next_tree_kernel<true, false, false>)
+                   : (vec ? next_tree_kernel<false, true, false> : next_tree_kernel<false, false, false>);
   if (p.ev_start)
     hipExtLaunchKernelGGL(kernel, grid, block, 0, s, (hipEvent_t)p.ev_start,
                           (hipEvent_t)p.ev_stop, 0, p);

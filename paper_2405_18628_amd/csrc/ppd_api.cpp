@@ -504,7 +504,7 @@ ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
 }
 
 ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, int32_t vocab,
-                         int32_t n_prompt, const float *logits, const int32_t *path,
+                         int32_t n_prompt, int32_t n_ept, const float *logits, const int32_t *path,
                          const int32_t *n_path, const int32_t *next_tok, int32_t tpl_T,
                          const int32_t *tpl_parent, const int32_t *tpl_kind, int32_t *next_ids,
                          void *ws, size_t ws_bytes, void *stream) {
@@ -512,6 +512,8 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
   if (tpl_T < 1 || tpl_T > PPD_T_MAX)
     return fail(PPD_EINVAL, "template size %d outside [1, %d]", tpl_T, PPD_T_MAX);
   if (vocab < 1 || n_prompt < 0) return fail(PPD_EINVAL, "vocab must be positive, n_prompt >= 0");
+  if (n_ept < 1 || n_ept > PPD_EPT_MAX || (int64_t)n_prompt * n_ept > 32767)
+    return fail(PPD_EINVAL, "n_ept=%d outside [1, %d] or too many prompt ids", n_ept, PPD_EPT_MAX);
   if (!parent || !ids || !logits || !path || !n_path || !next_tok || !tpl_parent || !tpl_kind ||
       !next_ids)
     return fail(PPD_EINVAL, "NULL argument");
@@ -521,6 +523,7 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
   p.ids = ids;
   p.T = T;
   p.vocab = vocab;
+  p.n_ept = n_ept;
   p.logits = logits;
   p.path = path;
   p.n_path = n_path;
@@ -529,7 +532,7 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
   p.status = (uint32_t *)ws;
   p.tpl_T = tpl_T;
   // the template: topological, candidates under the root or candidates,
-  // prompt chains in prompt-id order under candidates
+  // one prompt chain per EPT group under candidates, in token-distance order
   if (tpl_parent[0] != -1) return fail(PPD_EINVAL, "template: tpl_parent[0] must be -1");
   int n_depths = 0;
   for (int i = 0; i < tpl_T; ++i) {
@@ -549,11 +552,12 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
         p.k_of_depth[depth] = std::max(p.k_of_depth[depth], kind + 1);
         n_depths = std::max(n_depths, depth);
       } else {
-        const int j = -kind - 1;
-        if (j >= n_prompt || j > 32766)
-          return fail(PPD_EINVAL, "template: prompt id %d >= n_prompt", j);
-        if (j == 0 ? pk < 0 : pk != -j)
-          return fail(PPD_EINVAL, "template: prompt token %d of node %d out of chain order", j, i);
+        const int q = -kind - 1;  // prompt embedding: token distance j + 1, EPT group g
+        const int j = q / n_ept, g = q % n_ept;
+        if (kind < -32767 || j >= n_prompt)
+          return fail(PPD_EINVAL, "template: prompt id %d beyond %d token distances", q, n_prompt);
+        if (j == 0 ? pk < 0 : pk != -1 - ((j - 1) * n_ept + g))
+          return fail(PPD_EINVAL, "template: prompt token %d of node %d out of chain order", q, i);
       }
     }
     if (depth > 127) return fail(PPD_EINVAL, "template too deep");

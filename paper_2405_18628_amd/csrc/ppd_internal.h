@@ -164,6 +164,7 @@ hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s);
 struct NextTreeLaunch {
   const int32_t *parent, *ids;  // this step's tree
   int T, vocab;
+  int n_ept;                    // EPT groups per prompt token (1: plain chains)
   const float *logits;          // [T][vocab]
   const int32_t *path, *n_path, *next_tok;
   int32_t *next_ids;            // [tpl_T]

@@ -151,10 +151,10 @@ def test_next_tree_rejects_before_enqueue():
     L = ppd.lib()
     f = 0x4000
 
-    def call(tp, tk, T=8, vocab=100, n_prompt=3, ws=f, wsb=64, logits=f):
+    def call(tp, tk, T=8, vocab=100, n_prompt=3, ws=f, wsb=64, logits=f, n_ept=1):
         tp = np.asarray(tp, np.int32)
         tk = np.asarray(tk, np.int32)
-        return L.ppd_next_tree(T, f, f, vocab, n_prompt, logits, f, f, f, len(tp),
+        return L.ppd_next_tree(T, f, f, vocab, n_prompt, n_ept, logits, f, f, f, len(tp),
                                tp.ctypes.data, tk.ctypes.data, f, ws, wsb, None)
     assert call([0, 0], [0, 0]) == ppd.PPD_EINVAL                  # root not -1
     assert call([-1, 1], [0, 0]) == ppd.PPD_EINVAL                 # not topological
@@ -171,3 +171,10 @@ def test_next_tree_rejects_before_enqueue():
     assert call([-1, 0], [0, 0], logits=None) == ppd.PPD_EINVAL
     assert call(list(range(-1, 128)), [0] * 129) == ppd.PPD_EINVAL  # template > PPD_T_MAX
     assert "template" in ppd.ppd_last_error()
+    # ensemble prompt tokens: group g's chain continues with group g only
+    assert call([-1, 0], [0, 0], n_ept=0) == ppd.PPD_EINVAL
+    assert call([-1, 0], [0, 0], n_ept=65) == ppd.PPD_EINVAL       # > PPD_EPT_MAX
+    assert call([-1, 0, 1], [0, -1, -4], n_ept=2) == ppd.PPD_EINVAL  # group 0 then group 1
+    assert call([-1, 0, 1], [0, -2, -3], n_ept=2) == ppd.PPD_EINVAL  # group 1 then group 0
+    assert call([-1, 0], [0, -7], n_ept=2) == ppd.PPD_EINVAL         # token distance 4 > 3
+    assert call([-1, 0, 0], [0, 0, -3], n_ept=2) == ppd.PPD_EINVAL   # distance 2 under the root
