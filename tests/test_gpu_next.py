@@ -10,7 +10,7 @@ import torch
 
 import oracle as O
 import paper_2405_18628_amd as ppd
-from gpu_cases import make_case, say, tree_tensors, workspace
+from gpu_cases import check_logits, gpu_step, make_case, oracle_step, say, tree_tensors, workspace
 from synth import workload
 from synth.trees import RANK_PATHS_15, Tree, make_template, make_tree
 
@@ -270,3 +270,29 @@ def test_closed_loop_with_ept_on_device_is_lossless():
     assert emitted == ref
     case.k.copy_(k0)
     case.v.copy_(v0)
+
+
+def test_verify_logits_on_ept_tree():
+    """The verification forward on a tree with two EPT groups per prompt
+    token (a candidate's chains side by side, six prompt embeddings): every
+    node's logits, prompt nodes included, match the oracle at fp32 tolerance."""
+    import dataclasses
+    case = make_case(workload("tiny"))
+    sh = case.shape
+    n_ept = 2
+    sh2 = dataclasses.replace(sh, n_prompt=sh.n_prompt * n_ept)
+    W2 = dict(case.W)
+    gen = torch.Generator().manual_seed(10)
+    extra = (torch.randn(sh.n_prompt, sh.hidden, generator=gen) * 0.02).to(
+        W2["prompt_emb"].dtype).cuda()
+    W2["prompt_emb"] = torch.cat([case.W["prompt_emb"], extra]).contiguous()
+    case2 = dataclasses.replace(case, shape=sh2, W=W2, model=ppd.Model(sh2, W2),
+                                oracle_model=O.Model(sh2, W2))
+    rng = np.random.default_rng(12)
+    tree = _ept_tree([(0,), (1,), (2,), (0, 0), (0, 1), (1, 0), (0, 0, 0)], sh.vocab, sh.n_prompt,
+                     n_ept, rng, full=True)
+    ws = workspace(case2, tree.T)
+    say(f"[ept-verify] T={tree.T}")
+    gpu = gpu_step(case2, tree, ws)
+    ref = oracle_step(case2, tree)
+    check_logits(gpu["logits"], ref["logits"], sh.dtype)
