@@ -566,3 +566,76 @@ def next_tree_ids(parent: Sequence[int], ids: Sequence[int], vocab: int, path: S
             order_of[srcs] = rank_order(row)
         out[i] = int(order_of[srcs][k])
     return out
+
+
+# ----------------------------------------------------------------------------
+# tree sizing (Section 4.2, hardware-aware tree size; Proposition 1 of the
+# tree-construction appendix)
+#
+# Proposition 1: with an acceptance probability per tree position, the
+# expected number of accepted candidates of a tree is the sum over its
+# candidates of the product of the probabilities along the candidate's root
+# path.  Here a candidate at depth d with rank r (the r-th best guess at that
+# distance) is accepted, given its parent is, with probability p[d - 1][r],
+# independently of other depths.  The tree of n candidates that maximises
+# that sum takes the n rank paths of largest product (every product is at
+# most its prefix's, so those paths contain their prefixes).  The hardware-
+# aware size is then the n that maximises tokens per step over forward
+# latency, Speedup(n) = tau(n) / L_fp(n), with tau(n) = 1 + the expected
+# accepted candidates (the bonus token always comes).
+
+
+def prop1_expected_accepted(tpl_parent: Sequence[int], tpl_kind: Sequence[int],
+                            p_table) -> float:
+    """Proposition 1's sum for a template: candidates (kind >= 0) at depth d,
+    rank r contribute the product of p[depth - 1][rank] along their path."""
+    depth = template_depths(tpl_parent)
+    val = {0: 1.0}
+    total = 0.0
+    for i in range(1, len(tpl_parent)):
+        k = int(tpl_kind[i])
+        if k < 0:
+            continue
+        val[i] = val[int(tpl_parent[i])] * float(p_table[int(depth[i]) - 1][k])
+        total += val[i]
+    return total
+
+
+def best_candidate_paths(p_table, n_cand: int) -> List[Tuple[int, ...]]:
+    """The n_cand rank paths (depth <= len(p_table), ranks < len(p_table[0]))
+    of largest product, in order: larger product first, then shallower, then
+    the lexicographically smaller path.  Found by listing every path."""
+    import itertools
+    D, K = len(p_table), len(p_table[0])
+    scored = []
+    for d in range(1, D + 1):
+        for path in itertools.product(range(K), repeat=d):
+            v = 1.0
+            for j, r in enumerate(path):
+                v *= float(p_table[j][r])
+            scored.append((-v, d, path))
+    scored.sort()
+    return [s[2] for s in scored[:n_cand]]
+
+
+def sparse_template(p_table, n_cand: int, n_prompt: int, n_ept: int = 1):
+    """Template of the best n_cand candidates: root, the candidates in the
+    order of best_candidate_paths, then under the root and every candidate,
+    in node order, one chain of n_prompt prompt tokens per EPT group.
+    Returns (tpl_parent, tpl_kind, expected accepted candidates)."""
+    paths = best_candidate_paths(p_table, n_cand)
+    parent, kind = [-1], [0]
+    node_of = {(): 0}
+    for path in paths:
+        parent.append(node_of[path[:-1]])
+        kind.append(path[-1])
+        node_of[path] = len(parent) - 1
+    for c in range(len(parent)):
+        for g in range(n_ept):
+            prev = c
+            for j in range(n_prompt):
+                parent.append(prev)
+                kind.append(-1 - ept_prompt_id(j, g, n_ept))
+                prev = len(parent) - 1
+    return (np.asarray(parent, np.int64), np.asarray(kind, np.int64),
+            prop1_expected_accepted(parent, kind, p_table))

@@ -183,3 +183,28 @@ def template_tree(tpl: Template, ids) -> Tree:
     """The tree of a template with the given token ids."""
     n_cand = int(np.sum(tpl.kind[1:] >= 0)) + 1
     return Tree(tpl.parent.copy(), np.asarray(ids, np.int32), n_cand)
+
+
+# Synthetic acceptance table for tree sizing: p[d][r] = probability that the
+# true token at token distance d + 1 is the rank-r guess there.  Anchored on
+# the paper's prediction accuracies with one EPT (EPT appendix, accuracy
+# table: distance 1 top-1 0.472, top-5 0.771; distance 2 top-1 0.248, top-5
+# 0.576).  Within a distance, ranks 1-4 share top-5 minus top-1 geometrically
+# (ratio 0.6) and ranks 5-15 continue the same geometric tail; each further
+# distance is the previous row scaled by the distance-2 / distance-1 top-1
+# ratio.  Synthetic: no dataset is used.
+PAPER_TOP1 = (0.472, 0.248)
+PAPER_TOP5 = (0.771, 0.576)
+
+
+def synthetic_accept_table(depth: int = 3, k: int = 16, ratio: float = 0.6):
+    w = sum(ratio ** i for i in range(4))
+    table = []
+    for d in range(depth):
+        if d < len(PAPER_TOP1):
+            a = (PAPER_TOP5[d] - PAPER_TOP1[d]) / w
+            row = [PAPER_TOP1[d]] + [a * ratio ** i for i in range(k - 1)]
+        else:
+            row = [x * PAPER_TOP1[1] / PAPER_TOP1[0] for x in table[-1]]
+        table.append(row)
+    return np.asarray(table, np.float64)

@@ -639,3 +639,66 @@ def test_closed_loop_with_ept_candidates_is_lossless(tiny):
                               res["logits"].astype(np.float32), tpl.parent, tpl.kind, n_ept)
     ref = O.greedy_decode(m, kc0, vc0, L0, root, len(emitted), "f32")
     assert emitted == ref
+
+
+# ------------------------------------------------------------- tree sizing
+
+def test_best_candidate_paths_is_optimal():
+    """The rank paths of largest product maximise Proposition 1's sum over all
+    candidate trees of that size (exhaustive search over prefix-closed sets of
+    paths, depth <= 2, ranks < 3)."""
+    import itertools
+    rng = np.random.default_rng(41)
+    for trial in range(6):
+        p = rng.random((2, 3))
+        paths = [(a,) for a in range(3)] + [(a, b) for a in range(3) for b in range(3)]
+        val = {q: float(np.prod([p[j][r] for j, r in enumerate(q)])) for q in paths}
+        for n in range(1, 6):
+            best = 0.0
+            for sub in itertools.combinations(paths, n):
+                s = set(sub)
+                if all(len(q) == 1 or q[:-1] in s for q in sub):
+                    best = max(best, sum(val[q] for q in sub))
+            got = O.best_candidate_paths(p, n)
+            assert len(got) == n and all(len(q) == 1 or q[:-1] in set(got) for q in got)
+            assert abs(sum(val[q] for q in got) - best) < 1e-12
+
+
+def test_proposition1_on_sparse_template_monte_carlo():
+    """Proposition 1 for a built template: draw the true token's rank at each
+    distance independently from the table (or no match), verify with the
+    oracle's exact-match acceptance, and average the accepted candidates."""
+    from synth.trees import synthetic_accept_table
+    p = synthetic_accept_table(3, 4)
+    tp, tk, f = O.sparse_template(p, 9, 2)
+    O.validate_template(tp, tk, 2)
+    assert abs(O.prop1_expected_accepted(tp, tk, p) - f) < 1e-15
+    K = p.shape[1]
+    V = K + 1                      # token = rank; K = a token no candidate holds
+    depth = O.template_depths(tp)
+    ids = np.where(tk >= 0, tk, V + (-tk - 1))
+    ids[0] = 0
+    rng = np.random.default_rng(42)
+    n, acc = 20000, 0
+    for _ in range(n):
+        r = [int(rng.choice(K + 1, p=np.append(p[d], 1 - p[d].sum()))) for d in range(3)]
+        pred = np.array([r[int(depth[u])] if depth[u] < 3 else K for u in range(len(tp))])
+        _, n_path, _ = O.accept(tp, ids, pred, V)
+        acc += n_path - 1
+    mc = acc / n
+    se = math.sqrt(f * 3 / n) + 1e-3
+    assert abs(mc - f) < 4 * se, (mc, f)
+
+
+def test_sparse_template_layout():
+    from synth.trees import synthetic_accept_table
+    p = synthetic_accept_table()
+    for n, n_prompt, n_ept in ((0, 3, 1), (15, 3, 1), (7, 3, 2), (20, 2, 1)):
+        tp, tk, f = O.sparse_template(p, n, n_prompt, n_ept)
+        O.validate_template(tp, tk, n_prompt, n_ept)
+        assert len(tp) == 1 + n + (1 + n) * n_prompt * n_ept
+        assert int(np.sum(tk[1:] >= 0)) == n
+        assert O.template_depths(tp)[tk >= 0].max() <= p.shape[0]
+    # more candidates never lower the expected accepted length
+    fs = [O.sparse_template(p, n, 3)[2] for n in range(0, 32)]
+    assert all(b >= a for a, b in zip(fs, fs[1:]))
