@@ -1,12 +1,20 @@
 """Benchmark of the PPD tree-verification step on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload 7b] [--T 64] [--graph]
+    python bench.py --sweep [--workload 13b]     # hardware-aware tree size
 
 A step is one pass of the whole hot path on one synthetic batch:
 ppd_verify_step (forward over the T tree nodes, fp32 logits, greedy tokens)
 -> ppd_accept -> ppd_kv_compact, enqueued on one stream.  The cache length L is
 the same every step (the compaction writes past L, the next step overwrites).
 Inputs are resident in HBM before timing starts.  Prints one JSON line.
+
+--sweep measures the forward latency L_fp(T) of the sparse trees that
+ppd_sparse_template builds for 0..31 candidates (3 prompt tokens under every
+node: T = 4, 8, .., 128) and of vanilla decoding (T = 1), and prints one JSON
+line per size and one with the size that maximises
+Speedup = tau(T) / L_fp(T) against vanilla (Section 4.2), tau(T) = 1 + the
+expected accepted candidates under the synthetic acceptance table.
 
 The default workload is the Vicuna-7B-shaped decoder (32 layers, hidden 4096,
 32 heads x 128, ffn 11008, vocab 32000, bf16, random weights) with a
@@ -66,6 +74,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=4,
                     help="decoder layers in the CPU oracle's timed sample")
+    ap.add_argument("--sweep", action="store_true",
+                    help="tree-size sweep: L_fp(T) of the best sparse trees and the speedup")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -115,6 +125,9 @@ def main():
                                    todev(mask.view(np.int64)))
     model = ppd.Model(sh, W)
     kv = ppd.KVCache(k, v)
+    if args.sweep:
+        tree_size_sweep(args, ppd, wl, sh, model, kv, L, cap, dev)
+        return
     ws = torch.empty(ppd.ppd_workspace_bytes(model, T, cap), dtype=torch.uint8, device=dev)
     ppd.ppd_workspace_init(ws)
     logits = torch.empty((T, sh.vocab), device=dev)
@@ -270,6 +283,81 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(sh, W, k, v, L, tree, args.cpu_layers)
     print(json.dumps(out), flush=True)
+
+
+def tree_size_sweep(args, ppd, wl, sh, model, kv, L, cap, dev):
+    """Section 4.2's hardware-aware tree size on this GPU: L_fp(T) measured
+    for the best sparse tree of each candidate count, tau(T) from
+    Proposition 1 on the synthetic acceptance table, and the size with the
+    largest tau(T) * L_fp(1) / L_fp(T)."""
+    import numpy as np
+    import torch
+    from synth.trees import synthetic_accept_table
+
+    p_table = synthetic_accept_table()
+    rng = np.random.default_rng(wl.seeds["tree"])
+    n_prompt = 3
+    sizes = [(None, 1)] + [(n, 4 * (n + 1)) for n in range(0, 32)]
+    ws = torch.empty(ppd.ppd_workspace_bytes(model, 128, cap), dtype=torch.uint8, device=dev)
+    ppd.ppd_workspace_init(ws)
+    logits = torch.empty((128, sh.vocab), device=dev)
+    pred = torch.empty(128, dtype=torch.int32, device=dev)
+    path = torch.empty(128, dtype=torch.int32, device=dev)
+    n_path = torch.empty(1, dtype=torch.int32, device=dev)
+    nxt = torch.empty(1, dtype=torch.int32, device=dev)
+    todev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    rows, base = [], None
+    for n_cand, T in sizes:
+        if n_cand is None:                       # vanilla decoding: the root alone
+            tp, tk, f = np.array([-1], np.int32), np.array([0], np.int32), 0.0
+        else:
+            tp, tk, f = ppd.ppd_sparse_template(p_table, n_cand, n_prompt)
+        assert len(tp) == T
+        ids = np.where(tk < 0, sh.vocab + (-tk - 1), rng.integers(0, sh.vocab, T)).astype(np.int32)
+        depth, mask = ppd.ppd_build_tree_mask(tp)
+        ids_d, par_d, dep_d, mask_d = todev(ids), todev(tp.astype(np.int32)), todev(depth), \
+            todev(mask.view(np.int64))
+        lg = logits[:T]
+
+        def fwd():
+            ppd.ppd_verify_step(model, kv, L, T, ids_d, dep_d, mask_d, ws, lg, pred)
+
+        def step():
+            fwd()
+            ppd.ppd_accept(T, par_d, ids_d, pred, sh.vocab, path, n_path, nxt, ws)
+            ppd.ppd_kv_compact(model, kv, L, path, n_path)
+
+        res = {}
+        for name, fn in (("forward", fwd), ("step", step)):
+            for _ in range(args.warmup):
+                fn()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+            torch.cuda.synchronize()
+            ev[0].record()
+            for i in range(args.steps):
+                fn()
+                ev[i + 1].record()
+            torch.cuda.synchronize()
+            us = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(args.steps)])
+            res[name] = (float(np.median(us)), float(np.percentile(us, 10)),
+                         float(np.percentile(us, 90)))
+        tau = 1.0 + f
+        if base is None:
+            base = res["forward"][0]
+        row = {"sweep": sh.name, "cache_len": L, "tree_tokens": T,
+               "candidates": 0 if n_cand is None else n_cand,
+               "forward_us": [round(x, 1) for x in res["forward"]],
+               "step_us": [round(x, 1) for x in res["step"]],
+               "tau": round(tau, 4),
+               "speedup_vs_vanilla": round(tau * base / res["forward"][0], 4),
+               "step_hbm_gbs": round(step_bytes(sh, L, T, 1) / (res["step"][0] * 1e-6) / 1e9, 1)}
+        rows.append(row)
+        print(json.dumps(row), flush=True)
+    best = max(rows, key=lambda r: r["speedup_vs_vanilla"])
+    print(json.dumps({"sweep": sh.name, "cache_len": L, "best_tree_tokens": best["tree_tokens"],
+                      "best_candidates": best["candidates"], "best_speedup": best["speedup_vs_vanilla"],
+                      "tau": best["tau"], "note": "forward_us / step_us are [median, p10, p90] over "
+                      f"{args.steps} steps; tau from the synthetic acceptance table"}), flush=True)
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_gemm_7b_hbm_traffic.md")

@@ -271,6 +271,32 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
                          void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * Tree sizing (Section 4.2, the hardware-aware tree size; Proposition 1 of
+ * the tree-construction appendix).  Host only: enqueues nothing.
+ * Builds the template (for ppd_next_tree) of the n_cand candidates that
+ * maximise the expected number of accepted candidates when the rank-r guess
+ * at depth d is accepted, given its parent is, with probability
+ * p_table[(d - 1) * k_max + r], independently (Proposition 1: the sum over
+ * candidates of the product of the probabilities along their root paths).
+ * The best tree holds the n_cand rank paths of largest product (ties:
+ * shallower, then lexicographically smaller rank path); its layout is the
+ * root, the candidates in that order, then under the root and every
+ * candidate, in node order, one chain of n_prompt prompt tokens per EPT group
+ * (kinds as in ppd_next_tree).  The caller picks n_cand by measuring the
+ * forward latency of the resulting T (Speedup = (1 + expected) / latency).
+ *   p_table           host double[depth_max][k_max], entries in [0, 1]
+ *   depth_max, k_max  1..15, 1..PPD_TOPK_MAX
+ *   tpl_parent, tpl_kind   host int32[PPD_T_MAX] (outputs), tpl_T their length
+ *   expected_accepted host double (output, may be NULL): Proposition 1's sum
+ * PPD_EINVAL if T = 1 + n_cand + (1 + n_cand) n_prompt n_ept > PPD_T_MAX, the
+ * table holds fewer than n_cand rank paths, or an argument is out of range.
+ */
+ppd_status ppd_sparse_template(const double *p_table, int32_t depth_max, int32_t k_max,
+                               int32_t n_cand, int32_t n_prompt, int32_t n_ept,
+                               int32_t *tpl_parent, int32_t *tpl_kind, int32_t *tpl_T,
+                               double *expected_accepted);
+
+/*
  * Profiling aid, not needed for correctness.  While set, every
  * ppd_verify_step issued from this thread launches the i-th kernel of kind
  * `kind` in the step (i < n_events) with start_events[i] / stop_events[i]

@@ -77,10 +77,12 @@ def lib() -> C.CDLL:
         L.ppd_last_error.restype = C.c_char_p
         L.ppd_next_tree.argtypes = [i32, vp, vp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp, vp,
                                     sz, vp]
+        L.ppd_sparse_template.argtypes = [vp, i32, i32, i32, i32, i32, vp, vp, P(C.c_int32),
+                                          P(C.c_double)]
         L.ppd_packed_weight_bytes.argtypes = [i32, i32, i32]
         L.ppd_packed_weight_bytes.restype = sz
         L.ppd_pack_weight.argtypes = [i32, i32, i32, vp, vp, vp]
-        for f in ("ppd_next_tree", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
+        for f in ("ppd_next_tree", "ppd_sparse_template", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
                   "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -269,6 +271,23 @@ def ppd_next_tree(T: int, parent, ids, vocab: int, n_prompt: int, logits, path, 
                                _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def ppd_sparse_template(p_table, n_cand: int, n_prompt: int, n_ept: int = 1):
+    """Template of the n_cand candidates that maximise Proposition 1's expected
+    accepted length under the host table p_table[depth - 1][rank].  Returns
+    (tpl_parent, tpl_kind, expected accepted candidates)."""
+    p = np.ascontiguousarray(np.asarray(p_table, dtype=np.float64))
+    if p.ndim != 2:
+        raise ValueError("p_table must be 2-D [depth][rank]")
+    par = np.zeros(PPD_T_MAX, np.int32)
+    kind = np.zeros(PPD_T_MAX, np.int32)
+    T = C.c_int32(0)
+    f = C.c_double(0.0)
+    _check(lib().ppd_sparse_template(p.ctypes.data, p.shape[0], p.shape[1], int(n_cand),
+                                     int(n_prompt), int(n_ept), par.ctypes.data, kind.ctypes.data,
+                                     C.byref(T), C.byref(f)))
+    return par[:T.value].copy(), kind[:T.value].copy(), float(f.value)
+
+
 def ppd_kv_compact(model: Model, kv: KVCache, L: int, path, n_path, stream=None):
     _check(lib().ppd_kv_compact(C.byref(model.desc), C.byref(kv.desc), int(L), _ptr(path),
                                 _ptr(n_path), _stream(stream)))
@@ -303,6 +322,6 @@ def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):
     return st, sp
 
 
-__all__ = ["ppd_next_tree", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
+__all__ = ["ppd_next_tree", "ppd_sparse_template", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
            "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept", "ppd_kv_compact",
            "ppd_device_status", "ppd_last_error"]

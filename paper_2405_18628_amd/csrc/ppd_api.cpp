@@ -49,6 +49,21 @@ ppd_status fail(ppd_status s, const char *fmt, ...) {
   return s;
 }
 
+}  // namespace
+
+// the same for the library's other translation units
+ppd_status ppd_fail(ppd_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+namespace {
+
 #define PPD_TRY_HIP(call)                                                               \
   do {                                                                                  \
     hipError_t e_ = (call);                                                             \

@@ -177,6 +177,9 @@ struct NextTreeLaunch {
 };
 hipError_t launch_next_tree(const NextTreeLaunch &p, int n_depths, hipStream_t s);
 
+// records the thread's error message (ppd_last_error) and returns s
+ppd_status ppd_fail(ppd_status s, const char *fmt, ...);
+
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
                         int T, int vocab, int n_prompt, int H, const void *gain, float *x,
                         void *xg, float *ss, uint32_t *status, hipStream_t s);

@@ -178,3 +178,38 @@ def test_next_tree_rejects_before_enqueue():
     assert call([-1, 0, 1], [0, -2, -3], n_ept=2) == ppd.PPD_EINVAL  # group 1 then group 0
     assert call([-1, 0], [0, -7], n_ept=2) == ppd.PPD_EINVAL         # token distance 4 > 3
     assert call([-1, 0, 0], [0, 0, -3], n_ept=2) == ppd.PPD_EINVAL   # distance 2 under the root
+
+
+@pytest.mark.parametrize("depth_max,k_max,n_cand,n_prompt,n_ept,seed", [
+    (3, 16, 15, 3, 1, 0), (3, 16, 31, 3, 1, 1), (3, 16, 0, 3, 1, 2), (2, 3, 12, 2, 1, 3),
+    (4, 5, 20, 3, 1, 4), (3, 16, 7, 3, 2, 5), (1, 16, 16, 3, 1, 6), (3, 16, 24, 3, 1, 7),
+])
+def test_sparse_template_matches_oracle(depth_max, k_max, n_cand, n_prompt, n_ept, seed):
+    """The host tree-sizing builder against the oracle's listing of every
+    rank path: the same template, bit-exact, and the same Proposition-1
+    value.  Tables: the synthetic one, random ones, and rows with ties."""
+    from synth.trees import synthetic_accept_table
+    rng = np.random.default_rng(seed)
+    if seed == 0 or seed == 1 or seed == 2:
+        p = synthetic_accept_table(depth_max, k_max)
+    elif seed == 7:
+        p = np.round(rng.random((depth_max, k_max)) * 4) / 4   # many equal products
+    else:
+        p = rng.random((depth_max, k_max))
+    tp, tk, f = ppd.ppd_sparse_template(p, n_cand, n_prompt, n_ept)
+    rp, rk, rf = O.sparse_template(p, n_cand, n_prompt, n_ept)
+    assert tp.tolist() == rp.tolist() and tk.tolist() == rk.tolist()
+    assert f == rf
+
+
+def test_sparse_template_rejects():
+    p = np.full((3, 16), 0.1)
+    for bad in (dict(p_table=np.full((3, 16), 1.5)), dict(p_table=np.full((3, 16), np.nan)),
+                dict(p_table=np.full((16, 4), 0.1)), dict(p_table=np.full((3, 17), 0.1)),
+                dict(n_cand=32), dict(n_cand=-1), dict(n_ept=0),
+                dict(p_table=np.full((1, 2), 0.5), n_cand=3, n_prompt=1)):
+        args = dict(p_table=p, n_cand=10, n_prompt=3, n_ept=1)
+        args.update(bad)
+        with pytest.raises(ppd.PPDError):
+            ppd.ppd_sparse_template(args["p_table"], args["n_cand"], args["n_prompt"],
+                                    args["n_ept"])
