@@ -69,6 +69,7 @@ typedef enum {
 typedef enum { PPD_F32 = 0, PPD_BF16 = 1 } ppd_dtype;
 
 #define PPD_T_MAX 128
+#define PPD_CAPACITY_MAX (1 << 24) /* KV positions per head */
 #define PPD_MASK_WORDS 2
 
 /* device status bits (ppd_device_status) */
@@ -152,7 +153,7 @@ ppd_status ppd_pack_weight(int32_t kind, int32_t rows, int32_t cols, const void 
  */
 typedef struct {
   void *k, *v;
-  int32_t capacity;
+  int32_t capacity;   /* positions per head, 1 .. PPD_CAPACITY_MAX */
   int32_t *len_dev;
 } ppd_kv;
 

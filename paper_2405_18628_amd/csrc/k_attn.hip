@@ -127,18 +127,22 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
   // column c % 16; V^T chunk c is dim row c / 8, keys 8 (c % 8) .. + 7 of the
   // pair.  Key rows past the cache capacity are clamped into it (such keys
   // are never visible, and their values are cleared when staged).  Past the
-  // split the last pair is re-read, so every iteration issues the same loads.
+  // split every lane reads the head's first 16 bytes (offsets masked to 0:
+  // one line per load), so every iteration issues the same loads.
   const int b_last = nb > 0 ? b1 - 1 : 0;
   u32x4 kr[RING][2], vr[RING][2];
   auto request = [&](int st, u32x4(&kd)[2], u32x4(&vd)[2]) {
     const int kp0 = min(b0 + 2 * st, b_last) * 32;
+    // opaque to the compiler, so that it issues the same loads on every path
+    int keep = __builtin_amdgcn_readfirstlane(st < nsteps ? -1 : 0);
+    asm volatile("" : "+s"(keep));
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int c = tid + 512 * i;
       const int key = min(kp0 + (c >> 4), p.cap - 1);
-      kd[i] = __builtin_nontemporal_load((const u32x4 *)(kbase + (size_t)key * 128 + (c & 15) * 8));
+      kd[i] = __builtin_nontemporal_load((const u32x4 *)(kbase + ((key * 128 + (c & 15) * 8) & keep)));
       const int g0 = min(kp0 + (c & 7) * 8, p.cap - 8);
-      vd[i] = __builtin_nontemporal_load((const u32x4 *)(vbase + (size_t)(c >> 3) * p.cap + g0));
+      vd[i] = __builtin_nontemporal_load((const u32x4 *)(vbase + (((c >> 3) * p.cap + g0) & keep)));
     }
   };
   // LDS destinations of this thread's chunks: block parity and byte offset
@@ -411,11 +415,37 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
 
 }  // namespace
 
+// ring depth (block pairs requested ahead) for a split of n pairs: the loop
+// runs whole trips of RING pairs, so the depth leaving the fewest idle steps
+// in a full split, the deepest among those
+int ring_for(int n_pairs, int max_ring) {
+  int best = 1, idle_best = 1 << 30;
+  for (int r = 1; r <= max_ring; ++r) {
+    const int idle = (n_pairs + r - 1) / r * r - n_pairs;
+    if (idle <= idle_best) {
+      idle_best = idle;
+      best = r;
+    }
+  }
+  return best;
+}
+
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
   const dim3 grid(a.nh * a.splits), block(512), mblock(256);
   hipEvent_t ev0 = (hipEvent_t)a.ev_start, ev1 = (hipEvent_t)a.ev_stop;
   hipEvent_t main_stop = a.splits > 1 ? nullptr : ev1;
-  auto kernel = a.MT > 4 ? attn_bf16_kernel<2, 2> : attn_bf16_kernel<1, 4>;
+  const int n_pairs = (a.chunk + 1) / 2;
+  void (*kernel)(AttnLaunch);
+  if (a.MT > 4) {
+    static void (*const k2[])(AttnLaunch) = {attn_bf16_kernel<2, 1>, attn_bf16_kernel<2, 2>,
+                                             attn_bf16_kernel<2, 3>};
+    kernel = k2[ring_for(n_pairs, 3) - 1];
+  } else {
+    static void (*const k1[])(AttnLaunch) = {attn_bf16_kernel<1, 1>, attn_bf16_kernel<1, 2>,
+                                             attn_bf16_kernel<1, 3>, attn_bf16_kernel<1, 4>,
+                                             attn_bf16_kernel<1, 5>, attn_bf16_kernel<1, 6>};
+    kernel = k1[ring_for(n_pairs, 6) - 1];
+  }
   if (ev0)
     hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev0, main_stop, 0, a);
   else

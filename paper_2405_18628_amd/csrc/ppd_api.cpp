@@ -212,6 +212,8 @@ ppd_status check_kv(const ppd_model *m, const ppd_kv *kv) {
   if (kv->capacity < 1) return fail(PPD_EINVAL, "kv capacity must be positive");
   if (m->dtype == PPD_BF16 && kv->capacity % 8)
     return fail(PPD_EUNSUPPORTED, "bf16 caches need capacity %% 8 == 0");
+  if (kv->capacity > PPD_CAPACITY_MAX)  // per-head offsets are 32-bit in the kernels
+    return fail(PPD_EUNSUPPORTED, "capacity %d > %d", kv->capacity, PPD_CAPACITY_MAX);
   return PPD_OK;
 }
 
