@@ -69,6 +69,7 @@ typedef enum {
 typedef enum { PPD_F32 = 0, PPD_BF16 = 1 } ppd_dtype;
 
 #define PPD_T_MAX 128
+#define PPD_BATCH_MAX 16  /* sequences in one ppd_verify_batch call */
 #define PPD_CAPACITY_MAX (1 << 24) /* KV positions per head */
 #define PPD_MASK_WORDS 2
 
@@ -192,6 +193,29 @@ ppd_status ppd_verify_step(const ppd_model *model, const ppd_kv *kv, int32_t L, 
                            const int32_t *ids, const int32_t *depth, const uint64_t *mask,
                            void *ws, size_t ws_bytes, float *logits, int32_t *pred,
                            void *stream);
+
+/*
+ * Several sequences in one step, sharing the weight stream (batch > 1; the
+ * paper's batch-size experiment, Section "Effect of Batch Size on
+ * Speedup"): sequence s has its own cache kvs[s], cached length L[s] and
+ * tree of T[s] nodes, and the sequences are independent -- each sequence's
+ * logits, greedy tokens and cache rows are those ppd_verify_step gives for
+ * it alone.  The trees are packed in sequence order: sequence s owns rows
+ * [t0_s, t0_s + T[s]) of ids, depth, mask, logits and pred, t0_s = T[0] + ..
+ * + T[s - 1]; its depth and mask rows refer to its own tree (node indices
+ * local to the sequence, as ppd_build_tree_mask gives them).
+ *   B          1 .. PPD_BATCH_MAX sequences; T[0] + .. + T[B - 1] <= PPD_T_MAX
+ *   kvs        host array of B cache descriptors (all of the model's dtype)
+ *   L, T       host int32[B]
+ *   ws         as for ppd_verify_step with t_max = the total token count
+ * B > 1 needs a bf16 model (PPD_EUNSUPPORTED otherwise).  Acceptance and
+ * compaction stay per sequence: ppd_accept(T[s], parent + t0_s, ids + t0_s,
+ * pred + t0_s, ...) and ppd_kv_compact(model, &kvs[s], L[s], ...).
+ */
+ppd_status ppd_verify_batch(const ppd_model *model, int32_t B, const ppd_kv *kvs,
+                            const int32_t *L, const int32_t *T, const int32_t *ids,
+                            const int32_t *depth, const uint64_t *mask, void *ws, size_t ws_bytes,
+                            float *logits, int32_t *pred, void *stream);
 
 /*
  * Exact-matching verification and acceptance (Section 3).  Node i > 0 is

@@ -70,6 +70,8 @@ def lib() -> C.CDLL:
         L.ppd_build_tree_mask.argtypes = [i32, vp, vp, vp]
         L.ppd_verify_step.argtypes = [P(ppd_model), P(ppd_kv), i32, i32, vp, vp, vp, vp, sz, vp,
                                       vp, vp]
+        L.ppd_verify_batch.argtypes = [P(ppd_model), i32, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp,
+                                       vp]
         L.ppd_accept.argtypes = [i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
         L.ppd_kv_compact.argtypes = [P(ppd_model), P(ppd_kv), i32, vp, vp, vp]
         L.ppd_device_status.argtypes = [vp, sz, P(C.c_uint32), i32, vp]
@@ -82,7 +84,7 @@ def lib() -> C.CDLL:
         L.ppd_packed_weight_bytes.argtypes = [i32, i32, i32]
         L.ppd_packed_weight_bytes.restype = sz
         L.ppd_pack_weight.argtypes = [i32, i32, i32, vp, vp, vp]
-        for f in ("ppd_next_tree", "ppd_sparse_template", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
+        for f in ("ppd_next_tree", "ppd_sparse_template", "ppd_verify_batch", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
                   "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -241,6 +243,28 @@ def ppd_verify_step(model: Model, kv: KVCache, L: int, T: int, ids, depth, mask,
                                  _ptr(pred), _stream(stream)))
 
 
+def ppd_verify_batch(model: Model, kvs: Sequence[KVCache], L: Sequence[int], T: Sequence[int],
+                     ids, depth, mask, ws, logits, pred, stream=None):
+    """One step over len(kvs) sequences whose trees are packed in sequence
+    order (device ids / depth / mask / logits / pred rows)."""
+    import torch
+    for t, n in ((ids, "ids"), (depth, "depth"), (pred, "pred")):
+        _dev(t, torch.int32, n)
+    _dev(mask, None, "mask")
+    _dev(ws, None, "ws")
+    _dev(logits, torch.float32, "logits")
+    B = len(kvs)
+    if len(L) != B or len(T) != B:
+        raise ValueError("kvs, L and T differ in length")
+    descs = (ppd_kv * max(B, 1))(*[kv.desc for kv in kvs])
+    Ls = np.ascontiguousarray(np.asarray(L, dtype=np.int32))
+    Ts = np.ascontiguousarray(np.asarray(T, dtype=np.int32))
+    _check(lib().ppd_verify_batch(C.byref(model.desc), B, C.cast(descs, C.c_void_p),
+                                  Ls.ctypes.data, Ts.ctypes.data, _ptr(ids), _ptr(depth),
+                                  _ptr(mask), _ptr(ws), ws.numel() * ws.element_size(),
+                                  _ptr(logits) or None, _ptr(pred), _stream(stream)))
+
+
 def ppd_accept(T: int, parent, ids, pred, vocab: int, path, n_path, next_tok, ws, stream=None):
     import torch
     for t, n in ((parent, "parent"), (ids, "ids"), (pred, "pred"), (path, "path"),
@@ -322,6 +346,6 @@ def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):
     return st, sp
 
 
-__all__ = ["ppd_next_tree", "ppd_sparse_template", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
+__all__ = ["ppd_verify_batch", "ppd_next_tree", "ppd_sparse_template", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
            "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept", "ppd_kv_compact",
            "ppd_device_status", "ppd_last_error"]

@@ -9,8 +9,9 @@
 // Work decomposition.  The step is bound by reading the keys and values, and
 // a compute unit's load path sustains only ~35 GB/s, so the kernel reads
 // each key/value block once per compute unit and spreads the blocks over all
-// CUs: a workgroup owns one head h and one of KS contiguous key splits, and
-// all T queries.  The four waves load each block cooperatively (16-byte
+// CUs: a workgroup owns one sequence (a batched step packs several, each
+// with its own cache and tree), one head h and one of KS contiguous key
+// splits, and all of that sequence's T queries.  The four waves load each block cooperatively (16-byte
 // non-temporal loads into a register ring up to 8 blocks ahead), stage
 // it in a double-buffered LDS slot, and each wave multiplies it with its own
 // 16-query tiles (tiles w and w + 4), keeping one online softmax per query.
@@ -32,6 +33,8 @@
 // (rescaling only when a block's maximum exceeds it by more than 2^8); P
 // enters the PV product as the sum of two bf16 parts (hi, lo), i.e. to about
 // 16 significant bits.
+#include <algorithm>
+
 #include "ppd_internal.h"
 
 namespace {
@@ -91,25 +94,31 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qw = wave & 3, par = wave >> 2;
   const int lr = lane & 15, lg = lane >> 4;
-  const int KS = p.splits;
-  const int h = blockIdx.x / KS, ks = blockIdx.x % KS;
+  // this workgroup's sequence (uniform), head and key split
+  int sq = 0;
+  for (int j = 1; j < p.sb.B; ++j) sq = (int)blockIdx.x >= p.wg0[j] ? j : sq;
+  const int KS = p.splits[sq];
+  const int wl = blockIdx.x - p.wg0[sq];
+  const int h = wl / KS, ks = wl % KS;
   const int kvh = h / (p.nh / p.nkv);
-  const int n_keys = p.L + p.T;
+  const int t0 = p.sb.t0[sq], T = p.sb.t0[sq + 1] - t0, L = p.sb.L[sq], cap = p.sb.cap[sq];
+  const int n_keys = L + T;
   const int nblk = (n_keys + 31) >> 5;
-  const int b0 = min(nblk, ks * p.chunk), b1 = min(nblk, b0 + p.chunk);
+  const int b0 = min(nblk, ks * p.chunk[sq]), b1 = min(nblk, b0 + p.chunk[sq]);
   const int nb = b1 - b0;
   const int nsteps = (nb + 1) >> 1;  // block pairs
-  const bf16_t *kbase = p.kc + (size_t)kvh * p.cap * 128;
-  const bf16_t *vbase = p.vc + (size_t)kvh * 128 * p.cap;
+  const bf16_t *kbase = p.sb.k[sq] + (size_t)kvh * cap * 128;
+  const bf16_t *vbase = p.sb.v[sq] + (size_t)kvh * 128 * cap;
   const u32x4 *zp = (const u32x4 *)p.zeros;
 
-  // ---- this wave's query tiles that exist
-  const int n_live = min(NQ, (p.MT - qw + 3) / 4);
+  // ---- this wave's query tiles that exist (tokens t0 + tile 16 + lr)
+  const int n_live = min(NQ, ((T + 15) / 16 - qw + 3) / 4);
   QTile qt[NQ];
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
-    const int tq = (qw + 4 * i) * 16 + lr;
-    const bool qlive = tq < p.T;
+    const int tl = (qw + 4 * i) * 16 + lr;
+    const int tq = t0 + tl;
+    const bool qlive = tl < T;
 #pragma unroll
     for (int ds = 0; ds < 4; ++ds)
       qt[i].qf[ds] = *(qlive ? (const u32x4 *)(p.q + ((size_t)tq * p.nh + h) * 128 + ds * 32 + lg * 8) : zp);
@@ -139,10 +148,10 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int c = tid + 512 * i;
-      const int key = min(kp0 + (c >> 4), p.cap - 1);
+      const int key = min(kp0 + (c >> 4), cap - 1);
       kd[i] = __builtin_nontemporal_load((const u32x4 *)(kbase + ((key * 128 + (c & 15) * 8) & keep)));
-      const int g0 = min(kp0 + (c & 7) * 8, p.cap - 8);
-      vd[i] = __builtin_nontemporal_load((const u32x4 *)(vbase + (((c >> 3) * p.cap + g0) & keep)));
+      const int g0 = min(kp0 + (c & 7) * 8, cap - 8);
+      vd[i] = __builtin_nontemporal_load((const u32x4 *)(vbase + (((c >> 3) * cap + g0) & keep)));
     }
   };
   // LDS destinations of this thread's chunks: block parity and byte offset
@@ -221,12 +230,12 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 4; ++e) sv[kt * 4 + e] = s[kt][e];
-    if (key0 + 32 > p.L) {
+    if (key0 + 32 > L) {
       // this lane's 8 keys key0 + 8 lg .. + 7 (bit u = key j0 + u): visible
       // if in the cached prefix, or a tree key (j - L < T) whose bit j - L of
       // the ancestor mask is set; blocks wholly in the prefix skip this
       const int j0 = key0 + lg * 8;
-      const int sh = j0 - p.L;  // ancestor-mask bit of key j0
+      const int sh = j0 - L;  // ancestor-mask bit of key j0
       const uint32_t pre = (1u << min(8, max(0, -sh))) - 1u;
       const uint32_t valid = (1u << min(8, max(0, n_keys - j0))) - 1u;
       uint64_t win;  // mask bits sh .. sh + 7 in its low byte (0 below bit 0)
@@ -344,39 +353,39 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
     for (int dt = 0; dt < 8; ++dt) o[dt] = Q.o[dt] * s0 + *(const floatx4 *)(mrow + dt * 16 + lg * 4) * s1;
     l = l * s0 + ml1.y * s1;
     const int tile = qw + 4 * qi;
-    if (KS == 1) {
-      const int t = tile * 16 + lr;
-      if (t < p.T) {
+    const int tl = tile * 16 + lr;  // query within the sequence
+    if (tl < T) {
+      const size_t t = (size_t)t0 + tl;
+      if (KS == 1) {
         const float inv = 1.f / l;
-        bf16_t *dst = p.out + (size_t)t * p.nh * 128 + h * 128 + lg * 4;
+        bf16_t *dst = p.out + t * p.nh * 128 + h * 128 + lg * 4;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
           const floatx4 v = o[dt] * inv;
           *(u32x2 *)(dst + dt * 16) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
         }
-      }
-    } else {
-      float *row = p.part + (((size_t)h * KS + ks) * p.MT + tile) * 16 * OROW + lr * OROW;
+      } else {
+        float *row = p.part + (((size_t)h * p.max_splits + ks) * p.T_pad + t) * OROW;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) *(floatx4 *)(row + dt * 16 + lg * 4) = o[dt];
-      if (lg == 0) *(float2 *)(row + 128) = float2{M, l};
+        for (int dt = 0; dt < 8; ++dt) *(floatx4 *)(row + dt * 16 + lg * 4) = o[dt];
+        if (lg == 0) *(float2 *)(row + 128) = float2{M, l};
+      }
     }
   }
 }
 
-// ---- merge of the KS splits: workgroup (head h, query tile qt, 32-dim
-// quarter dq); thread -> query tq = tid / 16, dims 32 dq + 2 (tid % 16) and
-// + 1.  The splits' rows are read 8 at a time (one round trip per batch) and
-// added in split order, scaled to the running maximum.
+// ---- merge of the KS splits: workgroup (sequence s and head h, query tile
+// qt, 32-dim quarter dq); thread -> query tq = tid / 16, dims 32 dq + 2 (tid
+// % 16) and + 1.  The splits' rows are read 8 at a time (one round trip per
+// batch) and added in split order, scaled to the running maximum.
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
-  const int h = blockIdx.x, qt = blockIdx.y, dq = blockIdx.z;
+  const int sq = blockIdx.x / p.nh, h = blockIdx.x % p.nh, qt = blockIdx.y, dq = blockIdx.z;
   const int tq = threadIdx.x >> 4, d2 = dq * 32 + (threadIdx.x & 15) * 2;
-  const int t = qt * 16 + tq;
-  if (t >= p.T) return;
-  const int KS = p.splits;
-  auto row_of = [&](int s) {
-    return p.part + (((size_t)h * KS + s) * p.MT + qt) * 16 * OROW + tq * OROW;
-  };
+  const int KS = p.splits[sq];
+  const int tl = qt * 16 + tq;
+  if (KS == 1 || tl >= p.sb.t0[sq + 1] - p.sb.t0[sq]) return;  // one split: already final
+  const size_t t = (size_t)p.sb.t0[sq] + tl;
+  auto row_of = [&](int s) { return p.part + (((size_t)h * p.max_splits + s) * p.T_pad + t) * OROW; };
   constexpr int B = 8;
   float M = -INFINITY, lsum = 0.f;
   float2 acc = float2{0.f, 0.f};
@@ -410,7 +419,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
     }
   }
   const float inv = 1.f / lsum;
-  *(uint32_t *)(p.out + (size_t)t * p.nh * 128 + h * 128 + d2) = pack_bf16x2(acc.x * inv, acc.y * inv);
+  *(uint32_t *)(p.out + t * p.nh * 128 + h * 128 + d2) = pack_bf16x2(acc.x * inv, acc.y * inv);
 }
 
 }  // namespace
@@ -431,10 +440,14 @@ int ring_for(int n_pairs, int max_ring) {
 }
 
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
-  const dim3 grid(a.nh * a.splits), block(512), mblock(256);
+  const dim3 grid(a.wg0[a.sb.B]), block(512), mblock(256);
   hipEvent_t ev0 = (hipEvent_t)a.ev_start, ev1 = (hipEvent_t)a.ev_stop;
-  hipEvent_t main_stop = a.splits > 1 ? nullptr : ev1;
-  const int n_pairs = (a.chunk + 1) / 2;
+  int n_pairs = 1, max_ks = 1;  // over the sequences: the ring serves the longest split
+  for (int j = 0; j < a.sb.B; ++j) {
+    n_pairs = std::max(n_pairs, (a.chunk[j] + 1) / 2);
+    max_ks = std::max(max_ks, a.splits[j]);
+  }
+  hipEvent_t main_stop = max_ks > 1 ? nullptr : ev1;
   void (*kernel)(AttnLaunch);
   if (a.MT > 4) {
     static void (*const k2[])(AttnLaunch) = {attn_bf16_kernel<2, 1>, attn_bf16_kernel<2, 2>,
@@ -451,8 +464,8 @@ hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
   else
     hipLaunchKernelGGL(kernel, grid, block, 0, s, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.splits == 1) return e;
-  const dim3 mgrid(a.nh, a.MT, 4);
+  if (e != hipSuccess || max_ks == 1) return e;
+  const dim3 mgrid(a.nh * a.sb.B, a.MT, 4);
   if (ev1)
     hipExtLaunchKernelGGL(attn_merge_kernel, mgrid, mblock, 0, s, nullptr, ev1, 0, a);
   else

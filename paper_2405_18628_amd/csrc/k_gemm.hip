@@ -67,19 +67,20 @@ __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
 // ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) of tokens
 // tok0 .. tok0 + NT - 1 from the producer's sum-of-squares partials
-// ss[p][T_pad]: group j of the J = 256 / NT thread groups sums partials j,
-// j + J, ... in order (the first 16 per thread requested by rs_request, so
-// that a caller can overlap their latency), then the group sums are added in
-// group order.
+// ss[p][T_pad]: two threads per token, thread j adding partials j, j + 2,
+// j + 4, ... in order (the first 16 requested by rs_request, so that a caller
+// can overlap their latency), then the two sums are added.  The order is the
+// same whatever NT, so a token's scale does not depend on the other tokens
+// of the step (a batched step gives each sequence its own step's bits).
 template <int NT>
 __device__ __forceinline__ void rs_request(const GemmLaunch &g, int tok0, float (&ssv)[16]) {
-  constexpr int J = 256 / NT;
+  static_assert(2 * NT <= 256, "two threads per token");
   const int tid = threadIdx.x, t = tid % NT, j = tid / NT;
   const int T_pad = g.MT * 16;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const int pp = j + i * J;
-    const bool use = tid < J * NT && pp < g.n_ss;
+    const int pp = j + 2 * i;
+    const bool use = tid < 2 * NT && pp < g.n_ss;
     const float v = g.ss[(size_t)(use ? pp : 0) * T_pad + tok0 + t];  // always a valid row
     ssv[i] = use ? v : 0.f;
   }
@@ -88,23 +89,18 @@ __device__ __forceinline__ void rs_request(const GemmLaunch &g, int tok0, float 
 template <int NT>
 __device__ __forceinline__ void rs_finish(const GemmLaunch &g, int tok0, const float (&ssv)[16],
                                           float *gs, float *rs_s) {
-  constexpr int J = 256 / NT;
   const int tid = threadIdx.x;
   const int T_pad = g.MT * 16;
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) s += ssv[i];
-  if (tid < J * NT) {
+  if (tid < 2 * NT) {
     const int t = tid % NT, j = tid / NT;
-    for (int pp = j + 16 * J; pp < g.n_ss; pp += J) s += g.ss[(size_t)pp * T_pad + tok0 + t];
+    for (int pp = j + 32; pp < g.n_ss; pp += 2) s += g.ss[(size_t)pp * T_pad + tok0 + t];
     gs[tid] = s;
   }
   __syncthreads();
-  if (tid < NT) {
-    float v = 0.f;
-    for (int j = 0; j < J; ++j) v += gs[j * NT + tid];
-    rs_s[tok0 + tid] = rsqrtf(v * g.inv_h + g.eps);
-  }
+  if (tid < NT) rs_s[tok0 + tid] = rsqrtf((gs[tid] + gs[NT + tid]) * g.inv_h + g.eps);
 }
 
 // ---- epilogue operands
@@ -160,6 +156,16 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
     for (int mt = 0; mt < MTE; ++mt) {
       const int tk = (mt0 + mt) * 16 + lr;
       if (tk >= T) continue;
+      // this token's sequence: its cache and the position L + local index
+      bf16_t *kc = g.sb.k[0], *vc = g.sb.v[0];
+      int cap = g.sb.cap[0], pos = g.sb.L[0] + tk;
+      for (int j = 1; j < g.sb.B; ++j)
+        if (tk >= g.sb.t0[j]) {
+          kc = g.sb.k[j];
+          vc = g.sb.v[j];
+          cap = g.sb.cap[j];
+          pos = g.sb.L[j] + tk - g.sb.t0[j];
+        }
       const float rs = rs_s[tk];
       float lo[4], hi[4];
 #pragma unroll
@@ -180,15 +186,15 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
         const u32x2 plo = u32x2{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
         const u32x2 phi = u32x2{pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
         bf16_t *dst = hp < nh ? g.q + ((size_t)tk * nh + hp) * 128
-                              : g.kc + ((size_t)(hp - nh) * g.cap + g.L + tk) * 128;
+                              : kc + ((size_t)(hp - nh) * cap + pos) * 128;
         *(u32x2 *)(dst + i0) = plo;
         *(u32x2 *)(dst + i0 + 64) = phi;
       } else {
-        bf16_t *vb = g.vc + (size_t)(hp - nh - nkv) * 128 * g.cap + g.L + tk;
+        bf16_t *vb = vc + (size_t)(hp - nh - nkv) * 128 * cap + pos;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          vb[(size_t)(i0 + e) * g.cap] = f32_to_bf16(lo[e]);
-          vb[(size_t)(i0 + e + 64) * g.cap] = f32_to_bf16(hi[e]);
+          vb[(size_t)(i0 + e) * cap] = f32_to_bf16(lo[e]);
+          vb[(size_t)(i0 + e + 64) * cap] = f32_to_bf16(hi[e]);
         }
       }
     }

@@ -79,10 +79,13 @@ hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, 
 // angle of frequency i is pos * base^(-2i/d), evaluated in double precision
 // and rounded to float.  Padding rows get position 0.
 
-__global__ void rope_table_kernel(const int32_t *__restrict__ depth, int T, int L, int d,
+__global__ void rope_table_kernel(const int32_t *__restrict__ depth, SeqBatch sb, int d,
                                   float base, float2 *__restrict__ rope) {
   const int t = blockIdx.x;
   const int half = d / 2;
+  int L = sb.L[0];  // the cached length of token t's sequence
+  for (int j = 1; j < sb.B; ++j) L = t >= sb.t0[j] ? sb.L[j] : L;
+  const int T = sb.t0[sb.B];
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     double pos = t < T ? (double)L + (double)depth[t] : 0.0;
     double inv = exp(-(2.0 * i / d) * log((double)base));
@@ -92,10 +95,10 @@ __global__ void rope_table_kernel(const int32_t *__restrict__ depth, int T, int 
   }
 }
 
-hipError_t launch_rope_table(const int32_t *depth, int T, int L, int d, float base, float2 *rope,
-                             hipStream_t s) {
-  int T_pad = (T + 15) & ~15;
-  hipLaunchKernelGGL(rope_table_kernel, dim3(T_pad), dim3(64), 0, s, depth, T, L, d, base, rope);
+hipError_t launch_rope_table(const int32_t *depth, const SeqBatch &sb, int d, float base,
+                             float2 *rope, hipStream_t s) {
+  int T_pad = (sb.t0[sb.B] + 15) & ~15;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(T_pad), dim3(64), 0, s, depth, sb, d, base, rope);
   return hipGetLastError();
 }
 

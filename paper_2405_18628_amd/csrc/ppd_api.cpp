@@ -217,12 +217,33 @@ ppd_status check_kv(const ppd_model *m, const ppd_kv *kv) {
   return PPD_OK;
 }
 
-ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const int32_t *ids,
-                     const int32_t *depth, const uint64_t *mask, void *ws, const WsLayout &w,
-                     float *logits, int32_t *pred, hipStream_t s) {
+// the sequences of a step, with this layer's cache slices
+SeqBatch seq_batch(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t *Ls,
+                   const int32_t *Ts, int layer) {
+  SeqBatch sb{};
+  sb.B = B;
+  for (int j = 0; j < B; ++j) {
+    sb.t0[j + 1] = sb.t0[j] + Ts[j];
+    sb.L[j] = Ls[j];
+    sb.cap[j] = kvs[j].capacity;
+    const size_t per_layer = (size_t)m->n_kv_heads * kvs[j].capacity * m->head_dim;
+    sb.k[j] = (bf16_t *)kvs[j].k + (size_t)layer * per_layer;
+    sb.v[j] = (bf16_t *)kvs[j].v + (size_t)layer * per_layer;
+  }
+  return sb;
+}
+
+ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t *Ls,
+                     const int32_t *Ts, const int32_t *ids, const int32_t *depth,
+                     const uint64_t *mask, void *ws, const WsLayout &w, float *logits,
+                     int32_t *pred, hipStream_t s) {
   const int H = m->hidden, nh = m->n_heads, nkv = m->n_kv_heads;
+  int T = 0, MT_seq = 1;
+  for (int j = 0; j < B; ++j) {
+    T += Ts[j];
+    MT_seq = std::max(MT_seq, (Ts[j] + 15) / 16);
+  }
   const int Tp = t_pad_of(T), MT = Tp / 16;
-  const int cap = kv->capacity;
   uint32_t *status = at<uint32_t>(ws, w.status);
   float *x = at<float>(ws, w.x);
   bf16_t *xg = at<bf16_t>(ws, w.xg);
@@ -246,17 +267,21 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     g.split = sh.split;
   };
 
-  PPD_TRY_HIP(launch_rope_table(depth, T, L, m->head_dim, m->rope_base, rope, s));
+  PPD_TRY_HIP(launch_rope_table(depth, seq_batch(m, B, kvs, Ls, Ts, 0), m->head_dim,
+                                m->rope_base, rope, s));
   PPD_TRY_HIP(launch_embed(PPD_BF16, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
                            m->attn_norm[0], x, xg, ss, status, s));
   int n_ss = 1;
-  int splits, chunk;
-  attn_splits(m, L, T, &splits, &chunk);
+  // attention work per sequence: nh x splits workgroups
+  int splits[PPD_BATCH_MAX], chunk[PPD_BATCH_MAX], wg0[PPD_BATCH_MAX + 1] = {0};
+  for (int j = 0; j < B; ++j) {
+    attn_splits(m, Ls[j], Ts[j], &splits[j], &chunk[j]);
+    wg0[j + 1] = wg0[j] + nh * splits[j];
+  }
   const float inv_h = 1.0f / (float)H;
 
   for (int l = 0; l < m->n_layers; ++l) {
-    bf16_t *kc = (bf16_t *)kv->k + (size_t)l * nkv * cap * 128;
-    bf16_t *vc = (bf16_t *)kv->v + (size_t)l * nkv * 128 * cap;
+    const SeqBatch sb = seq_batch(m, B, kvs, Ls, Ts, l);
     GemmLaunch g{};
     g.T = T;
     g.MT = MT;
@@ -273,31 +298,29 @@ ppd_status step_bf16(const ppd_model *m, const ppd_kv *kv, int L, int T, const i
     g.n_ss = n_ss;
     g.rope = rope;
     g.q = q;
-    g.kc = kc;
-    g.vc = vc;
     g.nh = nh;
     g.nkv = nkv;
-    g.cap = cap;
-    g.L = L;
+    g.sb = sb;
     timer_events(TK_QKV, &g.ev_start, &g.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(g, s));
     // tree attention
     AttnLaunch a{};
     a.q = q;
-    a.kc = kc;
-    a.vc = vc;
     a.mask = mask;
     a.out = attn_o;
     a.part = at<float>(ws, w.attn_part);
     a.zeros = g.zeros;
-    a.T = T;
-    a.MT = MT;
-    a.L = L;
-    a.cap = cap;
+    a.T_pad = Tp;
     a.nh = nh;
     a.nkv = nkv;
-    a.splits = splits;
-    a.chunk = chunk;
+    a.max_splits = w.max_splits;
+    a.MT = MT_seq;
+    a.sb = sb;
+    for (int j = 0; j < B; ++j) {
+      a.splits[j] = splits[j];
+      a.chunk[j] = chunk[j];
+    }
+    for (int j = 0; j <= B; ++j) a.wg0[j] = wg0[j];
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt(128.0));
     timer_events(TK_ATTN, &a.ev_start, &a.ev_stop);
     PPD_TRY_HIP(launch_attn_bf16(a, s));
@@ -374,7 +397,11 @@ ppd_status step_f32(const ppd_model *m, const ppd_kv *kv, int L, int T, const in
   float *tmp = at<float>(ws, w.tmp);
   float2 *rope = at<float2>(ws, w.rope);
 
-  PPD_TRY_HIP(launch_rope_table(depth, T, L, d, m->rope_base, rope, s));
+  SeqBatch one{};
+  one.B = 1;
+  one.t0[1] = T;
+  one.L[0] = L;
+  PPD_TRY_HIP(launch_rope_table(depth, one, d, m->rope_base, rope, s));
   PPD_TRY_HIP(launch_embed(PPD_F32, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
                            nullptr, x, nullptr, nullptr, status, s));
   for (int l = 0; l < m->n_layers; ++l) {
@@ -469,28 +496,49 @@ ppd_status ppd_build_tree_mask(int32_t T, const int32_t *parent, int32_t *depth_
   return PPD_OK;
 }
 
-ppd_status ppd_verify_step(const ppd_model *model, const ppd_kv *kv, int32_t L, int32_t T,
-                           const int32_t *ids, const int32_t *depth, const uint64_t *mask,
-                           void *ws, size_t ws_bytes, float *logits, int32_t *pred,
-                           void *stream) {
+ppd_status ppd_verify_batch(const ppd_model *model, int32_t B, const ppd_kv *kvs,
+                            const int32_t *L, const int32_t *T, const int32_t *ids,
+                            const int32_t *depth, const uint64_t *mask, void *ws, size_t ws_bytes,
+                            float *logits, int32_t *pred, void *stream) {
   ppd_status st = check_model(model);
   if (st != PPD_OK) return st;
-  if ((st = check_kv(model, kv)) != PPD_OK) return st;
-  if (T < 1 || T > PPD_T_MAX) return fail(PPD_EINVAL, "T=%d outside [1, %d]", T, PPD_T_MAX);
-  if (L < 0) return fail(PPD_EINVAL, "L must be >= 0");
-  if ((int64_t)L + T > kv->capacity)
-    return fail(PPD_ECAPACITY, "L + T = %lld exceeds capacity %d", (long long)L + T,
-                kv->capacity);
+  if (B < 1 || B > PPD_BATCH_MAX)
+    return fail(PPD_EINVAL, "B=%d outside [1, %d]", B, PPD_BATCH_MAX);
+  if (!kvs || !L || !T) return fail(PPD_EINVAL, "NULL sequence arrays");
+  if (B > 1 && model->dtype != PPD_BF16)
+    return fail(PPD_EUNSUPPORTED, "batched steps need a bf16 model");
+  int64_t total = 0;
+  for (int j = 0; j < B; ++j) {
+    if ((st = check_kv(model, &kvs[j])) != PPD_OK) return st;
+    if (T[j] < 1) return fail(PPD_EINVAL, "T[%d]=%d must be >= 1", j, T[j]);
+    if (L[j] < 0) return fail(PPD_EINVAL, "L[%d] must be >= 0", j);
+    if ((int64_t)L[j] + T[j] > kvs[j].capacity)
+      return fail(PPD_ECAPACITY, "sequence %d: L + T = %lld exceeds capacity %d", j,
+                  (long long)L[j] + T[j], kvs[j].capacity);
+    total += T[j];
+  }
+  if (total > PPD_T_MAX)
+    return fail(PPD_EINVAL, "%lld tree tokens in all > %d", (long long)total, PPD_T_MAX);
   if (!ids || !depth || !mask || !pred) return fail(PPD_EINVAL, "NULL tree or output pointer");
-  const WsLayout w = layout_of(model, T);
+  const WsLayout w = layout_of(model, (int)total);
   if (!ws || ws_bytes < w.total)
     return fail(PPD_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu required", ws_bytes,
                 w.total);
   hipStream_t s = (hipStream_t)stream;
   g_timer.next = 0;
   if (model->dtype == PPD_BF16)
-    return step_bf16(model, kv, L, T, ids, depth, mask, ws, w, logits, pred, s);
-  return step_f32(model, kv, L, T, ids, depth, mask, ws, w, logits, pred, s);
+    return step_bf16(model, B, kvs, L, T, ids, depth, mask, ws, w, logits, pred, s);
+  return step_f32(model, &kvs[0], L[0], T[0], ids, depth, mask, ws, w, logits, pred, s);
+}
+
+ppd_status ppd_verify_step(const ppd_model *model, const ppd_kv *kv, int32_t L, int32_t T,
+                           const int32_t *ids, const int32_t *depth, const uint64_t *mask,
+                           void *ws, size_t ws_bytes, float *logits, int32_t *pred,
+                           void *stream) {
+  if (!kv) return fail(PPD_EINVAL, "kv cache pointers must be set");
+  if (T < 1 || T > PPD_T_MAX) return fail(PPD_EINVAL, "T=%d outside [1, %d]", T, PPD_T_MAX);
+  return ppd_verify_batch(model, 1, kv, &L, &T, ids, depth, mask, ws, ws_bytes, logits, pred,
+                          stream);
 }
 
 ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids, const int32_t *pred,

@@ -101,6 +101,18 @@ __host__ __device__ inline int gemm_group_owner(long Ng, int G, long x) {
   return (int)(((x + 1) * G - 1) / Ng);
 }
 
+// The sequences of one (batched) step: their tree tokens are packed in
+// sequence order, sequence s owning tokens [t0[s], t0[s + 1]); each has its
+// own cache and cached length.
+struct SeqBatch {
+  int B;
+  int t0[PPD_BATCH_MAX + 1];  // t0[B]: all tokens
+  int L[PPD_BATCH_MAX];       // tokens already in the sequence's cache
+  int cap[PPD_BATCH_MAX];     // its capacity
+  bf16_t *k[PPD_BATCH_MAX];   // this layer's keys [nkv][cap][128]
+  bf16_t *v[PPD_BATCH_MAX];   // this layer's values [nkv][128][cap]
+};
+
 struct GemmLaunch {
   // operands
   const bf16_t *W;      // packed weight (ppd_pack_weight)
@@ -118,8 +130,8 @@ struct GemmLaunch {
   const float2 *rope;  // [T_pad][64]
   // QKV outputs
   bf16_t *q;           // [T_pad][nh][128]
-  bf16_t *kc, *vc;     // layer slice of the caches
-  int nh, nkv, cap, L;
+  int nh, nkv;
+  SeqBatch sb;         // caches, positions: token t of sequence s goes to L[s] + t - t0[s]
   // RESID
   float *x;
   bf16_t *xg;
@@ -147,13 +159,16 @@ hipError_t launch_gemm_bf16(const GemmLaunch &g, hipStream_t s);
 
 struct AttnLaunch {
   const bf16_t *q;      // [T_pad][nh][d]
-  const bf16_t *kc;     // [nkv][cap][d]
-  const bf16_t *vc;     // [nkv][d][cap]
-  const uint64_t *mask;
+  const uint64_t *mask; // [T][2], bits over the token's own tree
   bf16_t *out;          // [T_pad][nh d]
-  float *part;          // [nh][splits][MT][16][PPD_ATTN_OROW] (splits > 1)
+  float *part;          // [nh][max_splits][T_pad][PPD_ATTN_OROW] (splits > 1)
   const bf16_t *zeros;  // >= 16 zero bytes
-  int T, MT, L, cap, nh, nkv, splits, chunk;  // chunk: 32-key blocks per split
+  int T_pad, nh, nkv, max_splits;
+  int MT;               // largest query-tile count of a sequence
+  SeqBatch sb;
+  // sequence s: workgroups [wg0[s], wg0[s + 1]) = nh x splits[s], chunk[s]
+  // 32-key blocks per split
+  int wg0[PPD_BATCH_MAX + 1], splits[PPD_BATCH_MAX], chunk[PPD_BATCH_MAX];
   float scale_log2;     // log2(e) / sqrt(d)
   void *ev_start, *ev_stop;  // optional events at the first dispatch's start / last one's end
 };
@@ -183,7 +198,7 @@ ppd_status ppd_fail(ppd_status s, const char *fmt, ...);
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
                         int T, int vocab, int n_prompt, int H, const void *gain, float *x,
                         void *xg, float *ss, uint32_t *status, hipStream_t s);
-hipError_t launch_rope_table(const int32_t *depth, int T, int L, int d, float base, float2 *rope,
+hipError_t launch_rope_table(const int32_t *depth, const SeqBatch &sb, int d, float base, float2 *rope,
                              hipStream_t s);
 hipError_t launch_argmax_final(const float2 *amax, int n_tiles, int T, int T_pad, int32_t *pred,
                                uint32_t *status, hipStream_t s);

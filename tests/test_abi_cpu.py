@@ -213,3 +213,30 @@ def test_sparse_template_rejects():
         with pytest.raises(ppd.PPDError):
             ppd.ppd_sparse_template(args["p_table"], args["n_cand"], args["n_prompt"],
                                     args["n_ept"])
+
+
+def test_verify_batch_rejects_before_enqueue():
+    L = ppd.lib()
+    m, keep = _fake_model()
+    fake = 0x4000
+    ws_bytes = L.ppd_workspace_bytes(C.byref(m), 128, 256)
+
+    def call(Ls, Ts, caps=None, B=None, wsb=ws_bytes, model=m):
+        B = len(Ls) if B is None else B
+        n = max(1, len(Ls))
+        kvs = (ppd.ppd_kv * n)(*[ppd.ppd_kv(0x2000, 0x3000, (caps or [256] * n)[j], None)
+                                 for j in range(n)])
+        La = np.asarray(Ls + [0] * (n - len(Ls)), np.int32)
+        Ta = np.asarray(Ts + [0] * (n - len(Ts)), np.int32)
+        return L.ppd_verify_batch(C.byref(model), B, C.cast(kvs, C.c_void_p), La.ctypes.data,
+                                  Ta.ctypes.data, fake, fake, fake, fake, wsb, None, fake, None)
+    assert call([0, 0], [16, 16], B=0) == ppd.PPD_EINVAL
+    assert call([0] * 17, [4] * 17) == ppd.PPD_EINVAL                 # B > PPD_BATCH_MAX
+    assert call([0, 0, 0], [64, 64, 1]) == ppd.PPD_EINVAL             # 129 tokens in all
+    assert call([0, 0], [16, 0]) == ppd.PPD_EINVAL                    # an empty tree
+    assert call([0, -1], [16, 16]) == ppd.PPD_EINVAL
+    assert call([0, 250], [16, 16]) == ppd.PPD_ECAPACITY             # sequence 1 overflows
+    assert call([0, 0], [16, 16], caps=[256, 252]) == ppd.PPD_EUNSUPPORTED
+    assert call([0, 0], [64, 64], wsb=ws_bytes - 1) == ppd.PPD_EWORKSPACE
+    mf, kf = _fake_model(ppd.PPD_F32, head_dim=64, hidden=256, ffn=688)
+    assert call([0, 0], [8, 8], model=mf) == ppd.PPD_EUNSUPPORTED       # batches need bf16
