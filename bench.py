@@ -2,6 +2,7 @@
 
     python bench.py [--steps K] [--warmup W] [--workload 7b] [--T 64] [--graph]
     python bench.py --sweep [--workload 13b]     # hardware-aware tree size
+    python bench.py --batch-sweep                # several sequences per step
 
 A step is one pass of the whole hot path on one synthetic batch:
 ppd_verify_step (forward over the T tree nodes, fp32 logits, greedy tokens)
@@ -15,6 +16,13 @@ node: T = 4, 8, .., 128) and of vanilla decoding (T = 1), and prints one JSON
 line per size and one with the size that maximises
 Speedup = tau(T) / L_fp(T) against vanilla (Section 4.2), tau(T) = 1 + the
 expected accepted candidates under the synthetic acceptance table.
+
+--batch-sweep times batched steps (ppd_verify_batch over B sequences, each
+with its own cache of L tokens and its own best sparse tree of T_s tokens,
+then acceptance and compaction per sequence) for B = 1, 2, 4, 8 and T_s =
+16, 32, next to vanilla batches (T_s = 1), and prints one JSON line each:
+the speedup of PPD over vanilla decoding at the same batch size is
+tau(T_s) x L(vanilla, B) / L(PPD, B).
 
 The default workload is the Vicuna-7B-shaped decoder (32 layers, hidden 4096,
 32 heads x 128, ffn 11008, vocab 32000, bf16, random weights) with a
@@ -76,6 +84,8 @@ def main():
                     help="decoder layers in the CPU oracle's timed sample")
     ap.add_argument("--sweep", action="store_true",
                     help="tree-size sweep: L_fp(T) of the best sparse trees and the speedup")
+    ap.add_argument("--batch-sweep", action="store_true",
+                    help="batched steps: B sequences per step, PPD against vanilla")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -127,6 +137,10 @@ def main():
     kv = ppd.KVCache(k, v)
     if args.sweep:
         tree_size_sweep(args, ppd, wl, sh, model, kv, L, cap, dev)
+        return
+    if args.batch_sweep:
+        del k, v, kv
+        batch_sweep(args, ppd, wl, sh, model, L, cap, dev)
         return
     ws = torch.empty(ppd.ppd_workspace_bytes(model, T, cap), dtype=torch.uint8, device=dev)
     ppd.ppd_workspace_init(ws)
@@ -358,6 +372,83 @@ def tree_size_sweep(args, ppd, wl, sh, model, kv, L, cap, dev):
                       "best_candidates": best["candidates"], "best_speedup": best["speedup_vs_vanilla"],
                       "tau": best["tau"], "note": "forward_us / step_us are [median, p10, p90] over "
                       f"{args.steps} steps; tau from the synthetic acceptance table"}), flush=True)
+
+
+def batch_sweep(args, ppd, wl, sh, model, L, cap, dev):
+    """Several sequences per step (ppd_verify_batch): step latency for B
+    sequences with their own caches (L tokens each) and best sparse trees of
+    T_s tokens, against vanilla decoding (T_s = 1) at the same B."""
+    import numpy as np
+    import torch
+    from synth.model import empty_kv, fill_kv_normal
+    from synth.trees import synthetic_accept_table
+
+    p_table = synthetic_accept_table()
+    todev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    B_max = 8
+    caches = []
+    for j in range(B_max):
+        k, v = empty_kv(sh, cap, device=dev)
+        fill_kv_normal(k, v, L, wl.seeds["kv"] + 100 * j)
+        caches.append(ppd.KVCache(k, v))
+    torch.cuda.synchronize()
+    ws = torch.empty(ppd.ppd_workspace_bytes(model, 128, cap), dtype=torch.uint8, device=dev)
+    ppd.ppd_workspace_init(ws)
+    logits = torch.empty((128, sh.vocab), device=dev)
+    pred = torch.empty(128, dtype=torch.int32, device=dev)
+    path = torch.empty(128, dtype=torch.int32, device=dev)
+    n_path = torch.empty(B_max, dtype=torch.int32, device=dev)
+    nxt = torch.empty(B_max, dtype=torch.int32, device=dev)
+    rng = np.random.default_rng(wl.seeds["tree"])
+    base = {}
+    for Ts in (1, 16, 32):
+        if Ts == 1:
+            tp, tk, f = np.array([-1], np.int32), np.array([0], np.int32), 0.0
+        else:
+            tp, tk, f = ppd.ppd_sparse_template(p_table, Ts // 4 - 1, 3)
+        depth, mask = ppd.ppd_build_tree_mask(tp)
+        for B in (1, 2, 4, 8):
+            if B * Ts > 128:
+                continue
+            ids = [np.where(tk < 0, sh.vocab + (-tk - 1), rng.integers(0, sh.vocab, Ts))
+                   for _ in range(B)]
+            ids_d = todev(np.concatenate(ids).astype(np.int32))
+            dep_d = todev(np.tile(depth, B))
+            mask_d = todev(np.tile(mask.view(np.int64), (B, 1)))
+            par_d = todev(np.tile(tp.astype(np.int32), B))
+            kvs, Ls = caches[:B], [L] * B
+
+            def step():
+                ppd.ppd_verify_batch(model, kvs, Ls, [Ts] * B, ids_d, dep_d, mask_d, ws,
+                                     logits[:B * Ts], pred[:B * Ts])
+                for j in range(B):
+                    o = j * Ts
+                    ppd.ppd_accept(Ts, par_d[o:o + Ts], ids_d[o:o + Ts], pred[o:o + Ts], sh.vocab,
+                                   path[o:o + Ts], n_path[j:j + 1], nxt[j:j + 1], ws)
+                    ppd.ppd_kv_compact(model, kvs[j], L, path[o:o + Ts], n_path[j:j + 1])
+
+            for _ in range(args.warmup):
+                step()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+            torch.cuda.synchronize()
+            ev[0].record()
+            for i in range(args.steps):
+                step()
+                ev[i + 1].record()
+            torch.cuda.synchronize()
+            us = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(args.steps)])
+            med = float(np.median(us))
+            tau = 1.0 + f
+            if Ts == 1:
+                base[B] = med
+            row = {"batch_sweep": sh.name, "cache_len": L, "sequences": B, "tree_tokens_each": Ts,
+                   "step_us": [round(med, 1), round(float(np.percentile(us, 10)), 1),
+                               round(float(np.percentile(us, 90)), 1)],
+                   "tau": round(tau, 4),
+                   "tree_tokens_per_s": round(B * Ts / (med * 1e-6), 1),
+                   "projected_tokens_per_s": round(B * tau / (med * 1e-6), 1),
+                   "speedup_vs_vanilla_same_batch": round(tau * base[B] / med, 4)}
+            print(json.dumps(row), flush=True)
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_gemm_7b_hbm_traffic.md")
