@@ -148,7 +148,9 @@ size_t tile_partial_floats(int Tp) { return (size_t)128 * Tp; }
 // key/value block once, so the splits spread the cache over the compute
 // units -- about one workgroup per CU, each keeping at least 4 of the
 // 32-key blocks.
-int attn_max_splits(int nh) { return std::min(PPD_ATTN_MAX_SPLITS, (kCUs + nh - 1) / nh); }
+// key splits per head: nh x splits workgroups must fit one round on the CUs
+// (one attention workgroup per CU), or the last ones run alone afterwards
+int attn_max_splits(int nh) { return std::max(1, std::min(PPD_ATTN_MAX_SPLITS, kCUs / nh)); }
 
 void attn_splits(const ppd_model *m, int L, int T, int *splits, int *chunk) {
   const int nblk = (L + T + 31) / 32;
