@@ -40,6 +40,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# the paper's mean tokens per step with PPD on MT-Bench (Table 1), by model
+PAPER_TAU = {"1.4b": 2.43, "7b": 2.54, "13b": 2.44, "7b-32k": 2.54}
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
@@ -171,13 +173,17 @@ def main():
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
+    # one event between consecutive steps: the mean over the K steps and the
+    # spread of the single steps
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record()
+    for i in range(args.steps):
         run()
-    e1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step_us = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(args.steps)])
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     n_acc = int(n_path.item())
     status = ppd.ppd_device_status(ws)
 
@@ -282,12 +288,19 @@ def main():
         "step_alg_bytes": alg,
         "step_alg_tflops": round(flops / (ms * 1e-3) / 1e12, 2),
         "forward_us": round(fwd_ms * 1e3, 1),
+        "step_us_p10_p50_p90": [round(float(np.percentile(per_step_us, q)), 1) for q in (10, 50, 90)],
         "tree_tokens_per_s": round(T / (ms * 1e-3), 1),
         "emitted_tokens_per_s": round(n_acc / (ms * 1e-3), 1),
         "kernel_us": {k2: round(v2, 2) for k2, v2 in kernels.items()},
         "next_tree_us": round(next_us, 2),
         "next_tree_ept2_us": round(next_ept_us, 2),
         "device_status": status,
+        "projected_tokens_per_s": (round(PAPER_TAU[args.workload] / (ms * 1e-3), 1)
+                                   if args.workload in PAPER_TAU else None),
+        "projection": ("the paper's mean accepted length on MT-Bench for this model "
+                       f"(Table 1: {PAPER_TAU.get(args.workload)} tokens per step) over this "
+                       "step's latency; a projection, not a measurement (random weights accept "
+                       "little)"),
         "roofline": {"bound": "hbm", "kernel": "gate_up GEMM + SwiGLU",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
