@@ -11,12 +11,16 @@
 // each key/value block once per compute unit and spreads the blocks over all
 // CUs: a workgroup owns one sequence (a batched step packs several, each
 // with its own cache and tree), one head h and one of KS contiguous key
-// splits, and all of that sequence's T queries.  The four waves load each block cooperatively (16-byte
-// non-temporal loads into a register ring up to 8 blocks ahead), stage
-// it in a double-buffered LDS slot, and each wave multiplies it with its own
-// 16-query tiles (tiles w and w + 4), keeping one online softmax per query.
-// With KS > 1 each wave stores its tiles' (O, m, l) and a merge kernel adds
-// the splits in split order; with KS = 1 the waves finish in place.
+// splits (at most one round of workgroups on the CUs), and all of that
+// sequence's T queries.  Its eight waves load the split's 64-key block pairs
+// cooperatively (16-byte non-temporal loads of whole 128-byte lines into a
+// register ring 1-6 pairs deep, chosen per launch so that full splits run no
+// idle steps), stage each pair in a double-buffered LDS slot, and multiply:
+// wave w takes the pair's block w / 4 with its 16-query tiles w % 4 (and
+// w % 4 + 4), keeping one online softmax per query; the two blocks' waves
+// are merged through LDS at the end.  With KS > 1 each query's (O, m, l) is
+// stored and a merge kernel adds the splits in split order; with KS = 1 the
+// workgroup writes the output itself.
 //
 // Per 32-key block and query tile, on the matrix cores
 // (v_mfma_f32_16x16x32_bf16):

@@ -77,6 +77,7 @@ def _run_single(case, s):
     ([0, 1, 700, 1024, 5, 64, 1200, 333], ["total:16"] * 8),
     ([1000], ["total:64"]),
     ([200, 900], ["total:64", "total:64"]),
+    ([500, 0, 33], ["total:100", "total:8", "total:20"]),  # a sequence over 64 tokens: two tiles per wave
 ])
 def test_batch_equals_single_sequences_and_oracle(small_case, Ls, specs):
     case = small_case
