@@ -13,9 +13,9 @@
 // with its own cache and tree), one head h and one of KS contiguous key
 // splits (at most one round of workgroups on the CUs), and all of that
 // sequence's T queries.  Its eight waves load the split's 64-key block pairs
-// cooperatively (16-byte non-temporal loads of whole 128-byte lines into a
-// register ring 1-6 pairs deep, chosen per launch so that full splits run no
-// idle steps), stage each pair in a double-buffered LDS slot, and multiply:
+// cooperatively (16-byte non-temporal loads of whole 128-byte lines into
+// registers, the next pair requested while the current one is multiplied),
+// stage each pair in a double-buffered LDS slot, and multiply:
 // wave w takes the pair's block w / 4 with its 16-query tiles w % 4 (and
 // w % 4 + 4), keeping one online softmax per query; the two blocks' waves
 // are merged through LDS at the end.  With KS > 1 each query's (O, m, l) is
@@ -435,41 +435,16 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
 
 }  // namespace
 
-// ring depth (block pairs requested ahead) for a split of n pairs: the loop
-// runs whole trips of RING pairs, so the depth leaving the fewest idle steps
-// in a full split, the deepest among those
-int ring_for(int n_pairs, int max_ring) {
-  int best = 1, idle_best = 1 << 30;
-  for (int r = 1; r <= max_ring; ++r) {
-    const int idle = (n_pairs + r - 1) / r * r - n_pairs;
-    if (idle <= idle_best) {
-      idle_best = idle;
-      best = r;
-    }
-  }
-  return best;
-}
-
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
   const dim3 grid(a.wg0[a.sb.B]), block(512), mblock(256);
   hipEvent_t ev0 = (hipEvent_t)a.ev_start, ev1 = (hipEvent_t)a.ev_stop;
-  int n_pairs = 1, max_ks = 1;  // over the sequences: the ring serves the longest split
-  for (int j = 0; j < a.sb.B; ++j) {
-    n_pairs = std::max(n_pairs, (a.chunk[j] + 1) / 2);
-    max_ks = std::max(max_ks, a.splits[j]);
-  }
+  int max_ks = 1;
+  for (int j = 0; j < a.sb.B; ++j) max_ks = std::max(max_ks, a.splits[j]);
   hipEvent_t main_stop = max_ks > 1 ? nullptr : ev1;
-  void (*kernel)(AttnLaunch);
-  if (a.MT > 4) {
-    static void (*const k2[])(AttnLaunch) = {attn_bf16_kernel<2, 1>, attn_bf16_kernel<2, 2>,
-                                             attn_bf16_kernel<2, 3>};
-    kernel = k2[ring_for(n_pairs, 3) - 1];
-  } else {
-    static void (*const k1[])(AttnLaunch) = {attn_bf16_kernel<1, 1>, attn_bf16_kernel<1, 2>,
-                                             attn_bf16_kernel<1, 3>, attn_bf16_kernel<1, 4>,
-                                             attn_bf16_kernel<1, 5>, attn_bf16_kernel<1, 6>};
-    kernel = k1[ring_for(n_pairs, 6) - 1];
-  }
+  // one pair requested ahead: deeper rings put every workgroup's whole split
+  // in flight at once, and the first pairs then arrive later (measured at
+  // 7B: 19.2 us per layer with one pair ahead, 22.5 with five)
+  auto kernel = a.MT > 4 ? attn_bf16_kernel<2, 1> : attn_bf16_kernel<1, 1>;
   if (ev0)
     hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev0, main_stop, 0, a);
   else
