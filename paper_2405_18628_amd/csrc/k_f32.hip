@@ -34,8 +34,9 @@ hipError_t launch_f32_rownorm(const float *x, const float *gain, int T, int H, f
 
 // out[t][n] = (r ? r[t] : 1) * sum_k A[t][k] W[n][k]; r follows A's T_pad rows when
 // scale_rows is set (see launch_f32_rownorm)
+// (grid: (N / 256, T) -- one row of blocks per token)
 __global__ __launch_bounds__(256) void f32_matmul_kernel(const float *__restrict__ A,
-                                                         const float *__restrict__ W, int T, int N,
+                                                         const float *__restrict__ W, int N,
                                                          int K, const float *__restrict__ r,
                                                          float *__restrict__ out) {
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
@@ -50,14 +51,14 @@ __global__ __launch_bounds__(256) void f32_matmul_kernel(const float *__restrict
 
 hipError_t launch_f32_matmul(const float *A, const float *W, int T, int N, int K, float *out,
                              hipStream_t s) {
-  hipLaunchKernelGGL(f32_matmul_kernel, dim3((N + 255) / 256, T), dim3(256), 0, s, A, W, T, N, K,
+  hipLaunchKernelGGL(f32_matmul_kernel, dim3((N + 255) / 256, T), dim3(256), 0, s, A, W, N, K,
                      (const float *)nullptr, out);
   return hipGetLastError();
 }
 
 hipError_t launch_f32_matmul_scaled(const float *A, const float *W, int T, int N, int K,
                                     const float *r, float *out, hipStream_t s) {
-  hipLaunchKernelGGL(f32_matmul_kernel, dim3((N + 255) / 256, T), dim3(256), 0, s, A, W, T, N, K,
+  hipLaunchKernelGGL(f32_matmul_kernel, dim3((N + 255) / 256, T), dim3(256), 0, s, A, W, N, K,
                      r, out);
   return hipGetLastError();
 }
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(128) void f32_attention_kernel(
     ps = red[0] + red[1];
     l_run = l_run * alpha + ps;
     m_run = m_new;
-    if (threadIdx.x < d) {
+    if ((int)threadIdx.x < d) {
       acc *= alpha;
       const int cn = min(128, n_keys - c0);
       for (int jj = 0; jj < cn; ++jj) {
@@ -158,7 +159,7 @@ __global__ __launch_bounds__(128) void f32_attention_kernel(
     }
     __syncthreads();
   }
-  if (threadIdx.x < d) out[(size_t)t * nh * d + h * d + threadIdx.x] = acc / l_run;
+  if ((int)threadIdx.x < d) out[(size_t)t * nh * d + h * d + threadIdx.x] = acc / l_run;
 }
 
 hipError_t launch_f32_attention(const float *q, const float *kc, const float *vc,
