@@ -36,20 +36,34 @@
 namespace {
 
 constexpr int KC = 64;            // K per chunk: two MFMA k-steps
-constexpr int BN = PPD_GEMM_BN;   // rows per tile: 8 sub-tiles of 16, wave w owns w and w + 4
+constexpr int BN = PPD_GEMM_BN;   // rows of a 128-row tile: 8 sub-tiles of 16
 constexpr int R = PPD_GEMM_RING;  // chunks requested ahead
 constexpr int FRAG = 64;          // u32x4 per packed operand fragment (1 KB)
-constexpr int UNIT = 16 * FRAG;   // u32x4 per packed (tile, chunk): 8 sub-tiles x 2 k-steps
 
-// weight row of tile row r (0 <= r < 128)
+// Sub-tiles of 16 rows per wave: QKV tiles are half a head (64 rows, wave w
+// owns sub-tile w), the others 128 rows (wave w owns sub-tiles w and w + 4).
+// Half-head tiles give the QKV GEMM 2 (heads + 2 kv heads) tiles -- 192 at
+// 7B, enough to run one whole tile per workgroup and finish it in place.
+template <int KIND>
+constexpr int SUBS = KIND == GEMM_QKV ? 1 : 2;
+// u32x4 per packed (tile, chunk): 4 SUBS sub-tiles x 2 k-steps
+template <int KIND>
+constexpr int UNIT = 8 * SUBS<KIND> * FRAG;
+
+// weight row of tile row r (0 <= r < 64 SUBS)
 template <int KIND>
 __device__ __forceinline__ int tile_row(int tile, int r, int N) {
   if constexpr (KIND == GEMM_SWIGLU) {
     // 64 features: gate rows f0..f0+63, then the matching up rows
     return r < 64 ? tile * 64 + r : N + tile * 64 + (r - 64);
+  } else if constexpr (KIND == GEMM_QKV) {
+    // half f of head part tile / 2: sub-tile b's rows 0..7 are dims
+    // 32 f + 8 b .. + 7, rows 8..15 their RoPE partners 64 + those dims, so
+    // a pair lies in lanes l and l + 32 of the accumulator
+    const int f = tile & 1, b = r >> 4, rr = r & 15;
+    return (tile >> 1) * 128 + (rr < 8 ? 0 : 64) + 32 * f + 8 * b + (rr & 7);
   } else {
-    // QKV: tile = one head's 128 rows (dims 0..127); others: consecutive rows
-    return tile * BN + r;
+    return tile * BN + r;  // consecutive rows
   }
 }
 
@@ -117,10 +131,11 @@ __device__ __forceinline__ void epi_request(const GemmLaunch &g, int t, int mt0,
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, r4 = (lane >> 4) * 4;
   if constexpr (KIND == GEMM_QKV) {
+    // pair indices 32 (t % 2) + 8 wave + 4 (lane / 16 % 2) + e, e < 4
+    const int i0 = 32 * (t & 1) + 8 * wave + 4 * ((lane >> 4) & 1);
 #pragma unroll
     for (int mt = 0; mt < MTE; ++mt) {
-      const floatx4 *rp =
-          (const floatx4 *)(g.rope + (size_t)((mt0 + mt) * 16 + lr) * 64 + wave * 16 + r4);
+      const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)((mt0 + mt) * 16 + lr) * 64 + i0);
       o.rope[mt][0] = rp[0];
       o.rope[mt][1] = rp[1];
     }
@@ -138,23 +153,44 @@ __device__ __forceinline__ void epi_request(const GemmLaunch &g, int t, int mt0,
 
 // Epilogue of tile t for token tiles mt0 .. mt0 + MTE - 1 from the complete
 // sums in acc.  Accumulator layout: the lane holds rows 4 (lane / 16) + e of
-// sub-tiles wave and wave + 4, token (mt0 + mt) 16 + lane % 16.  Called by
+// sub-tiles wave (and wave + 4), token (mt0 + mt) 16 + lane % 16.  Called by
 // all 256 threads (it has barriers); rs_s holds the row scales by token.
 template <int KIND, int MTE>
 __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
-                                         const floatx4 (&acc)[2][MTE],
+                                         const floatx4 (&acc)[SUBS<KIND>][MTE],
                                          const EpiOperands<KIND, MTE> &o, const float *rs_s,
                                          float (*red_s)[128][2]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, r4 = (lane >> 4) * 4;
   const int T = g.T, T_pad = g.MT * 16;
   if constexpr (KIND == GEMM_QKV) {
-    const int hp = t;               // head part: q heads, then k, then v
-    const int i0 = wave * 16 + r4;  // dims i0..i0+3 and their partners +64
+    const int hp = t >> 1;          // head part: q heads, then k, then v
+    const bool upper = lane >= 32;  // rows 8..15: the partner dims (+64)
+    const int i0 = 32 * (t & 1) + 8 * wave + 4 * ((lane >> 4) & 1);
+    const int d0 = i0 + (upper ? 64 : 0);  // this lane's dims d0 .. d0 + 3
     const int nh = g.nh, nkv = g.nkv;
 #pragma unroll
     for (int mt = 0; mt < MTE; ++mt) {
+      // padding tokens have a finite row scale too: the pair exchange below
+      // runs on all lanes (lanes l and l + 32 hold the same token)
       const int tk = (mt0 + mt) * 16 + lr;
+      const float rs = rs_s[tk];
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = acc[0][mt][e] * rs;
+      if (hp < nh + nkv) {
+        const float cs[8] = {o.rope[mt][0][0], o.rope[mt][0][1], o.rope[mt][0][2], o.rope[mt][0][3],
+                             o.rope[mt][1][0], o.rope[mt][1][1], o.rope[mt][1][2], o.rope[mt][1][3]};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          // [0]: lane l % 32's value (dim i), [1]: lane l % 32 + 32's (dim i + 64)
+          const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[e]), __float_as_uint(v[e]),
+                                                           false, false);
+          const float a = __uint_as_float(pr[0]), b = __uint_as_float(pr[1]);
+          const float c = cs[2 * e], sn = cs[2 * e + 1];
+          v[e] = upper ? b * c + a * sn : a * c - b * sn;
+        }
+      }
       if (tk >= T) continue;
       // this token's sequence: its cache and the position L + local index
       bf16_t *kc = g.sb.k[0], *vc = g.sb.v[0];
@@ -166,36 +202,14 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
           cap = g.sb.cap[j];
           pos = g.sb.L[j] + tk - g.sb.t0[j];
         }
-      const float rs = rs_s[tk];
-      float lo[4], hi[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        lo[e] = acc[0][mt][e] * rs;
-        hi[e] = acc[1][mt][e] * rs;
-      }
       if (hp < nh + nkv) {
-        const float cs[8] = {o.rope[mt][0][0], o.rope[mt][0][1], o.rope[mt][0][2], o.rope[mt][0][3],
-                             o.rope[mt][1][0], o.rope[mt][1][1], o.rope[mt][1][2], o.rope[mt][1][3]};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float c = cs[2 * e], sn = cs[2 * e + 1];
-          const float a = lo[e], b = hi[e];
-          lo[e] = a * c - b * sn;
-          hi[e] = b * c + a * sn;
-        }
-        const u32x2 plo = u32x2{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
-        const u32x2 phi = u32x2{pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
         bf16_t *dst = hp < nh ? g.q + ((size_t)tk * nh + hp) * 128
                               : kc + ((size_t)(hp - nh) * cap + pos) * 128;
-        *(u32x2 *)(dst + i0) = plo;
-        *(u32x2 *)(dst + i0 + 64) = phi;
+        *(u32x2 *)(dst + d0) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
       } else {
         bf16_t *vb = vc + (size_t)(hp - nh - nkv) * 128 * cap + pos;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          vb[(size_t)(i0 + e) * cap] = f32_to_bf16(lo[e]);
-          vb[(size_t)(i0 + e + 64) * cap] = f32_to_bf16(hi[e]);
-        }
+        for (int e = 0; e < 4; ++e) vb[(size_t)(d0 + e) * cap] = f32_to_bf16(v[e]);
       }
     }
   } else if constexpr (KIND == GEMM_SWIGLU) {
@@ -341,14 +355,15 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   // e = tid + 256 i of the [T_pad][64] chunk (row e / 8, column e % 8).
   // Requests past the range read one 16-byte line (lane offsets masked to 0),
   // so every iteration issues the same loads.
+  constexpr int S = SUBS<KIND>;
   const u32x4 *wp = (const u32x4 *)g.W;
-  u32x4 wr[R][4], ar[R][NAP];
-  auto request_w = [&](int u, u32x4(&dw)[4]) {
+  u32x4 wr[R][2 * S], ar[R][NAP];
+  auto request_w = [&](int u, u32x4(&dw)[2 * S]) {
     const int live = u < u1 ? 63 : 0;
     const int uu = u < u1 ? u : u1 - 1;
-    const u32x4 *wu = wp + (size_t)uu * UNIT + (lane & live);
+    const u32x4 *wu = wp + (size_t)uu * UNIT<KIND> + (lane & live);
 #pragma unroll
-    for (int q = 0; q < 2; ++q)
+    for (int q = 0; q < S; ++q)
 #pragma unroll
       for (int s = 0; s < 2; ++s)
         dw[q * 2 + s] = __builtin_nontemporal_load(wu + ((wave + 4 * q) * 2 + s) * FRAG);
@@ -386,7 +401,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
     }
   };
 
-  floatx4 acc[2][MT];
+  floatx4 acc[S][MT];
   int tile = u0 / kc;
   [[maybe_unused]] EpiOperands<KIND, MT> eo;
   if constexpr (!SPLIT) epi_request<KIND, MT>(g, tile, 0, eo);
@@ -413,7 +428,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   for (int gu = u0; gu < u1;) {
     const int ue = min(u1, (tile + 1) * kc);
 #pragma unroll
-    for (int q = 0; q < 2; ++q)
+    for (int q = 0; q < S; ++q)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
     for (; gu < ue; gu += R) {
@@ -438,7 +453,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
             af[mt] = *(const u32x4 *)(al + r * 128 + swz(r, s * 4 + lg) * 16);
           }
 #pragma unroll
-          for (int q = 0; q < 2; ++q)
+          for (int q = 0; q < S; ++q)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
               acc[q][mt] = mfma16x16x32(as_bf16x8(wr[j][q * 2 + s]), as_bf16x8(af[mt]), acc[q][mt]);
@@ -455,9 +470,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
       const int first = gemm_group_owner(Ng, G, (long)tile * kc / R);
       floatx4 *dst = partial_of(g, tile, blockIdx.x - first);
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int q = 0; q < S; ++q)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) dst[((wave * 2 + q) * MT + mt) * 64 + lane] = acc[q][mt];
+        for (int mt = 0; mt < MT; ++mt) dst[((wave * S + q) * MT + mt) * 64 + lane] = acc[q][mt];
       ++tile;
     } else {
       epilogue<KIND, MT>(g, tile, 0, acc, eo, rs_s, red_s);
@@ -489,22 +504,23 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(GemmLaunch g) {
 
   // U contributors' partials are requested together (one round trip), then
   // added in order
-  constexpr int U = 8;
-  floatx4 acc[2][1];
-  acc[0][0] = acc[1][0] = floatx4{0.f, 0.f, 0.f, 0.f};
+  constexpr int U = 8, S = SUBS<KIND>;
+  floatx4 acc[S][1];
+#pragma unroll
+  for (int q = 0; q < S; ++q) acc[q][0] = floatx4{0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < n_c; c0 += U) {
-    floatx4 buf[U][2];
+    floatx4 buf[U][S];
 #pragma unroll
     for (int v = 0; v < U; ++v) {
       const floatx4 *src = partial_of(g, t, min(c0 + v, n_c - 1));
 #pragma unroll
-      for (int q = 0; q < 2; ++q) buf[v][q] = src[((wave * 2 + q) * g.MT + mt) * 64 + lane];
+      for (int q = 0; q < S; ++q) buf[v][q] = src[((wave * S + q) * g.MT + mt) * 64 + lane];
     }
 #pragma unroll
     for (int v = 0; v < U; ++v)
       if (c0 + v < n_c) {
-        acc[0][0] += buf[v][0];
-        acc[1][0] += buf[v][1];
+#pragma unroll
+        for (int q = 0; q < S; ++q) acc[q][0] += buf[v][q];
       }
   }
   if constexpr (KIND != GEMM_RESID) rs_finish<16>(g, mt * 16, ssv, &red_s[0][0][0], rs_s);
@@ -549,7 +565,7 @@ hipError_t launch_kind(const GemmLaunch &g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// ---- weight packing.  Packed 16-byte item (tile, chunk, sub-tile q < 8,
+// ---- weight packing.  Packed 16-byte item (tile, chunk, sub-tile q < 4 SUBS,
 // k-step s < 2, lane l < 64) holds the 8 bf16 of weight row
 // tile_row(tile, 16 q + l % 16) at columns 64 chunk + 32 s + 8 (l / 16) ..
 // + 7; rows and columns past the matrix (padding) are zero.
@@ -558,10 +574,11 @@ __global__ __launch_bounds__(256) void pack_kernel(const bf16_t *__restrict__ sr
                                                    int N, int K, int rows_total, int kc_pad, long n_items) {
   for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_items;
        i += (long)gridDim.x * blockDim.x) {
+    constexpr int NQ = 4 * SUBS<KIND>;  // sub-tiles per tile
     const int l = (int)(i & 63);
-    const long f = i >> 6;  // fragment ((tile kc_pad + chunk) 8 + q) 2 + s
-    const int s = (int)(f & 1), q = (int)((f >> 1) & 7);
-    const long tc = f >> 4;
+    const long f = i >> 6;  // fragment ((tile kc_pad + chunk) NQ + q) 2 + s
+    const int s = (int)(f & 1), q = (int)((f >> 1) % NQ);
+    const long tc = f / (2 * NQ);
     const int chunk = (int)(tc % kc_pad), tile = (int)(tc / kc_pad);
     const int row = tile_row<KIND>(tile, 16 * q + (l & 15), N);
     const int col = chunk * KC + 32 * s + 8 * (l >> 4);
@@ -574,7 +591,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const bf16_t *__restrict__ sr
 template <int KIND>
 hipError_t launch_pack_kind(int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s) {
   const int n_tiles = gemm_tiles_of(KIND, N), kc_pad = gemm_kc_pad_of(K);
-  const long n_items = (long)n_tiles * kc_pad * UNIT;
+  const long n_items = (long)n_tiles * kc_pad * UNIT<KIND>;
   const int rows_total = KIND == GEMM_SWIGLU ? 2 * N : N;
   const dim3 grid((unsigned)std::min<long>(8192, (n_items + 255) / 256)), block(256);
   hipLaunchKernelGGL(pack_kernel<KIND>, grid, block, 0, s, src, (u32x4 *)dst, N, K, rows_total,
@@ -584,7 +601,11 @@ hipError_t launch_pack_kind(int N, int K, const bf16_t *src, bf16_t *dst, hipStr
 
 }  // namespace
 
-int gemm_tiles_of(int kind, int N) { return kind == GEMM_SWIGLU ? N / 64 : (N + BN - 1) / BN; }
+int gemm_tiles_of(int kind, int N) {
+  return kind == GEMM_SWIGLU || kind == GEMM_QKV ? N / 64 : (N + BN - 1) / BN;
+}
+
+int gemm_tile_rows_of(int kind) { return kind == GEMM_QKV ? 64 : BN; }
 
 int gemm_kc_pad_of(int K) { return ((K / KC + R - 1) / R) * R; }
 

@@ -134,7 +134,7 @@ GemmShape gemm_shape(int kind, int N, int K) {
 enum { SH_QKV = 0, SH_O = 1, SH_GATE_UP = 2, SH_DOWN = 3, SH_LM = 4 };
 
 void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
-  out[SH_QKV] = gemm_shape(GEMM_QKV, qkv_rows(m), m->hidden);        // one head per tile
+  out[SH_QKV] = gemm_shape(GEMM_QKV, qkv_rows(m), m->hidden);        // half a head per tile
   out[SH_O] = gemm_shape(GEMM_RESID, m->hidden, m->n_heads * 128);  // output projection
   out[SH_GATE_UP] = gemm_shape(GEMM_SWIGLU, m->ffn, m->hidden);     // 64 features per tile
   out[SH_DOWN] = gemm_shape(GEMM_RESID, m->hidden, m->ffn);         // down projection
@@ -668,7 +668,8 @@ const char *ppd_last_error(void) { return g_err.c_str(); }
 size_t ppd_packed_weight_bytes(int32_t kind, int32_t rows, int32_t cols) {
   int gk, N;
   if (pack_args(kind, rows, cols, &gk, &N) != PPD_OK) return 0;
-  return (size_t)gemm_tiles_of(gk, N) * gemm_kc_pad_of(cols) * PPD_GEMM_BN * 64 * sizeof(bf16_t);
+  return (size_t)gemm_tiles_of(gk, N) * gemm_kc_pad_of(cols) * gemm_tile_rows_of(gk) * 64 *
+         sizeof(bf16_t);
 }
 
 ppd_status ppd_pack_weight(int32_t kind, int32_t rows, int32_t cols, const void *src, void *dst,

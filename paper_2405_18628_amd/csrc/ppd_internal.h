@@ -82,9 +82,10 @@ struct WsLayout {
 // ---------------------------------------------------------------------------
 // kernel launchers (defined in the .hip files, called by the host driver)
 
-// Skinny GEMM partition.  Tiles of 128 output rows; each tile's K is cut in
-// 64-column chunks, padded with zero chunks to kc_pad, a multiple of
-// PPD_GEMM_RING; a group is PPD_GEMM_RING consecutive chunks of one tile.
+// Skinny GEMM partition.  Tiles of 128 output rows (QKV: 64, half a head);
+// each tile's K is cut in 64-column chunks, padded with zero chunks to
+// kc_pad, a multiple of PPD_GEMM_RING; a group is PPD_GEMM_RING consecutive
+// chunks of one tile.
 // Unit u = tile * kc_pad + chunk.  Workgroup w of G owns the contiguous
 // groups [Ng w / G, Ng (w + 1) / G), Ng = n_tiles * kc_pad / PPD_GEMM_RING,
 // so every workgroup streams an equal share and tile boundaries fall between
@@ -151,6 +152,7 @@ enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_SWIGLU = 2, GEMM_LOGITS = 3 }
 // packed layout of a weight for GEMM kind `kind` with N output rows (SwiGLU:
 // F features, 2F rows) and K columns
 int gemm_tiles_of(int kind, int N);
+int gemm_tile_rows_of(int kind);  // 64 (QKV: half a head) or 128
 int gemm_kc_pad_of(int K);
 hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s);
 hipError_t launch_gemm_bf16(const GemmLaunch &g, hipStream_t s);

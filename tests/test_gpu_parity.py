@@ -215,22 +215,31 @@ def test_tiny_multistep_lossless(tiny_case):
 def _expected_packing(w, kind):
     """The packed layout of include/ppd.h, written out with numpy indexing:
     item (tile, chunk, q, s, lane) = row r(tile, 16 q + lane % 16), columns
-    64 chunk + 32 s + 8 (lane // 16) .. + 7; zeros past the matrix."""
+    64 chunk + 32 s + 8 (lane // 16) .. + 7; zeros past the matrix.  QKV
+    tiles are half a head: sub-tile q of half f holds dims 32 f + 8 q .. + 7
+    in its rows 0..7 and their RoPE partners (+64) in rows 8..15."""
     rows, cols = w.shape
     kc = -(-(cols // 64) // 4) * 4
     if kind == ppd.PPD_W_GATE_UP:
         F = rows // 2
         n_tiles = F // 64
         tr = np.concatenate([np.arange(64), F + np.arange(64)])[None, :] + 64 * np.arange(n_tiles)[:, None]
+    elif kind == ppd.PPD_W_QKV:
+        n_tiles = rows // 64
+        r = np.arange(64)
+        dims = np.where(r % 16 < 8, 0, 64) + 8 * (r // 16) + r % 8          # within a half
+        half = np.arange(n_tiles) % 2
+        tr = 128 * (np.arange(n_tiles) // 2)[:, None] + 32 * half[:, None] + dims[None, :]
     else:
         n_tiles = -(-rows // 128)
         tr = np.arange(128)[None, :] + 128 * np.arange(n_tiles)[:, None]
+    nq = tr.shape[1] // 16
     wp = np.zeros((n_tiles * 128 + rows, kc * 64), dtype=w.dtype)
     wp[:rows, :cols] = w
     tr = np.where(tr < rows, tr, rows + 1)          # padding rows read the zero block
     lane = np.arange(64)
-    out = np.zeros((n_tiles, kc, 8, 2, 64, 8), dtype=w.dtype)
-    for q in range(8):
+    out = np.zeros((n_tiles, kc, nq, 2, 64, 8), dtype=w.dtype)
+    for q in range(nq):
         rr = tr[:, 16 * q + lane % 16]              # [tiles][64]
         for s in range(2):
             for c in range(kc):
