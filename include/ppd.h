@@ -114,8 +114,10 @@ typedef struct {
  * Weight packing for PPD_BF16 models.  The verification step streams every
  * projection weight from HBM once per step (its cost is that stream), so the
  * library keeps them in the order its matrix-core GEMMs consume them: 128-row
- * tiles x 64-column chunks, each chunk a run of 1 KB operand fragments of 16
- * rows x 32 columns in the lane order of the gfx950 bf16 MFMA instruction.
+ * tiles (PPD_W_QKV: 64-row half-head tiles, each head's RoPE partner rows
+ * i and i + 64 side by side) x 64-column chunks, each chunk a run of 1 KB
+ * operand fragments of 16 rows x 32 columns in the lane order of the gfx950
+ * bf16 MFMA instruction.
  * Rows and columns past the matrix are zero-filled (e.g. the LM head's last
  * tile when vocab % 128 != 0).  The packed form depends only on the matrix,
  * not on T or L; pack once at load time.

@@ -18,14 +18,15 @@
 //    XOR-swizzled LDS slot read by the four waves;
 //  * a compute unit's load path sustains only ~35 GB/s, so a GEMM needs
 //    (nearly) every CU streaming to approach the HBM rate.  GEMMs with enough
-//    128-row tiles run one whole tile per workgroup and finish it in place
-//    (fused epilogue).  The others are cut Stream-K style: the (tile, chunk)
-//    units are split into equal contiguous ranges, one per compute unit; a
-//    workgroup streams across tile boundaries and stores the partial sums of
-//    each tile segment, and a small finish kernel (one workgroup per tile and
-//    16-token block) adds a tile's partials in workgroup order and runs the
-//    epilogue -- the kernel boundary orders the two, so no cross-workgroup
-//    synchronisation is needed and results never depend on timing;
+//    tiles (128 rows; QKV: 64, half a head) run one whole tile per workgroup
+//    and finish it in place (fused epilogue).  The others are cut Stream-K
+//    style: the (tile, chunk) units are split into equal contiguous ranges,
+//    one per compute unit; a workgroup streams across tile boundaries and
+//    stores the partial sums of each tile segment, and a small finish kernel
+//    (one workgroup per tile and 16-token block) adds a tile's partials in
+//    workgroup order and runs the epilogue -- the kernel boundary orders the
+//    two, so no cross-workgroup synchronisation is needed and results never
+//    depend on timing;
 //  * the epilogue: RMSNorm row scale, RoPE + query/key/value stores into the
 //    cache (QKV), residual add + next norm operand + sum of squares (output /
 //    down projection), SwiGLU (gate/up), logits + argmax partials (LM head).
