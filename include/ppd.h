@@ -113,13 +113,19 @@ typedef struct {
 /*
  * Weight packing for PPD_BF16 models.  The verification step streams every
  * projection weight from HBM once per step (its cost is that stream), so the
- * library keeps them in the order its matrix-core GEMMs consume them: 128-row
- * tiles (PPD_W_QKV: 64-row half-head tiles, each head's RoPE partner rows
- * i and i + 64 side by side) x 64-column chunks, each chunk a run of 1 KB
- * operand fragments of 16 rows x 32 columns in the lane order of the gfx950
- * bf16 MFMA instruction.
+ * library keeps them in the order its matrix-core GEMMs consume them: tiles
+ * of output rows x 64-column chunks, each chunk a run of 1 KB operand
+ * fragments of 16 rows x 32 columns in the lane order of the gfx950 bf16 MFMA
+ * instruction.  A tile holds ns groups: 16 QKV rows (dims 8j .. 8j + 7 of a
+ * head and their RoPE partners + 64), or 16 gate/up features (their gate rows
+ * and up rows), or 32 consecutive rows of the other matrices (ns = 4, 128
+ * rows).  ns = 3 for PPD_W_QKV and PPD_W_GATE_UP when cols % 512 == 0, their
+ * tiles of 4 groups number at least 160, and tiles of 3 leave fewer groups
+ * per compute unit over the 256 CUs of an MI355X (Vicuna-7B shapes: 256 QKV
+ * tiles, 230 gate/up tiles), else ns = 4.
  * Rows and columns past the matrix are zero-filled (e.g. the LM head's last
- * tile when vocab % 128 != 0).  The packed form depends only on the matrix,
+ * tile when vocab % 128 != 0, the last gate/up tile when ffn % (16 ns) != 0).
+ * The packed form depends only on the matrix,
  * not on T or L; pack once at load time.
  *   kind  which matrix (ppd_weight_kind); rows, cols: its row-major shape,
  *         i.e. PPD_W_QKV [(n_heads + 2 n_kv_heads) 128][hidden],

@@ -40,29 +40,45 @@ constexpr int KC = 64;            // K per chunk: two MFMA k-steps
 constexpr int BN = PPD_GEMM_BN;   // rows of a 128-row tile: 8 sub-tiles of 16
 constexpr int R = PPD_GEMM_RING;  // chunks requested ahead
 constexpr int FRAG = 64;          // u32x4 per packed operand fragment (1 KB)
+// Ring depth of 3-group whole tiles (needs K % 512 == 0).  Measured at 7B:
+// with 3 of 4 waves streaming weights a 4-chunk ring keeps too few bytes in
+// flight (QKV 30.0, gate/up 40.1 us against 28.9 / 37.5 with 4-group tiles);
+// 8 chunks give 28.1 / 35.9 us.  4-group tiles and split GEMMs are slower
+// with 8 (gate/up 38.5, output / down projection 18.9 / 28.2 against 17.3 /
+// 26.2 us).
+constexpr int kRing3 = 8;
 
-// Sub-tiles of 16 rows per wave: QKV tiles are half a head (64 rows, wave w
-// owns sub-tile w), the others 128 rows (wave w owns sub-tiles w and w + 4).
-// Half-head tiles give the QKV GEMM 2 (heads + 2 kv heads) tiles -- 192 at
-// 7B, enough to run one whole tile per workgroup and finish it in place.
+// A tile holds NS row groups, one per wave (waves NS..3 stage activations
+// only), each of SUBS sub-tiles of 16 rows: wave w owns sub-tiles w (QKV:
+// 16 rows, 8 dims of a head and their RoPE partners) or w and w + NS
+// (SwiGLU: 16 gate rows and the matching 16 up rows; others: 16 + 16
+// consecutive rows).  NS = 4 gives 64-row QKV tiles (half a head), 64
+// features per gate/up tile and 128-row tiles elsewhere; NS = 3 (whole-tile
+// QKV and gate/up only) cuts the tiles a quarter smaller where that lets
+// every CU run one tile of 3 groups instead of some CUs idling while the
+// others run 4 (7B: 256 QKV tiles instead of 192, 230 gate/up tiles instead
+// of 172).
 template <int KIND>
 constexpr int SUBS = KIND == GEMM_QKV ? 1 : 2;
-// u32x4 per packed (tile, chunk): 4 SUBS sub-tiles x 2 k-steps
-template <int KIND>
-constexpr int UNIT = 8 * SUBS<KIND> * FRAG;
+// u32x4 per packed (tile, chunk): NS SUBS sub-tiles x 2 k-steps
+template <int KIND, int NS>
+constexpr int UNIT = 2 * NS * SUBS<KIND> * FRAG;
 
-// weight row of tile row r (0 <= r < 64 SUBS)
-template <int KIND>
+// weight row of tile row r (0 <= r < 16 NS SUBS); rows >= the matrix's are
+// padding (zero weights, no output)
+template <int KIND, int NS>
 __device__ __forceinline__ int tile_row(int tile, int r, int N) {
   if constexpr (KIND == GEMM_SWIGLU) {
-    // 64 features: gate rows f0..f0+63, then the matching up rows
-    return r < 64 ? tile * 64 + r : N + tile * 64 + (r - 64);
+    // 16 NS features: gate rows f0 .. f0 + 16 NS - 1, then the matching up rows
+    constexpr int FT = 16 * NS;
+    const int f = tile * FT + (r < FT ? r : r - FT);
+    return f >= N ? 2 * N : r < FT ? f : N + f;  // features past F: padding
   } else if constexpr (KIND == GEMM_QKV) {
-    // half f of head part tile / 2: sub-tile b's rows 0..7 are dims
-    // 32 f + 8 b .. + 7, rows 8..15 their RoPE partners 64 + those dims, so
-    // a pair lies in lanes l and l + 32 of the accumulator
-    const int f = tile & 1, b = r >> 4, rr = r & 15;
-    return (tile >> 1) * 128 + (rr < 8 ? 0 : 64) + 32 * f + 8 * b + (rr & 7);
+    // global sub-tile gs: sub-tile gs % 8 of head part gs / 8; its rows 0..7
+    // are dims 8 (gs % 8) .. + 7, rows 8..15 their RoPE partners 64 + those
+    // dims, so a pair lies in lanes l and l + 32 of the accumulator
+    const int gs = tile * NS + (r >> 4), rr = r & 15;
+    return (gs >> 3) * 128 + (rr < 8 ? 0 : 64) + 8 * (gs & 7) + (rr & 7);
   } else {
     return tile * BN + r;  // consecutive rows
   }
@@ -126,14 +142,15 @@ struct EpiOperands {
   uint2 gain[2];         // RESID: next norm gain of the lane's rows
 };
 
-template <int KIND, int MTE>
+template <int KIND, int MTE, int NS = 4>
 __device__ __forceinline__ void epi_request(const GemmLaunch &g, int t, int mt0,
                                             EpiOperands<KIND, MTE> &o) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, r4 = (lane >> 4) * 4;
   if constexpr (KIND == GEMM_QKV) {
-    // pair indices 32 (t % 2) + 8 wave + 4 (lane / 16 % 2) + e, e < 4
-    const int i0 = 32 * (t & 1) + 8 * wave + 4 * ((lane >> 4) & 1);
+    // pair indices 8 (gs % 8) + 4 (lane / 16 % 2) + e, e < 4, of the wave's
+    // global sub-tile gs (waves >= NS read a valid pair and do not use it)
+    const int i0 = 8 * ((t * NS + wave) & 7) + 4 * ((lane >> 4) & 1);
 #pragma unroll
     for (int mt = 0; mt < MTE; ++mt) {
       const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)((mt0 + mt) * 16 + lr) * 64 + i0);
@@ -156,7 +173,7 @@ __device__ __forceinline__ void epi_request(const GemmLaunch &g, int t, int mt0,
 // sums in acc.  Accumulator layout: the lane holds rows 4 (lane / 16) + e of
 // sub-tiles wave (and wave + 4), token (mt0 + mt) 16 + lane % 16.  Called by
 // all 256 threads (it has barriers); rs_s holds the row scales by token.
-template <int KIND, int MTE>
+template <int KIND, int MTE, int NS = 4>
 __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
                                          const floatx4 (&acc)[SUBS<KIND>][MTE],
                                          const EpiOperands<KIND, MTE> &o, const float *rs_s,
@@ -165,11 +182,13 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
   const int lr = lane & 15, r4 = (lane >> 4) * 4;
   const int T = g.T, T_pad = g.MT * 16;
   if constexpr (KIND == GEMM_QKV) {
-    const int hp = t >> 1;          // head part: q heads, then k, then v
-    const bool upper = lane >= 32;  // rows 8..15: the partner dims (+64)
-    const int i0 = 32 * (t & 1) + 8 * wave + 4 * ((lane >> 4) & 1);
-    const int d0 = i0 + (upper ? 64 : 0);  // this lane's dims d0 .. d0 + 3
+    const int gs = t * NS + wave;   // the wave's global sub-tile
     const int nh = g.nh, nkv = g.nkv;
+    if (wave >= NS || gs >= (nh + 2 * nkv) * 8) return;  // no rows (no barriers below)
+    const int hp = gs >> 3;         // head part: q heads, then k, then v
+    const bool upper = lane >= 32;  // rows 8..15: the partner dims (+64)
+    const int i0 = 8 * (gs & 7) + 4 * ((lane >> 4) & 1);
+    const int d0 = i0 + (upper ? 64 : 0);  // this lane's dims d0 .. d0 + 3
 #pragma unroll
     for (int mt = 0; mt < MTE; ++mt) {
       // padding tokens have a finite row scale too: the pair exchange below
@@ -214,7 +233,8 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
       }
     }
   } else if constexpr (KIND == GEMM_SWIGLU) {
-    const int f0 = t * 64 + wave * 16 + r4;
+    const int f0 = t * 16 * NS + wave * 16 + r4;
+    if (wave >= NS || f0 >= g.N) return;  // no features (no barriers below)
 #pragma unroll
     for (int mt = 0; mt < MTE; ++mt) {
       const int tk = (mt0 + mt) * 16 + lr;
@@ -328,8 +348,11 @@ __device__ __forceinline__ floatx4 *partial_of(const GemmLaunch &g, int t, int s
 // ---- the GEMM.  Workgroup w of G owns the units [u0, u1) (see
 // PPD_GEMM_RING); SPLIT: store the partial of every tile segment, else every
 // segment is a whole tile and is finished in place.
-template <int MT, int KIND, bool SPLIT>
+template <int MT, int KIND, bool SPLIT, int NS, int RING>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
+  static_assert(NS == 4 || (!SPLIT && (KIND == GEMM_QKV || KIND == GEMM_SWIGLU)),
+                "3-group tiles: whole-tile QKV and gate/up only");
+  static_assert(RING == R || (!SPLIT && RING % R == 0), "whole tiles only take a deeper ring");
   constexpr int T_pad = MT * 16;
   constexpr int NAP = (T_pad * 8 + 255) / 256;  // 16-byte activation pieces per thread per chunk
   __shared__ __attribute__((aligned(16))) unsigned char lds_a[2][T_pad * 128];
@@ -340,11 +363,13 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15;  // MFMA row (weights) / column (tokens) within a 16-tile
   const int lg = lane >> 4;  // this lane's 16-byte k group within a 32-step
+  // waves >= NS own no rows: they stage activations and skip the weights
+  const bool owns = NS == 4 || __builtin_amdgcn_readfirstlane(wave) < NS;
   const int K = g.K, kc = g.kc_pad, G = g.G;
-  const long Ng = (long)g.n_tiles * kc / R;
+  const long Ng = (long)g.n_tiles * kc / RING;
   // this workgroup's units [u0, u1) (uniform: kept in scalar registers)
-  const int u0 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x) * R);
-  const int u1 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x + 1) * R);
+  const int u0 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x) * RING);
+  const int u1 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x + 1) * RING);
 
   // norm row scales, requested before the weight stream starts
   constexpr bool kScale = !SPLIT && KIND != GEMM_RESID;
@@ -352,22 +377,23 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   if constexpr (kScale) rs_request<T_pad>(g, 0, ssv);
 
   // ---- register rings.  Unit u's weight fragments for this wave: sub-tiles
-  // wave and wave + 4, k-steps 0 and 1.  Its activation pieces: 16-byte piece
+  // wave (and wave + NS), k-steps 0 and 1.  Its activation pieces: 16-byte piece
   // e = tid + 256 i of the [T_pad][64] chunk (row e / 8, column e % 8).
   // Requests past the range read one 16-byte line (lane offsets masked to 0),
   // so every iteration issues the same loads.
   constexpr int S = SUBS<KIND>;
   const u32x4 *wp = (const u32x4 *)g.W;
-  u32x4 wr[R][2 * S], ar[R][NAP];
+  u32x4 wr[RING][2 * S], ar[RING][NAP];
   auto request_w = [&](int u, u32x4(&dw)[2 * S]) {
+    if (!owns) return;
     const int live = u < u1 ? 63 : 0;
     const int uu = u < u1 ? u : u1 - 1;
-    const u32x4 *wu = wp + (size_t)uu * UNIT<KIND> + (lane & live);
+    const u32x4 *wu = wp + (size_t)uu * UNIT<KIND, NS> + (lane & live);
 #pragma unroll
     for (int q = 0; q < S; ++q)
 #pragma unroll
       for (int s = 0; s < 2; ++s)
-        dw[q * 2 + s] = __builtin_nontemporal_load(wu + ((wave + 4 * q) * 2 + s) * FRAG);
+        dw[q * 2 + s] = __builtin_nontemporal_load(wu + ((wave + NS * q) * 2 + s) * FRAG);
   };
   // per-lane element offsets of the activation pieces within a chunk;
   // pieces e >= T_pad * 8 (odd MT) load row 0 and are not staged
@@ -405,10 +431,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   floatx4 acc[S][MT];
   int tile = u0 / kc;
   [[maybe_unused]] EpiOperands<KIND, MT> eo;
-  if constexpr (!SPLIT) epi_request<KIND, MT>(g, tile, 0, eo);
-  const int c0 = u0 - tile * kc;  // first unit's chunk (a multiple of R)
+  if constexpr (!SPLIT) epi_request<KIND, MT, NS>(g, tile, 0, eo);
+  const int c0 = u0 - tile * kc;  // first unit's chunk (a multiple of RING)
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
+  for (int j = 0; j < RING; ++j) {
     request_w(u0 + j, wr[j]);
     request_a(u0 + j, c0 + j, ar[j]);
   }
@@ -418,10 +444,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   // written by an epilogue, after them as well
 
   // ---- main loop over segments (the units of one tile within [u0, u1)),
-  // R units per trip.  Unit u: stage its activations (requested R units ago)
-  // into LDS slot (u - u0) & 1 and request unit u + R's into the freed
-  // registers; barrier; multiply with the weight fragments requested R units
-  // ago, then request unit u + R's weights into them.  The slot staged here
+  // RING units per trip.  Unit u: stage its activations (requested RING units ago)
+  // into LDS slot (u - u0) & 1 and request unit u + RING's into the freed
+  // registers; barrier; multiply with the weight fragments requested RING units
+  // ago, then request unit u + RING's weights into them.  The slot staged here
   // was last read for unit u - 2, which every wave finished before unit
   // u - 1's barrier.  The accumulators are zeroed per segment, so the inner
   // loop carries them unchanged.
@@ -432,21 +458,22 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
     for (int q = 0; q < S; ++q)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (; gu < ue; gu += R) {
-      // chunk of unit gu + R + j: gc + R + j, wrapped into the next tile
-      const int nc = gc + R < kc ? gc + R : gc + R - kc;
+    for (; gu < ue; gu += RING) {
+      // chunk of unit gu + RING + j: gc + RING + j, wrapped into the next tile
+      const int nc = gc + RING < kc ? gc + RING : gc + RING - kc;
 #pragma unroll
-      for (int j = 0; j < R; ++j) {
+      for (int j = 0; j < RING; ++j) {
         const int u = gu + j;
         const int slot = (u - u0) & 1;
         stage(ar[j], slot);
         __builtin_amdgcn_sched_barrier(0);
-        request_a(u + R, nc + j, ar[j]);
+        request_a(u + RING, nc + j, ar[j]);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
         const unsigned char *al = lds_a[slot];
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
+          if (!owns) break;
           u32x4 af[MT];
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
@@ -460,7 +487,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
               acc[q][mt] = mfma16x16x32(as_bf16x8(wr[j][q * 2 + s]), as_bf16x8(af[mt]), acc[q][mt]);
         }
         __builtin_amdgcn_sched_barrier(0);
-        request_w(u + R, wr[j]);
+        request_w(u + RING, wr[j]);
         __builtin_amdgcn_sched_barrier(0);
       }
       gc = nc;
@@ -468,7 +495,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
     if constexpr (SPLIT) {
       // this segment's partial, in slot (this workgroup - the tile's first
       // contributor); plain stores: the finish kernel runs after this grid
-      const int first = gemm_group_owner(Ng, G, (long)tile * kc / R);
+      const int first = gemm_group_owner(Ng, G, (long)tile * kc / RING);
       floatx4 *dst = partial_of(g, tile, blockIdx.x - first);
 #pragma unroll
       for (int q = 0; q < S; ++q)
@@ -476,10 +503,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
         for (int mt = 0; mt < MT; ++mt) dst[((wave * S + q) * MT + mt) * 64 + lane] = acc[q][mt];
       ++tile;
     } else {
-      epilogue<KIND, MT>(g, tile, 0, acc, eo, rs_s, red_s);
+      epilogue<KIND, MT, NS>(g, tile, 0, acc, eo, rs_s, red_s);
       if (ue < u1) {
         __syncthreads();  // red_s is written again by the next tile's epilogue
-        epi_request<KIND, MT>(g, ++tile, 0, eo);
+        epi_request<KIND, MT, NS>(g, ++tile, 0, eo);
       }
     }
   }
@@ -535,25 +562,29 @@ hipError_t launch_kind(const GemmLaunch &g, hipStream_t s) {
   hipEvent_t ev0 = (hipEvent_t)g.ev_start, ev1 = (hipEvent_t)g.ev_stop;
   // timed: from the GEMM dispatch's start to the last dispatch's end
   hipEvent_t gemm_stop = g.split ? nullptr : ev1;
+  constexpr bool kNs3 = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
+  if (g.ns != 4 && !(kNs3 && g.ns == 3 && !g.split && g.kc_pad % kRing3 == 0))
+    return hipErrorInvalidValue;
   switch (g.MT) {
+#define PPD_LAUNCH(M, SP, NS, RG)                                                            \
+  if (ev0)                                                                                   \
+    hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND, SP, NS, RG>), grid, block, 0, s, ev0,   \
+                          gemm_stop, 0, g);                                                  \
+  else                                                                                       \
+    hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND, SP, NS, RG>), grid, block, 0, s, g);
 #define PPD_CASE(M)                                                                          \
   case M:                                                                                    \
     if (g.split) {                                                                           \
-      if (ev0)                                                                               \
-        hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND, true>), grid, block, 0, s, ev0,     \
-                              gemm_stop, 0, g);                                              \
-      else                                                                                   \
-        hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND, true>), grid, block, 0, s, g);         \
+      PPD_LAUNCH(M, true, 4, R)                                                              \
+    } else if (g.ns == 3) {                                                                  \
+      if constexpr (kNs3) { PPD_LAUNCH(M, false, (kNs3 ? 3 : 4), kRing3) }                   \
     } else {                                                                                 \
-      if (ev0)                                                                               \
-        hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND, false>), grid, block, 0, s, ev0,    \
-                              gemm_stop, 0, g);                                              \
-      else                                                                                   \
-        hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND, false>), grid, block, 0, s, g);        \
+      PPD_LAUNCH(M, false, 4, R)                                                             \
     }                                                                                        \
     break;
     PPD_CASE(1) PPD_CASE(2) PPD_CASE(3) PPD_CASE(4) PPD_CASE(5) PPD_CASE(6) PPD_CASE(7) PPD_CASE(8)
 #undef PPD_CASE
+#undef PPD_LAUNCH
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
@@ -570,18 +601,18 @@ hipError_t launch_kind(const GemmLaunch &g, hipStream_t s) {
 // k-step s < 2, lane l < 64) holds the 8 bf16 of weight row
 // tile_row(tile, 16 q + l % 16) at columns 64 chunk + 32 s + 8 (l / 16) ..
 // + 7; rows and columns past the matrix (padding) are zero.
-template <int KIND>
+template <int KIND, int NS>
 __global__ __launch_bounds__(256) void pack_kernel(const bf16_t *__restrict__ src, u32x4 *__restrict__ dst,
                                                    int N, int K, int rows_total, int kc_pad, long n_items) {
   for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_items;
        i += (long)gridDim.x * blockDim.x) {
-    constexpr int NQ = 4 * SUBS<KIND>;  // sub-tiles per tile
+    constexpr int NQ = NS * SUBS<KIND>;  // sub-tiles per tile
     const int l = (int)(i & 63);
     const long f = i >> 6;  // fragment ((tile kc_pad + chunk) NQ + q) 2 + s
     const int s = (int)(f & 1), q = (int)((f >> 1) % NQ);
     const long tc = f / (2 * NQ);
     const int chunk = (int)(tc % kc_pad), tile = (int)(tc / kc_pad);
-    const int row = tile_row<KIND>(tile, 16 * q + (l & 15), N);
+    const int row = tile_row<KIND, NS>(tile, 16 * q + (l & 15), N);
     const int col = chunk * KC + 32 * s + 8 * (l >> 4);
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (row < rows_total && col < K) v = *(const u32x4 *)(src + (size_t)row * K + col);
@@ -589,33 +620,43 @@ __global__ __launch_bounds__(256) void pack_kernel(const bf16_t *__restrict__ sr
   }
 }
 
-template <int KIND>
+template <int KIND, int NS>
 hipError_t launch_pack_kind(int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s) {
-  const int n_tiles = gemm_tiles_of(KIND, N), kc_pad = gemm_kc_pad_of(K);
-  const long n_items = (long)n_tiles * kc_pad * UNIT<KIND>;
+  const int n_tiles = gemm_tiles_of(KIND, N, NS), kc_pad = gemm_kc_pad_of(K);
+  const long n_items = (long)n_tiles * kc_pad * UNIT<KIND, NS>;
   const int rows_total = KIND == GEMM_SWIGLU ? 2 * N : N;
   const dim3 grid((unsigned)std::min<long>(8192, (n_items + 255) / 256)), block(256);
-  hipLaunchKernelGGL(pack_kernel<KIND>, grid, block, 0, s, src, (u32x4 *)dst, N, K, rows_total,
+  hipLaunchKernelGGL((pack_kernel<KIND, NS>), grid, block, 0, s, src, (u32x4 *)dst, N, K, rows_total,
                      kc_pad, n_items);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int gemm_tiles_of(int kind, int N) {
-  return kind == GEMM_SWIGLU || kind == GEMM_QKV ? N / 64 : (N + BN - 1) / BN;
+int gemm_tiles_of(int kind, int N, int ns) {
+  // QKV: N / 16 sub-tiles; gate/up: N / 16 blocks of 16 features
+  return kind == GEMM_SWIGLU || kind == GEMM_QKV ? (N / 16 + ns - 1) / ns : (N + BN - 1) / BN;
 }
 
-int gemm_tile_rows_of(int kind) { return kind == GEMM_QKV ? 64 : BN; }
+int gemm_tile_rows_of(int kind, int ns) {
+  return kind == GEMM_QKV ? 16 * ns : kind == GEMM_SWIGLU ? 32 * ns : BN;
+}
 
 int gemm_kc_pad_of(int K) { return ((K / KC + R - 1) / R) * R; }
 
-hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s) {
+hipError_t launch_pack_weight(int kind, int N, int K, int ns, const bf16_t *src, bf16_t *dst,
+                              hipStream_t s) {
+  if (ns == 3) {
+    if (kind == GEMM_QKV) return launch_pack_kind<GEMM_QKV, 3>(N, K, src, dst, s);
+    if (kind == GEMM_SWIGLU) return launch_pack_kind<GEMM_SWIGLU, 3>(N, K, src, dst, s);
+    return hipErrorInvalidValue;
+  }
+  if (ns != 4) return hipErrorInvalidValue;
   switch (kind) {
-    case GEMM_QKV: return launch_pack_kind<GEMM_QKV>(N, K, src, dst, s);
-    case GEMM_RESID: return launch_pack_kind<GEMM_RESID>(N, K, src, dst, s);
-    case GEMM_SWIGLU: return launch_pack_kind<GEMM_SWIGLU>(N, K, src, dst, s);
-    case GEMM_LOGITS: return launch_pack_kind<GEMM_LOGITS>(N, K, src, dst, s);
+    case GEMM_QKV: return launch_pack_kind<GEMM_QKV, 4>(N, K, src, dst, s);
+    case GEMM_RESID: return launch_pack_kind<GEMM_RESID, 4>(N, K, src, dst, s);
+    case GEMM_SWIGLU: return launch_pack_kind<GEMM_SWIGLU, 4>(N, K, src, dst, s);
+    case GEMM_LOGITS: return launch_pack_kind<GEMM_LOGITS, 4>(N, K, src, dst, s);
   }
   return hipErrorInvalidValue;
 }

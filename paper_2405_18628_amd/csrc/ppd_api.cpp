@@ -115,11 +115,28 @@ constexpr int kWholeTileMin = 160;
 
 struct GemmShape {
   int kind, N, K;
-  int n_tiles, kc_pad, G, maxc, split;
+  int n_tiles, kc_pad, G, maxc, split, ns;
 };
 
+// Row groups per tile of a GEMM with N outputs (gate/up: features): 4, or 3
+// for whole-tile QKV and gate/up GEMMs when the smaller tiles leave every CU
+// fewer groups to stream (one whole tile per workgroup, one workgroup per CU
+// and round: 7B QKV 768 groups as 256 tiles of 3 instead of 192 of 4,
+// gate/up 688 as 230 of 3 instead of 172 of 4).  A function of the matrix
+// shape alone, so the packed weight does not depend on T or L.
+int gemm_ns_of(int kind, int N, int K) {
+  if (kind != GEMM_QKV && kind != GEMM_SWIGLU) return 4;
+  if (K % 512) return 4;  // their 8-chunk ring needs 8 | K / 64
+  const int groups = N / 16;
+  const int t4 = (groups + 3) / 4, t3 = (groups + 2) / 3;
+  if (t4 < kWholeTileMin) return 4;  // split over all CUs instead
+  const int rounds4 = (t4 + kCUs - 1) / kCUs, rounds3 = (t3 + kCUs - 1) / kCUs;
+  return 3 * rounds3 < 4 * rounds4 ? 3 : 4;
+}
+
 GemmShape gemm_shape(int kind, int N, int K) {
-  GemmShape g{kind, N, K, gemm_tiles_of(kind, N), gemm_kc_pad_of(K), 0, 1, 0};
+  const int ns = gemm_ns_of(kind, N, K);
+  GemmShape g{kind, N, K, gemm_tiles_of(kind, N, ns), gemm_kc_pad_of(K), 0, 1, 0, ns};
   const long Ng = (long)g.n_tiles * g.kc_pad / PPD_GEMM_RING;
   g.split = g.n_tiles < kWholeTileMin;
   g.G = g.split ? (int)std::min<long>(kCUs, Ng) : g.n_tiles;
@@ -267,6 +284,7 @@ ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t
     g.G = sh.G;
     g.maxc = sh.maxc;
     g.split = sh.split;
+    g.ns = sh.ns;
   };
 
   PPD_TRY_HIP(launch_rope_table(depth, seq_batch(m, B, kvs, Ls, Ts, 0), m->head_dim,
@@ -668,7 +686,8 @@ const char *ppd_last_error(void) { return g_err.c_str(); }
 size_t ppd_packed_weight_bytes(int32_t kind, int32_t rows, int32_t cols) {
   int gk, N;
   if (pack_args(kind, rows, cols, &gk, &N) != PPD_OK) return 0;
-  return (size_t)gemm_tiles_of(gk, N) * gemm_kc_pad_of(cols) * gemm_tile_rows_of(gk) * 64 *
+  const int ns = gemm_ns_of(gk, N, cols);
+  return (size_t)gemm_tiles_of(gk, N, ns) * gemm_kc_pad_of(cols) * gemm_tile_rows_of(gk, ns) * 64 *
          sizeof(bf16_t);
 }
 
@@ -678,7 +697,7 @@ ppd_status ppd_pack_weight(int32_t kind, int32_t rows, int32_t cols, const void 
   ppd_status st = pack_args(kind, rows, cols, &gk, &N);
   if (st != PPD_OK) return st;
   if (!src || !dst) return fail(PPD_EINVAL, "NULL weight pointer");
-  PPD_TRY_HIP(launch_pack_weight(gk, N, cols, (const bf16_t *)src, (bf16_t *)dst,
+  PPD_TRY_HIP(launch_pack_weight(gk, N, cols, gemm_ns_of(gk, N, cols), (const bf16_t *)src, (bf16_t *)dst,
                                  (hipStream_t)stream));
   return PPD_OK;
 }

@@ -82,7 +82,9 @@ struct WsLayout {
 // ---------------------------------------------------------------------------
 // kernel launchers (defined in the .hip files, called by the host driver)
 
-// Skinny GEMM partition.  Tiles of 128 output rows (QKV: 64, half a head);
+// Skinny GEMM partition.  Tiles of ns row groups of 16 (QKV) or 32 rows
+// (ns = 4: 128 rows, QKV 64, half a head; ns = 3 for whole-tile QKV and
+// gate/up where that spreads them over more CUs, see gemm_ns_of);
 // each tile's K is cut in 64-column chunks, padded with zero chunks to
 // kc_pad, a multiple of PPD_GEMM_RING; a group is PPD_GEMM_RING consecutive
 // chunks of one tile.
@@ -122,6 +124,7 @@ struct GemmLaunch {
   int N, K, T, MT;      // N = output rows (SwiGLU: F), MT = T_pad / 16
   int kind;             // GemmKind
   int n_tiles, kc_pad, G, maxc;  // partition (see above); maxc: max workgroups per tile
+  int ns;               // row groups (waves with rows) per tile: 4, or 3 (whole QKV / gate/up)
   int split;            // G != n_tiles: partial sums + finish kernel
   float *part;          // split: [n_tiles][maxc][8 MT 64][4] partial sums
   // epilogue inputs
@@ -151,10 +154,12 @@ enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_SWIGLU = 2, GEMM_LOGITS = 3 }
 
 // packed layout of a weight for GEMM kind `kind` with N output rows (SwiGLU:
 // F features, 2F rows) and K columns
-int gemm_tiles_of(int kind, int N);
-int gemm_tile_rows_of(int kind);  // 64 (QKV: half a head) or 128
+// with ns row groups per tile
+int gemm_tiles_of(int kind, int N, int ns);
+int gemm_tile_rows_of(int kind, int ns);  // 16 ns (QKV), 32 ns (gate/up) or 128
 int gemm_kc_pad_of(int K);
-hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s);
+hipError_t launch_pack_weight(int kind, int N, int K, int ns, const bf16_t *src, bf16_t *dst,
+                              hipStream_t s);
 hipError_t launch_gemm_bf16(const GemmLaunch &g, hipStream_t s);
 
 #define PPD_ATTN_OROW 132  // floats per partial row: 128 dims, m, l, padding

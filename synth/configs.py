@@ -77,6 +77,10 @@ VICUNA_13B = ModelShape("vicuna-13b", 40, 5120, 40, 40, 128, 13824, 32000, "bf16
 # small bf16 shapes for fast parity tests (several tiles, ragged vocab/ffn/L)
 SMALL_BF16 = ModelShape("small-bf16", 2, 512, 4, 4, 128, 1344, 1000, "bf16")
 SMALL_GQA = ModelShape("small-gqa-bf16", 2, 512, 4, 2, 128, 1408, 1000, "bf16")
+# narrow hidden, 7B-wide heads and ffn: the QKV and gate/up GEMMs take the
+# 7B tilings (256 QKV tiles of 3 row groups; 230 gate/up tiles of 48
+# features, the last one ragged) at a size the oracle runs in seconds
+WIDE_BF16 = ModelShape("wide-bf16", 1, 512, 32, 32, 128, 11008, 1000, "bf16")
 
 WORKLOADS = {
     # 0: tiny fp32 decoder, 128-token prefix from a real prefill, 10-candidate tree
@@ -92,6 +96,7 @@ WORKLOADS = {
     # test-only shapes
     "small": Workload("small", SMALL_BF16, 300, "total:40", 4, "normal", 10),
     "small-gqa": Workload("small-gqa", SMALL_GQA, 77, "total:29", 4, "normal", 11),
+    "wide": Workload("wide", WIDE_BF16, 300, "total:40", 4, "normal", 12),
 }
 
 T13B_SWEEP = (16, 32, 64, 128)

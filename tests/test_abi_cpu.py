@@ -122,12 +122,15 @@ def test_accept_and_compact_reject_before_enqueue():
 
 def test_packed_weight_sizes_and_rejections():
     """Packed size = tiles x (64-column chunks rounded up to a multiple of 4)
-    x 128 rows x 64 columns x 2 bytes; rows past the matrix (the LM head's
-    last tile) and padding chunks are counted, nothing else."""
+    x tile rows x 64 columns x 2 bytes; rows past the matrix (the LM head's
+    last tile, the last 48-feature gate/up tile at 7B) and padding chunks are
+    counted, nothing else.  Sizes below in 128-row x 64-column units."""
     L = ppd.lib()
     unit = 128 * 64 * 2
     cases = [(ppd.PPD_W_QKV, 3 * 4096, 4096, 96 * 64), (ppd.PPD_W_O, 4096, 4096, 32 * 64),
-             (ppd.PPD_W_GATE_UP, 2 * 11008, 4096, 172 * 64), (ppd.PPD_W_DOWN, 4096, 11008, 32 * 172),
+             (ppd.PPD_W_GATE_UP, 2 * 11008, 4096, 230 * 64 * 96 // 128),
+             (ppd.PPD_W_GATE_UP, 2 * 13824, 5120, 216 * 80), (ppd.PPD_W_QKV, 3 * 5120, 5120, 120 * 80),
+             (ppd.PPD_W_GATE_UP, 2 * 11008, 256, 172 * 4), (ppd.PPD_W_DOWN, 4096, 11008, 32 * 172),
              (ppd.PPD_W_LM_HEAD, 32000, 4096, 250 * 64), (ppd.PPD_W_LM_HEAD, 1000, 512, 8 * 8),
              (ppd.PPD_W_DOWN, 512, 1344, 4 * 24), (ppd.PPD_W_GATE_UP, 2 * 1344, 512, 21 * 8)]
     for kind, rows, cols, units in cases:

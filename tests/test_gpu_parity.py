@@ -133,6 +133,22 @@ def test_small_bf16_long_prefix(small_long_case, L, spec):
     _check_tree_kv(case, tree, ref, L=L)
 
 
+def test_wide_heads_and_ffn():
+    """7B-wide heads and ffn over a narrow hidden size: QKV and gate/up run
+    the 3-group tiles (gate/up's last tile ragged), every output against the
+    oracle."""
+    case = make_case(workload("wide"))
+    for spec in ("total:40", "total:64"):
+        tree = tree_for(case, spec=spec)
+        say(f"[wide] T={tree.T}")
+        ws = workspace(case, tree.T)
+        res = gpu_step(case, tree, ws)
+        ref = oracle_step(case, tree)
+        check_logits(res["logits"], ref["logits"], "bf16")
+        check_pred(res["pred"], ref["logits"], "bf16")
+        _check_tree_kv(case, tree, ref)
+
+
 def test_small_gqa():
     case = make_case(workload("small-gqa"))
     for spec in ("total:29", "total:70"):
@@ -220,16 +236,25 @@ def _expected_packing(w, kind):
     in its rows 0..7 and their RoPE partners (+64) in rows 8..15."""
     rows, cols = w.shape
     kc = -(-(cols // 64) // 4) * 4
+    if kind in (ppd.PPD_W_GATE_UP, ppd.PPD_W_QKV):
+        # ns groups of 16 features (gate/up) or 16 QKV rows per tile: 4, or 3
+        # when cols % 512 == 0, every tile stays whole (>= 160 tiles of 4)
+        # and 3-group tiles need fewer groups per CU over 256 CUs
+        groups = rows // 32 if kind == ppd.PPD_W_GATE_UP else rows // 16
+        t4, t3 = -(-groups // 4), -(-groups // 3)
+        ns = 3 if cols % 512 == 0 and t4 >= 160 and 3 * -(-t3 // 256) < 4 * -(-t4 // 256) else 4
+        n_tiles = -(-groups // ns)
     if kind == ppd.PPD_W_GATE_UP:
         F = rows // 2
-        n_tiles = F // 64
-        tr = np.concatenate([np.arange(64), F + np.arange(64)])[None, :] + 64 * np.arange(n_tiles)[:, None]
+        f = 16 * ns * np.arange(n_tiles)[:, None] + np.arange(16 * ns)[None, :]
+        tr = np.concatenate([f, F + f], axis=1)
+        tr = np.where(np.concatenate([f, f], axis=1) < F, tr, rows)   # padding features
     elif kind == ppd.PPD_W_QKV:
-        n_tiles = rows // 64
-        r = np.arange(64)
-        dims = np.where(r % 16 < 8, 0, 64) + 8 * (r // 16) + r % 8          # within a half
-        half = np.arange(n_tiles) % 2
-        tr = 128 * (np.arange(n_tiles) // 2)[:, None] + 32 * half[:, None] + dims[None, :]
+        r = np.arange(16 * ns)
+        gs = ns * np.arange(n_tiles)[:, None] + (r // 16)[None, :]   # global 16-row group
+        # group gs: dims 8 (gs % 8) .. + 7 of head part gs // 8 in rows 0..7,
+        # their RoPE partners (+64) in rows 8..15
+        tr = 128 * (gs // 8) + np.where(r % 16 < 8, 0, 64)[None, :] + 8 * (gs % 8) + (r % 8)[None, :]
     else:
         n_tiles = -(-rows // 128)
         tr = np.arange(128)[None, :] + 128 * np.arange(n_tiles)[:, None]
@@ -252,7 +277,10 @@ def _expected_packing(w, kind):
 @pytest.mark.parametrize("kind,rows,cols", [(ppd.PPD_W_LM_HEAD, 1000, 512),
                                             (ppd.PPD_W_GATE_UP, 2 * 1344, 512),
                                             (ppd.PPD_W_DOWN, 512, 1344),
-                                            (ppd.PPD_W_QKV, 6 * 128, 256)])
+                                            (ppd.PPD_W_QKV, 6 * 128, 256),
+                                            (ppd.PPD_W_GATE_UP, 2 * 11008, 512),
+                                            (ppd.PPD_W_QKV, 96 * 128, 512),
+                                            (ppd.PPD_W_QKV, 96 * 128, 256)])
 def test_pack_weight_layout(kind, rows, cols):
     say(f"[pack] kind={kind} {rows}x{cols}")
     g = torch.Generator().manual_seed(rows * 7 + cols)
