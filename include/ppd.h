@@ -122,7 +122,9 @@ typedef struct {
  * rows).  ns = 3 for PPD_W_QKV and PPD_W_GATE_UP when cols % 512 == 0, their
  * tiles of 4 groups number at least 160, and tiles of 3 leave fewer groups
  * per compute unit over the 256 CUs of an MI355X (Vicuna-7B shapes: 256 QKV
- * tiles, 230 gate/up tiles), else ns = 4.
+ * tiles, 230 gate/up tiles); ns = 2 for PPD_W_GATE_UP when cols % 512 == 0,
+ * its tiles of 4 groups number fewer than 160 and tiles of 2 number 160 to
+ * 256 (MobileLLaMA-1.4B shape: 176 tiles); else ns = 4.
  * Rows and columns past the matrix are zero-filled (e.g. the LM head's last
  * tile when vocab % 128 != 0, the last gate/up tile when ffn % (16 ns) != 0).
  * The packed form depends only on the matrix,

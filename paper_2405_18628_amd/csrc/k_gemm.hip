@@ -40,7 +40,7 @@ constexpr int KC = 64;            // K per chunk: two MFMA k-steps
 constexpr int BN = PPD_GEMM_BN;   // rows of a 128-row tile: 8 sub-tiles of 16
 constexpr int R = PPD_GEMM_RING;  // chunks requested ahead
 constexpr int FRAG = 64;          // u32x4 per packed operand fragment (1 KB)
-// Ring depth of 3-group whole tiles (needs K % 512 == 0).  Measured at 7B:
+// Ring depth of 3- and 2-group whole tiles (needs K % 512 == 0).  Measured at 7B:
 // with 3 of 4 waves streaming weights a 4-chunk ring keeps too few bytes in
 // flight (QKV 30.0, gate/up 40.1 us against 28.9 / 37.5 with 4-group tiles);
 // 8 chunks give 28.1 / 35.9 us.  4-group tiles and split GEMMs are slower
@@ -48,16 +48,17 @@ constexpr int FRAG = 64;          // u32x4 per packed operand fragment (1 KB)
 // 26.2 us).
 constexpr int kRing3 = 8;
 
-// A tile holds NS row groups, one per wave (waves NS..3 stage activations
-// only), each of SUBS sub-tiles of 16 rows: wave w owns sub-tiles w (QKV:
-// 16 rows, 8 dims of a head and their RoPE partners) or w and w + NS
-// (SwiGLU: 16 gate rows and the matching 16 up rows; others: 16 + 16
-// consecutive rows).  NS = 4 gives 64-row QKV tiles (half a head), 64
-// features per gate/up tile and 128-row tiles elsewhere; NS = 3 (whole-tile
-// QKV and gate/up only) cuts the tiles a quarter smaller where that lets
-// every CU run one tile of 3 groups instead of some CUs idling while the
-// others run 4 (7B: 256 QKV tiles instead of 192, 230 gate/up tiles instead
-// of 172).
+// A tile holds NS row groups, each of SUBS sub-tiles of 16 rows: wave w
+// owns group w, i.e. sub-tiles w (QKV: 16 rows, 8 dims of a head and their
+// RoPE partners) or w and w + NS (SwiGLU: 16 gate rows and the matching 16
+// up rows; others: 16 + 16 consecutive rows).  NS = 4 gives 64-row QKV tiles
+// (half a head), 64 features per gate/up tile and 128-row tiles elsewhere.
+// Whole-tile QKV and gate/up GEMMs may take smaller tiles where that spreads
+// them over more CUs: NS = 3 (waves 0-2 own the groups, wave 3 only stages
+// activations; 7B: 256 QKV tiles instead of 192, 230 gate/up tiles instead
+// of 172) or NS = 2 (waves w and w + 2 share group w, each multiplying one of
+// the two k-steps of every chunk, and add their sums through LDS at the end;
+// 1.4B: 176 whole gate/up tiles instead of a split GEMM).
 template <int KIND>
 constexpr int SUBS = KIND == GEMM_QKV ? 1 : 2;
 // u32x4 per packed (tile, chunk): NS SUBS sub-tiles x 2 k-steps
@@ -351,7 +352,7 @@ __device__ __forceinline__ floatx4 *partial_of(const GemmLaunch &g, int t, int s
 template <int MT, int KIND, bool SPLIT, int NS, int RING>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   static_assert(NS == 4 || (!SPLIT && (KIND == GEMM_QKV || KIND == GEMM_SWIGLU)),
-                "3-group tiles: whole-tile QKV and gate/up only");
+                "3- and 2-group tiles: whole-tile QKV and gate/up only");
   static_assert(RING == R || (!SPLIT && RING % R == 0), "whole tiles only take a deeper ring");
   constexpr int T_pad = MT * 16;
   constexpr int NAP = (T_pad * 8 + 255) / 256;  // 16-byte activation pieces per thread per chunk
@@ -363,8 +364,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15;  // MFMA row (weights) / column (tokens) within a 16-tile
   const int lg = lane >> 4;  // this lane's 16-byte k group within a 32-step
-  // waves >= NS own no rows: they stage activations and skip the weights
-  const bool owns = NS == 4 || __builtin_amdgcn_readfirstlane(wave) < NS;
+  // NS = 3: wave 3 owns no rows (it stages activations, skips the weights);
+  // NS = 2: wave w multiplies k-step w / 2 of group w % 2
+  const bool owns = NS != 3 || __builtin_amdgcn_readfirstlane(wave) < NS;
+  const int kst = __builtin_amdgcn_readfirstlane(wave >> 1);  // NS = 2: this wave's k-step
   const int K = g.K, kc = g.kc_pad, G = g.G;
   const long Ng = (long)g.n_tiles * kc / RING;
   // this workgroup's units [u0, u1) (uniform: kept in scalar registers)
@@ -389,11 +392,18 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
     const int live = u < u1 ? 63 : 0;
     const int uu = u < u1 ? u : u1 - 1;
     const u32x4 *wu = wp + (size_t)uu * UNIT<KIND, NS> + (lane & live);
+    if constexpr (NS == 2) {
+      // group wave % 2, k-step kst only (held in slot q * 2)
 #pragma unroll
-    for (int q = 0; q < S; ++q)
+      for (int q = 0; q < S; ++q)
+        dw[q * 2] = __builtin_nontemporal_load(wu + (((wave & 1) + 2 * q) * 2 + kst) * FRAG);
+    } else {
 #pragma unroll
-      for (int s = 0; s < 2; ++s)
-        dw[q * 2 + s] = __builtin_nontemporal_load(wu + ((wave + NS * q) * 2 + s) * FRAG);
+      for (int q = 0; q < S; ++q)
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+          dw[q * 2 + s] = __builtin_nontemporal_load(wu + ((wave + NS * q) * 2 + s) * FRAG);
+    }
   };
   // per-lane element offsets of the activation pieces within a chunk;
   // pieces e >= T_pad * 8 (odd MT) load row 0 and are not staged
@@ -471,9 +481,22 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
         const unsigned char *al = lds_a[slot];
+        if constexpr (NS == 2) {
+          u32x4 af[MT];
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const int r = mt * 16 + lr;
+            af[mt] = *(const u32x4 *)(al + r * 128 + swz(r, kst * 4 + lg) * 16);
+          }
+#pragma unroll
+          for (int q = 0; q < S; ++q)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[q][mt] = mfma16x16x32(as_bf16x8(wr[j][q * 2]), as_bf16x8(af[mt]), acc[q][mt]);
+        }
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-          if (!owns) break;
+          if (NS == 2 || !owns) break;
           u32x4 af[MT];
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
@@ -503,6 +526,26 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
         for (int mt = 0; mt < MT; ++mt) dst[((wave * S + q) * MT + mt) * 64 + lane] = acc[q][mt];
       ++tile;
     } else {
+      if constexpr (NS == 2) {
+        // wave w + 2 adds its k-step's sums into wave w's through the
+        // activation slots (2 S MT KB <= their 4 MT KB), once every wave is
+        // done reading them
+        floatx4 *red = (floatx4 *)&lds_a[0][0];
+        __syncthreads();
+        if (wave >= 2) {
+#pragma unroll
+          for (int q = 0; q < S; ++q)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) red[(((wave - 2) * S + q) * MT + mt) * 64 + lane] = acc[q][mt];
+        }
+        __syncthreads();
+        if (wave < 2) {
+#pragma unroll
+          for (int q = 0; q < S; ++q)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[q][mt] += red[((wave * S + q) * MT + mt) * 64 + lane];
+        }
+      }
       epilogue<KIND, MT, NS>(g, tile, 0, acc, eo, rs_s, red_s);
       if (ue < u1) {
         __syncthreads();  // red_s is written again by the next tile's epilogue
@@ -563,7 +606,7 @@ hipError_t launch_kind(const GemmLaunch &g, hipStream_t s) {
   // timed: from the GEMM dispatch's start to the last dispatch's end
   hipEvent_t gemm_stop = g.split ? nullptr : ev1;
   constexpr bool kNs3 = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
-  if (g.ns != 4 && !(kNs3 && g.ns == 3 && !g.split && g.kc_pad % kRing3 == 0))
+  if (g.ns != 4 && !(kNs3 && (g.ns == 3 || g.ns == 2) && !g.split && g.kc_pad % kRing3 == 0))
     return hipErrorInvalidValue;
   switch (g.MT) {
 #define PPD_LAUNCH(M, SP, NS, RG)                                                            \
@@ -578,6 +621,8 @@ hipError_t launch_kind(const GemmLaunch &g, hipStream_t s) {
       PPD_LAUNCH(M, true, 4, R)                                                              \
     } else if (g.ns == 3) {                                                                  \
       if constexpr (kNs3) { PPD_LAUNCH(M, false, (kNs3 ? 3 : 4), kRing3) }                   \
+    } else if (g.ns == 2) {                                                                  \
+      if constexpr (kNs3) { PPD_LAUNCH(M, false, (kNs3 ? 2 : 4), kRing3) }                   \
     } else {                                                                                 \
       PPD_LAUNCH(M, false, 4, R)                                                             \
     }                                                                                        \
@@ -649,6 +694,11 @@ hipError_t launch_pack_weight(int kind, int N, int K, int ns, const bf16_t *src,
   if (ns == 3) {
     if (kind == GEMM_QKV) return launch_pack_kind<GEMM_QKV, 3>(N, K, src, dst, s);
     if (kind == GEMM_SWIGLU) return launch_pack_kind<GEMM_SWIGLU, 3>(N, K, src, dst, s);
+    return hipErrorInvalidValue;
+  }
+  if (ns == 2) {
+    if (kind == GEMM_QKV) return launch_pack_kind<GEMM_QKV, 2>(N, K, src, dst, s);
+    if (kind == GEMM_SWIGLU) return launch_pack_kind<GEMM_SWIGLU, 2>(N, K, src, dst, s);
     return hipErrorInvalidValue;
   }
   if (ns != 4) return hipErrorInvalidValue;

@@ -118,18 +118,27 @@ struct GemmShape {
   int n_tiles, kc_pad, G, maxc, split, ns;
 };
 
-// Row groups per tile of a GEMM with N outputs (gate/up: features): 4, or 3
-// for whole-tile QKV and gate/up GEMMs when the smaller tiles leave every CU
+// Row groups per tile of a GEMM with N outputs (gate/up: features): 4, or
+// for QKV and gate/up GEMMs 3 when the smaller whole tiles leave every CU
 // fewer groups to stream (one whole tile per workgroup, one workgroup per CU
 // and round: 7B QKV 768 groups as 256 tiles of 3 instead of 192 of 4,
-// gate/up 688 as 230 of 3 instead of 172 of 4).  A function of the matrix
-// shape alone, so the packed weight does not depend on T or L.
+// gate/up 688 as 230 of 3 instead of 172 of 4), or, for gate/up, 2 when
+// tiles of 4 would be too few to stay whole and tiles of 2 fill one round
+// (1.4B: 352 groups as 176 tiles instead of a split GEMM and its finish
+// kernel: 20.0 against 22.0 us).  QKV stays split there: a 2-group QKV tile
+// streams 32 weight rows per read of the whole activation operand (320 KB at
+// T = 80 for 128 KB of weights), and took 18.7 against 18.3 us split.  A
+// function of the matrix shape alone, so the packed weight does not depend
+// on T or L.
 int gemm_ns_of(int kind, int N, int K) {
   if (kind != GEMM_QKV && kind != GEMM_SWIGLU) return 4;
   if (K % 512) return 4;  // their 8-chunk ring needs 8 | K / 64
   const int groups = N / 16;
   const int t4 = (groups + 3) / 4, t3 = (groups + 2) / 3;
-  if (t4 < kWholeTileMin) return 4;  // split over all CUs instead
+  if (t4 < kWholeTileMin) {
+    const int t2 = (groups + 1) / 2;
+    return kind == GEMM_SWIGLU && t2 >= kWholeTileMin && t2 <= kCUs ? 2 : 4;  // else split
+  }
   const int rounds4 = (t4 + kCUs - 1) / kCUs, rounds3 = (t3 + kCUs - 1) / kCUs;
   return 3 * rounds3 < 4 * rounds4 ? 3 : 4;
 }

@@ -81,6 +81,10 @@ SMALL_GQA = ModelShape("small-gqa-bf16", 2, 512, 4, 2, 128, 1408, 1000, "bf16")
 # 7B tilings (256 QKV tiles of 3 row groups; 230 gate/up tiles of 48
 # features, the last one ragged) at a size the oracle runs in seconds
 WIDE_BF16 = ModelShape("wide-bf16", 1, 512, 32, 32, 128, 11008, 1000, "bf16")
+# narrow hidden, 1.4B-wide heads and ffn: QKV and gate/up take the 1.4B
+# tilings (split QKV; 176 gate/up tiles of 2 feature groups, each group's
+# two k-steps on two waves)
+MID_BF16 = ModelShape("mid-bf16", 1, 512, 16, 16, 128, 5632, 1000, "bf16")
 
 WORKLOADS = {
     # 0: tiny fp32 decoder, 128-token prefix from a real prefill, 10-candidate tree
@@ -97,6 +101,7 @@ WORKLOADS = {
     "small": Workload("small", SMALL_BF16, 300, "total:40", 4, "normal", 10),
     "small-gqa": Workload("small-gqa", SMALL_GQA, 77, "total:29", 4, "normal", 11),
     "wide": Workload("wide", WIDE_BF16, 300, "total:40", 4, "normal", 12),
+    "mid": Workload("mid", MID_BF16, 300, "total:40", 4, "normal", 13),
 }
 
 T13B_SWEEP = (16, 32, 64, 128)

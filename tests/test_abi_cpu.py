@@ -130,7 +130,8 @@ def test_packed_weight_sizes_and_rejections():
     cases = [(ppd.PPD_W_QKV, 3 * 4096, 4096, 96 * 64), (ppd.PPD_W_O, 4096, 4096, 32 * 64),
              (ppd.PPD_W_GATE_UP, 2 * 11008, 4096, 230 * 64 * 96 // 128),
              (ppd.PPD_W_GATE_UP, 2 * 13824, 5120, 216 * 80), (ppd.PPD_W_QKV, 3 * 5120, 5120, 120 * 80),
-             (ppd.PPD_W_GATE_UP, 2 * 11008, 256, 172 * 4), (ppd.PPD_W_DOWN, 4096, 11008, 32 * 172),
+             (ppd.PPD_W_GATE_UP, 2 * 11008, 256, 172 * 4), (ppd.PPD_W_QKV, 3 * 2048, 2048, 48 * 32),
+             (ppd.PPD_W_GATE_UP, 2 * 5632, 2048, 176 * 32 // 2), (ppd.PPD_W_GATE_UP, 2 * 5632, 1024, 88 * 16), (ppd.PPD_W_DOWN, 4096, 11008, 32 * 172),
              (ppd.PPD_W_LM_HEAD, 32000, 4096, 250 * 64), (ppd.PPD_W_LM_HEAD, 1000, 512, 8 * 8),
              (ppd.PPD_W_DOWN, 512, 1344, 4 * 24), (ppd.PPD_W_GATE_UP, 2 * 1344, 512, 21 * 8)]
     for kind, rows, cols, units in cases:

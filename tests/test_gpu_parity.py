@@ -133,14 +133,15 @@ def test_small_bf16_long_prefix(small_long_case, L, spec):
     _check_tree_kv(case, tree, ref, L=L)
 
 
-def test_wide_heads_and_ffn():
-    """7B-wide heads and ffn over a narrow hidden size: QKV and gate/up run
-    the 3-group tiles (gate/up's last tile ragged), every output against the
-    oracle."""
-    case = make_case(workload("wide"))
-    for spec in ("total:40", "total:64"):
+@pytest.mark.parametrize("name", ["wide", "mid"])
+def test_wide_heads_and_ffn(name):
+    """7B- or 1.4B-wide heads and ffn over a narrow hidden size: QKV and
+    gate/up run the 3-group tiles (gate/up's last tile ragged) or the 2-group
+    tiles with one k-step per wave, every output against the oracle."""
+    case = make_case(workload(name))
+    for spec in ("total:40", "total:64", "total:128"):
         tree = tree_for(case, spec=spec)
-        say(f"[wide] T={tree.T}")
+        say(f"[{name}] T={tree.T}")
         ws = workspace(case, tree.T)
         res = gpu_step(case, tree, ws)
         ref = oracle_step(case, tree)
@@ -237,12 +238,18 @@ def _expected_packing(w, kind):
     rows, cols = w.shape
     kc = -(-(cols // 64) // 4) * 4
     if kind in (ppd.PPD_W_GATE_UP, ppd.PPD_W_QKV):
-        # ns groups of 16 features (gate/up) or 16 QKV rows per tile: 4, or 3
-        # when cols % 512 == 0, every tile stays whole (>= 160 tiles of 4)
-        # and 3-group tiles need fewer groups per CU over 256 CUs
+        # ns groups of 16 features (gate/up) or 16 QKV rows per tile: 4, or
+        # (cols % 512 == 0) 3 when every tile stays whole (>= 160 tiles of 4)
+        # and 3-group tiles need fewer groups per CU over 256 CUs, or (gate/up)
+        # 2 when tiles of 4 are fewer than 160 and tiles of 2 number 160..256
         groups = rows // 32 if kind == ppd.PPD_W_GATE_UP else rows // 16
-        t4, t3 = -(-groups // 4), -(-groups // 3)
-        ns = 3 if cols % 512 == 0 and t4 >= 160 and 3 * -(-t3 // 256) < 4 * -(-t4 // 256) else 4
+        t4, t3, t2 = -(-groups // 4), -(-groups // 3), -(-groups // 2)
+        ns = 4
+        if cols % 512 == 0:
+            if t4 >= 160:
+                ns = 3 if 3 * -(-t3 // 256) < 4 * -(-t4 // 256) else 4
+            elif kind == ppd.PPD_W_GATE_UP and 160 <= t2 <= 256:
+                ns = 2
         n_tiles = -(-groups // ns)
     if kind == ppd.PPD_W_GATE_UP:
         F = rows // 2
@@ -280,7 +287,9 @@ def _expected_packing(w, kind):
                                             (ppd.PPD_W_QKV, 6 * 128, 256),
                                             (ppd.PPD_W_GATE_UP, 2 * 11008, 512),
                                             (ppd.PPD_W_QKV, 96 * 128, 512),
-                                            (ppd.PPD_W_QKV, 96 * 128, 256)])
+                                            (ppd.PPD_W_QKV, 96 * 128, 256),
+                                            (ppd.PPD_W_QKV, 48 * 128, 512),
+                                            (ppd.PPD_W_GATE_UP, 2 * 5632, 512)])
 def test_pack_weight_layout(kind, rows, cols):
     say(f"[pack] kind={kind} {rows}x{cols}")
     g = torch.Generator().manual_seed(rows * 7 + cols)
