@@ -85,6 +85,9 @@ WIDE_BF16 = ModelShape("wide-bf16", 1, 512, 32, 32, 128, 11008, 1000, "bf16")
 # tilings (split QKV; 176 gate/up tiles of 2 feature groups, each group's
 # two k-steps on two waves)
 MID_BF16 = ModelShape("mid-bf16", 1, 512, 16, 16, 128, 5632, 1000, "bf16")
+# grouped-query heads whose QKV groups (80 x 8 = 640) leave the last 3-group
+# QKV tile with one real group
+WIDE_GQA = ModelShape("wide-gqa-bf16", 1, 512, 64, 8, 128, 1344, 1000, "bf16")
 
 WORKLOADS = {
     # 0: tiny fp32 decoder, 128-token prefix from a real prefill, 10-candidate tree
@@ -102,6 +105,7 @@ WORKLOADS = {
     "small-gqa": Workload("small-gqa", SMALL_GQA, 77, "total:29", 4, "normal", 11),
     "wide": Workload("wide", WIDE_BF16, 300, "total:40", 4, "normal", 12),
     "mid": Workload("mid", MID_BF16, 300, "total:40", 4, "normal", 13),
+    "wide-gqa": Workload("wide-gqa", WIDE_GQA, 300, "total:40", 4, "normal", 14),
 }
 
 T13B_SWEEP = (16, 32, 64, 128)

@@ -133,11 +133,12 @@ def test_small_bf16_long_prefix(small_long_case, L, spec):
     _check_tree_kv(case, tree, ref, L=L)
 
 
-@pytest.mark.parametrize("name", ["wide", "mid"])
+@pytest.mark.parametrize("name", ["wide", "mid", "wide-gqa"])
 def test_wide_heads_and_ffn(name):
     """7B- or 1.4B-wide heads and ffn over a narrow hidden size: QKV and
-    gate/up run the 3-group tiles (gate/up's last tile ragged) or the 2-group
-    tiles with one k-step per wave, every output against the oracle."""
+    gate/up run the 3-group tiles (gate/up's last tile ragged; with 64 heads
+    over 8 kv heads the last QKV tile too) or the 2-group tiles with one
+    k-step per wave, every output against the oracle."""
     case = make_case(workload(name))
     for spec in ("total:40", "total:64", "total:128"):
         tree = tree_for(case, spec=spec)
@@ -289,6 +290,7 @@ def _expected_packing(w, kind):
                                             (ppd.PPD_W_QKV, 96 * 128, 512),
                                             (ppd.PPD_W_QKV, 96 * 128, 256),
                                             (ppd.PPD_W_QKV, 48 * 128, 512),
+                                            (ppd.PPD_W_QKV, 80 * 128, 512),
                                             (ppd.PPD_W_GATE_UP, 2 * 5632, 512)])
 def test_pack_weight_layout(kind, rows, cols):
     say(f"[pack] kind={kind} {rows}x{cols}")
