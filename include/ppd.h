@@ -246,12 +246,16 @@ ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids,
  * Commit accepted keys/values (Section 5.3: one cache shared by guessing and
  * verification; prompt-token entries are never committed):
  * cache[L + k] <- cache[L + path[k]] for k < *n_path, every layer and kv head.
- * path, n_path: device (as written by ppd_accept).  L: host value used by the
- * matching ppd_verify_step.  Requires L + max_T <= capacity where max_T bounds
- * *n_path; *n_path is clamped to [0, capacity - L] on the device.
+ * path: device int32[path_len] and n_path: device int32 (as written by
+ * ppd_accept, whose path holds T entries: pass path_len = T).  L: host value
+ * used by the matching ppd_verify_step.  *n_path is read on the device and
+ * clamped to [0, min(path_len, capacity - L)], so a stale or foreign count
+ * never reads past the path or writes past the cache; path entries are
+ * clamped the same way.  1 <= path_len <= PPD_T_MAX, else PPD_EINVAL.
  */
 ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
-                          const int32_t *path, const int32_t *n_path, void *stream);
+                          const int32_t *path, int32_t path_len, const int32_t *n_path,
+                          void *stream);
 
 /*
  * Candidate generation for the next step (Section 3, step (1); Section 3.1;

@@ -219,18 +219,45 @@ def embed(model: Model, ids: Sequence[int]) -> np.ndarray:
 # the verification forward pass (Sections 3 and 4.1)
 
 
+def _matmul(a: np.ndarray, b: np.ndarray, acc: str) -> np.ndarray:
+    """a @ b summed in float64 ("f64") or, for a second, independently
+    rounded computation of the same values, in float32 ("f32": operands and
+    products in float32, as a float32-accumulating matrix unit sums them)."""
+    if acc == "f64":
+        return a @ b
+    if acc == "f32":
+        return (a.astype(np.float32) @ b.astype(np.float32)).astype(np.float64)
+    raise ValueError(acc)
+
+
 def verify_forward(model: Model, k_cache: Sequence[np.ndarray], v_cache: Sequence[np.ndarray],
                    L: int, ids: Sequence[int], parent: Sequence[int],
-                   store: Optional[str]) -> Dict:
+                   store: Optional[str], acc: str = "f64", taps: Sequence[int] = ()) -> Dict:
     """One forward pass over all T tree nodes.
 
     k_cache[l] / v_cache[l]: [n_kv_heads, >=L, d] float64 keys (after RoPE) and
     values of the accepted prefix.  Node i sits at position L + depth[i] and
     attends to cache positions [0, L) and to its tree ancestors and itself.
 
+    acc: "f64" (the oracle) or "f32" -- every matrix product summed in
+    float32 and the residual stream kept in float32, the same values rounded
+    differently; two such computations bound how closely any two correct
+    implementations with the same storage roundings can agree.
+    taps: decoder depths n (1 <= n <= n_layers) at which the final norm and
+    LM head are also applied to the residual stream after n layers, i.e. the
+    logits of the same model cut to its first n layers ("tap_logits").
+
     Returns logits [T, vocab], the tree keys/values per layer
     ([n_kv_heads, T, d], rounded to the storage type) and depth."""
     sh = model.shape
+    mm = lambda a, b: _matmul(a, b, acc)
+    resid = (lambda v: v) if acc == "f64" else (lambda v: round_store(v, "f32"))
+
+    def head(xr):
+        a_, r_ = normed_rows(xr, model.final_norm, sh.rms_eps, store)
+        return r_[:, None] * mm(a_, model.lm_head.T)
+
+    tap_logits = {}
     T = len(ids)
     depth, anc = build_mask(parent)
     pos = L + depth
@@ -242,7 +269,7 @@ def verify_forward(model: Model, k_cache: Sequence[np.ndarray], v_cache: Sequenc
     for l in range(sh.n_layers):
         lay = model.layer(l)
         a, r = normed_rows(x, lay["attn_norm"], sh.rms_eps, store)
-        qkv = r[:, None] * (a @ lay["w_qkv"].T)
+        qkv = r[:, None] * mm(a, lay["w_qkv"].T)
         q = qkv[:, :nh * d].reshape(T, nh, d)
         k = qkv[:, nh * d:(nh + nkv) * d].reshape(T, nkv, d)
         v = qkv[:, (nh + nkv) * d:].reshape(T, nkv, d)
@@ -257,18 +284,22 @@ def verify_forward(model: Model, k_cache: Sequence[np.ndarray], v_cache: Sequenc
         for h in range(nh):
             kh = np.concatenate([k_cache[l][h // grp][:L], kt[h // grp]], axis=0)
             vh = np.concatenate([v_cache[l][h // grp][:L], vt[h // grp]], axis=0)
-            s = (q[:, h, :] @ kh.T) / np.sqrt(d)            # [T, L+T]
+            s = mm(q[:, h, :], kh.T) / np.sqrt(d)           # [T, L+T]
             s[:, L:][~anc] = -np.inf                        # tree part: ancestors only
-            o[:, h, :] = softmax_rows(s) @ vh
+            o[:, h, :] = mm(softmax_rows(s), vh)
         o = round_store(o.reshape(T, nh * d), store)
-        x = x + o @ lay["w_o"].T
+        x = resid(x + mm(o, lay["w_o"].T))
         a, r = normed_rows(x, lay["mlp_norm"], sh.rms_eps, store)
-        gu = r[:, None] * (a @ lay["w_gate_up"].T)
+        gu = r[:, None] * mm(a, lay["w_gate_up"].T)
         act = round_store(silu(gu[:, :sh.ffn]) * gu[:, sh.ffn:], store)
-        x = x + act @ lay["w_down"].T
-    a, r = normed_rows(x, model.final_norm, sh.rms_eps, store)
-    logits = r[:, None] * (a @ model.lm_head.T)
-    return {"logits": logits, "tree_k": tree_k, "tree_v": tree_v, "depth": depth}
+        x = resid(x + mm(act, lay["w_down"].T))
+        if l + 1 in taps and l + 1 < sh.n_layers:
+            tap_logits[l + 1] = head(x)
+    logits = head(x)
+    if sh.n_layers in taps:
+        tap_logits[sh.n_layers] = logits
+    return {"logits": logits, "tree_k": tree_k, "tree_v": tree_v, "depth": depth,
+            "tap_logits": tap_logits}
 
 
 def argmax_first(logits: np.ndarray) -> np.ndarray:

@@ -73,7 +73,7 @@ def lib() -> C.CDLL:
         L.ppd_verify_batch.argtypes = [P(ppd_model), i32, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp,
                                        vp]
         L.ppd_accept.argtypes = [i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
-        L.ppd_kv_compact.argtypes = [P(ppd_model), P(ppd_kv), i32, vp, vp, vp]
+        L.ppd_kv_compact.argtypes = [P(ppd_model), P(ppd_kv), i32, vp, i32, vp, vp]
         L.ppd_device_status.argtypes = [vp, sz, P(C.c_uint32), i32, vp]
         L.ppd_set_kernel_timer.argtypes = [i32, vp, vp, i32]
         L.ppd_last_error.restype = C.c_char_p
@@ -173,6 +173,20 @@ class Model:
             C.cast(a["w_o"], C.POINTER(C.c_void_p)), C.cast(a["mlp_norm"], C.POINTER(C.c_void_p)),
             C.cast(a["w_gate_up"], C.POINTER(C.c_void_p)), C.cast(a["w_down"], C.POINTER(C.c_void_p)),
             _ptr(w["final_norm"]), _ptr(self.lm_head))
+
+
+    def first_layers(self, n: int) -> "Model":
+        """The same model cut to its first n decoder layers (final norm and
+        LM head unchanged), sharing this object's packed weights: no copy."""
+        import copy
+        if not 1 <= n <= self.shape.n_layers:
+            raise ValueError(f"n={n} outside [1, {self.shape.n_layers}]")
+        m = copy.copy(self)
+        m.shape = self.shape.with_layers(n)
+        m.desc = ppd_model.from_buffer_copy(self.desc)
+        m.desc.n_layers = n
+        m._parent = self
+        return m
 
 
 class KVCache:
@@ -312,8 +326,15 @@ def ppd_sparse_template(p_table, n_cand: int, n_prompt: int, n_ept: int = 1):
     return par[:T.value].copy(), kind[:T.value].copy(), float(f.value)
 
 
-def ppd_kv_compact(model: Model, kv: KVCache, L: int, path, n_path, stream=None):
-    _check(lib().ppd_kv_compact(C.byref(model.desc), C.byref(kv.desc), int(L), _ptr(path),
+def ppd_kv_compact(model: Model, kv: KVCache, L: int, path, n_path, stream=None,
+                   path_len: Optional[int] = None):
+    """path: device int32 tensor (its length is passed as path_len unless
+    given); n_path: device int32 count, clamped on the device."""
+    import torch
+    _dev(path, torch.int32, "path")
+    _dev(n_path, torch.int32, "n_path")
+    n = int(path.numel()) if path_len is None else int(path_len)
+    _check(lib().ppd_kv_compact(C.byref(model.desc), C.byref(kv.desc), int(L), _ptr(path), n,
                                 _ptr(n_path), _stream(stream)))
 
 

@@ -230,19 +230,21 @@ hipError_t launch_accept(int T, const int32_t *parent, const int32_t *ids, const
 // KV compaction (Section 5.3: one cache; only accepted tokens are committed):
 // cache[L + k] <- cache[L + path[k]], k < n.  Sources are read into LDS before
 // any destination is written, so overlapping moves are safe.  One block per
-// (layer, kv head).
+// (layer, kv head).  n = *n_path clamped to the path's length and to the
+// cache's room past L, path entries clamped to that room.
 
 template <typename ET>
 __global__ __launch_bounds__(256) void kv_compact_kernel(ET *__restrict__ k, ET *__restrict__ v,
                                                          int cap, int d, int L,
                                                          const int32_t *__restrict__ path,
+                                                         int path_len,
                                                          const int32_t *__restrict__ n_path,
                                                          int32_t *len_dev) {
   __shared__ ET buf[PPD_T_MAX * 128];
   __shared__ int sp[PPD_T_MAX];
   int n = *n_path;
   const int room = min(cap - L, PPD_T_MAX);
-  n = max(0, min(n, room));
+  n = max(0, min(n, min(room, path_len)));
   for (int j = threadIdx.x; j < n; j += blockDim.x) {
     int p = path[j];
     sp[j] = max(0, min(p, room - 1));
@@ -276,15 +278,15 @@ __global__ __launch_bounds__(256) void kv_compact_kernel(ET *__restrict__ k, ET 
 }
 
 hipError_t launch_kv_compact(int dtype, void *k, void *v, int n_layers, int nkv, int cap, int d,
-                             int L, const int32_t *path, const int32_t *n_path, int32_t *len_dev,
-                             hipStream_t s) {
+                             int L, const int32_t *path, int path_len, const int32_t *n_path,
+                             int32_t *len_dev, hipStream_t s) {
   dim3 grid(n_layers * nkv);
   if (dtype == PPD_BF16)
     hipLaunchKernelGGL(kv_compact_kernel<bf16_t>, grid, dim3(256), 0, s, (bf16_t *)k, (bf16_t *)v,
-                       cap, d, L, path, n_path, len_dev);
+                       cap, d, L, path, path_len, n_path, len_dev);
   else
     hipLaunchKernelGGL(kv_compact_kernel<float>, grid, dim3(256), 0, s, (float *)k, (float *)v, cap,
-                       d, L, path, n_path, len_dev);
+                       d, L, path, path_len, n_path, len_dev);
   return hipGetLastError();
 }
 

@@ -584,16 +584,19 @@ ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids, cons
 }
 
 ppd_status ppd_kv_compact(const ppd_model *model, const ppd_kv *kv, int32_t L,
-                          const int32_t *path, const int32_t *n_path, void *stream) {
+                          const int32_t *path, int32_t path_len, const int32_t *n_path,
+                          void *stream) {
   ppd_status st = check_model(model);
   if (st != PPD_OK) return st;
   if ((st = check_kv(model, kv)) != PPD_OK) return st;
   if (L < 0 || L >= kv->capacity)
     return fail(PPD_ECAPACITY, "L=%d must be in [0, capacity=%d)", L, kv->capacity);
   if (!path || !n_path) return fail(PPD_EINVAL, "NULL path");
+  if (path_len < 1 || path_len > PPD_T_MAX)
+    return fail(PPD_EINVAL, "path_len=%d outside [1, %d]", path_len, PPD_T_MAX);
   PPD_TRY_HIP(launch_kv_compact(model->dtype, kv->k, kv->v, model->n_layers, model->n_kv_heads,
-                                kv->capacity, model->head_dim, L, path, n_path, kv->len_dev,
-                                (hipStream_t)stream));
+                                kv->capacity, model->head_dim, L, path, path_len, n_path,
+                                kv->len_dev, (hipStream_t)stream));
   return PPD_OK;
 }
 

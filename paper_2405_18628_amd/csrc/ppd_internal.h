@@ -213,8 +213,8 @@ hipError_t launch_accept(int T, const int32_t *parent, const int32_t *ids, const
                          int vocab, int32_t *path, int32_t *n_path, int32_t *next_tok,
                          uint32_t *status, hipStream_t s);
 hipError_t launch_kv_compact(int dtype, void *k, void *v, int n_layers, int nkv, int cap, int d,
-                             int L, const int32_t *path, const int32_t *n_path, int32_t *len_dev,
-                             hipStream_t s);
+                             int L, const int32_t *path, int path_len, const int32_t *n_path,
+                             int32_t *len_dev, hipStream_t s);
 hipError_t launch_ws_init(void *ws, size_t n_words, hipStream_t s);
 
 // fp32 path (simple kernels for float32 models)

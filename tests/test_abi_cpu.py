@@ -115,8 +115,10 @@ def test_accept_and_compact_reject_before_enqueue():
     assert L.ppd_accept(4, f, f, f, 0, f, f, f, f, 64, None) == ppd.PPD_EINVAL
     assert L.ppd_accept(4, f, f, f, 10, f, f, f, None, 64, None) == ppd.PPD_EWORKSPACE
     kv = ppd.ppd_kv(0x2000, 0x3000, 256, None)
-    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 256, f, f, None) == ppd.PPD_ECAPACITY
-    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 10, None, f, None) == ppd.PPD_EINVAL
+    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 256, f, 4, f, None) == ppd.PPD_ECAPACITY
+    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 10, None, 4, f, None) == ppd.PPD_EINVAL
+    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 10, f, 0, f, None) == ppd.PPD_EINVAL
+    assert L.ppd_kv_compact(C.byref(m), C.byref(kv), 10, f, 129, f, None) == ppd.PPD_EINVAL
     assert L.ppd_workspace_init(None, 0, None) == ppd.PPD_EWORKSPACE
 
 

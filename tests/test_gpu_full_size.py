@@ -74,14 +74,20 @@ def _case(name, n_layers):
     return _CASES[key]
 
 
-@pytest.mark.parametrize("name,spec", [("1.4b", None), ("7b", None), ("13b", "total:16"),
-                                       ("13b", "total:32"), ("13b", "total:64"),
-                                       ("13b", "total:128"), ("7b-32k", None)])
-def test_full_width_sampled_nodes(name, spec):
+@pytest.mark.parametrize("name,spec", [("1.4b", None), ("7b", None), ("7b", "root"),
+                                       ("13b", "total:16"), ("13b", "total:32"),
+                                       ("13b", "total:64"), ("13b", "total:128"),
+                                       ("7b-32k", None)])
+def test_full_width_all_nodes(name, spec):
+    """One decoder layer at the workload's full width: every node's logits,
+    greedy token and tree keys / values against the oracle."""
     case = _case(name, 1)
-    tree = tree_for(case, spec=spec)
-    nodes = sample_nodes(tree, case.shape.vocab)
-    say(f"[full-width] {name} T={tree.T} L={case.L} nodes={nodes}")
+    if spec == "root":
+        tree = Tree(np.array([-1], np.int32), np.array([case.root], np.int32), 1)
+    else:
+        tree = tree_for(case, spec=spec)
+    nodes = list(range(tree.T))
+    say(f"[full-width] {name} T={tree.T} L={case.L} (all nodes)")
     ws = workspace(case, tree.T)
     res = gpu_step(case, tree, ws)
     assert ppd.ppd_device_status(ws) == 0

@@ -9,7 +9,7 @@ import paper_2405_18628_amd as ppd
 from gpu_cases import (check_logits, check_pred, gpu_step, make_case, oracle_step, say,
                        subtree, tree_for, workspace)
 from synth import workload
-from synth.trees import make_tree
+from synth.trees import Tree, make_tree
 
 pytestmark = pytest.mark.gpu
 
@@ -228,6 +228,46 @@ def test_tiny_multistep_lossless(tiny_case):
     assert emitted == ref
     case.k.copy_(k0)
     case.v.copy_(v0)
+
+
+def root_only_tree(case):
+    """T = 1: the root alone, i.e. vanilla one-token decoding (reading c1)."""
+    return Tree(np.array([-1], np.int32), np.array([case.root], np.int32), 1)
+
+
+def vanilla_decode_reference(case, L):
+    """Logits and keys / values of the root decoded alone by the oracle's
+    plain decoder (no tree, no mask) on a copy of the cache."""
+    sh = case.shape
+    kc = [np.zeros((sh.n_kv_heads, L + 1, sh.head_dim)) for _ in range(sh.n_layers)]
+    vc = [np.zeros((sh.n_kv_heads, L + 1, sh.head_dim)) for _ in range(sh.n_layers)]
+    for l in range(sh.n_layers):
+        kc[l][:, :L] = case.kc_host[l][:, :L]
+        vc[l][:, :L] = case.vc_host[l][:, :L]
+    logits = O.decode_token(case.oracle_model, kc, vc, L, case.root, sh.dtype)
+    return logits, [k[:, L] for k in kc], [v[:, L] for v in vc]
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "small-gqa", "wide"])
+def test_root_only_tree_is_vanilla_decode(name, tiny_case, small_case):
+    """A one-node tree is one step of ordinary decoding: its logits, greedy
+    token and cached key / value equal the oracle's plain decoder's."""
+    case = {"tiny": tiny_case, "small": small_case}.get(name) or make_case(workload(name))
+    sh = case.shape
+    tree = root_only_tree(case)
+    say(f"[root-only] {name} L={case.L}")
+    ws = workspace(case, 1)
+    res = gpu_step(case, tree, ws)
+    ref, k_ref, v_ref = vanilla_decode_reference(case, case.L)
+    check_logits(res["logits"], ref[None, :], sh.dtype, "root logits")
+    check_pred(res["pred"], ref[None, :], sh.dtype)
+    L = case.L
+    for l in range(sh.n_layers):
+        check_logits(O.to_f64(case.k[l, :, L, :]), k_ref[l], sh.dtype, f"root K layer {l}")
+        check_logits(O.to_f64(case.v[l, :, :, L]), v_ref[l], sh.dtype, f"root V layer {l}")
+    n = _accept_and_compact(case, tree, res, ws)
+    assert n == 1
+    assert ppd.ppd_device_status(ws) == 0
 
 
 def _expected_packing(w, kind):

@@ -60,6 +60,10 @@ def test_matches_hf_llama_tree_forward():
     hf_logits, pkv = hf_prefill(hf, ids[:-1])
     k_hf = pkv.layers[1].keys[0].numpy()
     v_hf = pkv.layers[1].values[0].numpy()
+    # the prefill's last logits: the oracle's plain decoder (decode_token)
+    # against the library's causal forward
+    _, _, last = O.prefill(m, ids[:-1], L + 8, None)
+    assert np.abs(np.asarray(hf_logits)[-1, :sh.vocab] - last).max() < 2e-5
     assert np.abs(k_hf - kc[1][:, :L]).max() < 1e-5
     assert np.abs(v_hf - vc[1][:, :L]).max() < 1e-5
     for seed in range(3):
@@ -109,6 +113,32 @@ def test_tree_nodes_equal_causal_paths_bf16():
         seq = O.path_tokens(tree.parent, tree.ids, i)
         ref = O.causal_logits(m, kc, vc, L, seq, "bf16")[-1]
         assert np.abs(ref - res["logits"][i]).max() < 1e-9
+
+
+def test_depth_taps_are_the_cut_models(tiny):
+    """tap_logits[n]: the logits of the same model cut to its first n layers
+    (its own forward, run separately)."""
+    sh, W, m, kc, vc, L, root = tiny
+    tree = make_tree("candidates:10", sh.vocab, 3, 4, 4, root)
+    res = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, "f32", taps=(1, 2))
+    W1 = dict(W)
+    W1["layers"] = W["layers"][:1]
+    m1 = O.Model(sh.with_layers(1), W1)
+    cut = O.verify_forward(m1, kc[:1], vc[:1], L, tree.ids, tree.parent, "f32")
+    assert np.array_equal(res["tap_logits"][1], cut["logits"])
+    assert np.array_equal(res["tap_logits"][2], res["logits"])
+
+
+def test_float32_sums_agree_at_float32_precision(tiny):
+    """acc="f32" computes the same values with float32 products and residual:
+    within the float32 tolerance of the float64 sums, and not identical."""
+    sh, W, m, kc, vc, L, root = tiny
+    tree = make_tree("total:25", sh.vocab, 3, 4, 6, root)
+    a = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, "f32")
+    b = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, "f32", acc="f32")
+    err = np.abs(a["logits"] - b["logits"])
+    assert err.max() < 1e-4 * (1 + np.abs(a["logits"]).max())
+    assert err.max() > 0
 
 
 def test_chain_tree_is_multitoken_decode(tiny):
