@@ -77,6 +77,13 @@ typedef enum { PPD_F32 = 0, PPD_BF16 = 1 } ppd_dtype;
 #define PPD_DEV_BAD_TOKEN 1u   /* an id >= vocab + n_prompt was clamped      */
 #define PPD_DEV_BAD_PARENT 2u  /* ppd_accept saw parent[i] outside [0, i)    */
 #define PPD_DEV_NAN_LOGIT 4u   /* a NaN logit was seen by the greedy argmax  */
+#define PPD_DEV_XCD_PLACEMENT 8u /* workgroups that hand partial sums over
+                                    through one XCD's L2 ran on different
+                                    XCDs (the dispatch was not round-robin
+                                    over the 8 XCDs); outputs are invalid    */
+#define PPD_DEV_SYNC_TIMEOUT 16u /* a workgroup gave up waiting for the other
+                                    workgroups of its tile (bounded wait); the
+                                    step's outputs are then invalid          */
 
 /*
  * Llama-style decoder (the paper's MobileLLaMA / Vicuna family): pre-RMSNorm
@@ -113,27 +120,24 @@ typedef struct {
 /*
  * Weight packing for PPD_BF16 models.  The verification step streams every
  * projection weight from HBM once per step (its cost is that stream), so the
- * library keeps them in the order its matrix-core GEMMs consume them: tiles
- * of output rows x 64-column chunks, each chunk a run of 1 KB operand
- * fragments of 16 rows x 32 columns in the lane order of the gfx950 bf16 MFMA
- * instruction.  A tile holds ns groups: 16 QKV rows (dims 8j .. 8j + 7 of a
- * head and their RoPE partners + 64), or 16 gate/up features (their gate rows
- * and up rows), or 32 consecutive rows of the other matrices (ns = 4, 128
- * rows).  ns = 3 for PPD_W_QKV and PPD_W_GATE_UP when cols % 512 == 0, their
- * tiles of 4 groups number at least 160, and tiles of 3 leave fewer groups
- * per compute unit over the 256 CUs of an MI355X (Vicuna-7B shapes: 256 QKV
- * tiles, 230 gate/up tiles); ns = 2 for PPD_W_GATE_UP when cols % 512 == 0,
- * its tiles of 4 groups number fewer than 160 and tiles of 2 number 160 to
- * 256 (MobileLLaMA-1.4B shape: 176 tiles); else ns = 4.
- * Rows and columns past the matrix are zero-filled (e.g. the LM head's last
- * tile when vocab % 128 != 0, the last gate/up tile when ffn % (16 ns) != 0).
- * The packed form depends only on the matrix,
- * not on T or L; pack once at load time.
+ * library keeps them in the order its matrix-core GEMMs consume them,
+ * group-major: a group is 16 output rows -- 16 QKV rows (dims 8j .. 8j + 7
+ * of a head and their RoPE partners + 64), 16 gate/up features (their 16
+ * gate rows, then their 16 up rows), or 16 consecutive rows of the other
+ * matrices -- and group g's 64-column chunks follow one another, each a run
+ * of 1 KB operand fragments of 16 rows x 32 columns in the lane order of the
+ * gfx950 bf16 MFMA instruction: 16-byte item (g, chunk, sub-tile q, k-step s,
+ * lane l) holds row r(g, q, l % 16), columns 64 chunk + 32 s + 8 (l / 16) ..
+ * + 7.  The layout fixes no tiling: how many groups a workgroup streams and
+ * over which columns is chosen per step (from T).  Rows past the matrix
+ * (the LM head's last group when vocab % 16 != 0) are zero.  The packed form
+ * depends only on the matrix, not on T or L; pack once at load time.
  *   kind  which matrix (ppd_weight_kind); rows, cols: its row-major shape,
  *         i.e. PPD_W_QKV [(n_heads + 2 n_kv_heads) 128][hidden],
  *         PPD_W_O [hidden][n_heads 128], PPD_W_GATE_UP [2 ffn][hidden],
  *         PPD_W_DOWN [hidden][ffn], PPD_W_LM_HEAD [vocab][hidden].
  *         cols % 64 == 0; rows % 128 == 0 except for the LM head.
+ *         Size: (rows rounded up to 16) x cols x 2 bytes.
  *   src   device bfloat16 [rows][cols], row-major (not modified)
  *   dst   device buffer of ppd_packed_weight_bytes(kind, rows, cols) bytes,
  *         caller-owned, must not overlap src

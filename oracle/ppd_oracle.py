@@ -22,12 +22,15 @@ The decoder is Llama-style (the paper's MobileLLaMA / Vicuna family):
 pre-RMSNorm, rotary position embedding with rotate-half pairing, multi-head
 (optionally grouped) attention, SwiGLU MLP, tied nothing.
 
-Precision.  Every sum is taken in float64.  With `store="bf16"` (or "f32") the
-oracle rounds to that storage type exactly where the GPU path stores values in
-it: weights and embeddings (already rounded on input), keys/values/queries after
-RoPE, and the input operand of every matrix product (attention output, SwiGLU
-output, and the RMS-normalised activations, see `normed_rows`).  The residual
-stream, softmax and logits are not rounded.
+Precision.  Every sum is taken in float64.  `store` is the storage type of the
+model: its weights and embeddings (already rounded on input) and its KV cache.
+The keys and values a step writes to the cache are rounded to it; the
+activations between matrix products (queries, the normalised operands, the
+attention and SwiGLU outputs) are rounded only for a float32 model, whose GPU
+path stores them in float32 -- a bf16 model's GPU path keeps them in float32
+too and feeds the bf16 matrix cores their two-part (hi + lo) bf16 sum, so they
+are left unrounded here.  The residual stream, softmax and logits are never
+rounded.
 """
 from __future__ import annotations
 
@@ -161,14 +164,19 @@ def rms_scale(x: np.ndarray, eps: float) -> np.ndarray:
     return 1.0 / np.sqrt(np.mean(x * x, axis=-1) + eps)
 
 
-def normed_rows(x: np.ndarray, g: np.ndarray, eps: float, store) -> Tuple[np.ndarray, np.ndarray]:
-    """RMSNorm(x) * g, split as (rounded operand, row scale).
+def round_act(x: np.ndarray, store: Optional[str]) -> np.ndarray:
+    """An activation between matrix products: float32 models store it in
+    float32; bf16 models keep it unrounded (see the module header)."""
+    return round_store(x, "f32") if store == "f32" else x
 
-    RMSNorm(x)_k * g_k = r * (x_k * g_k) with r = 1/sqrt(mean(x^2) + eps).  The
-    GPU stores x*g in the storage type and applies r to each output row of the
-    following matrix product, which is the same product up to rounding; the
-    oracle rounds at the same point.  Returns (round(x*g), r)."""
-    return round_store(x * g, store), rms_scale(x, eps)
+
+def normed_rows(x: np.ndarray, g: np.ndarray, eps: float, store) -> Tuple[np.ndarray, np.ndarray]:
+    """RMSNorm(x) * g, split as (operand, row scale).
+
+    RMSNorm(x)_k * g_k = r * (x_k * g_k) with r = 1/sqrt(mean(x^2) + eps), so
+    (RMSNorm(x) * g) W = r * ((x * g) W) exactly; the operand x * g is
+    rounded as an activation (round_act).  Returns (x * g, r)."""
+    return round_act(x * g, store), rms_scale(x, eps)
 
 
 def rope_tables(pos: np.ndarray, d: int, base: float) -> Tuple[np.ndarray, np.ndarray]:
@@ -273,25 +281,26 @@ def verify_forward(model: Model, k_cache: Sequence[np.ndarray], v_cache: Sequenc
         q = qkv[:, :nh * d].reshape(T, nh, d)
         k = qkv[:, nh * d:(nh + nkv) * d].reshape(T, nkv, d)
         v = qkv[:, (nh + nkv) * d:].reshape(T, nkv, d)
-        q = round_store(apply_rope(q, cos, sin), store)
-        k = round_store(apply_rope(k, cos, sin), store)
+        q = round_act(apply_rope(q, cos, sin), store)
+        k = round_store(apply_rope(k, cos, sin), store)     # the cache's type
         v = round_store(v, store)
         kt = k.transpose(1, 0, 2)                           # [nkv, T, d]
         vt = v.transpose(1, 0, 2)
         tree_k.append(kt)
         tree_v.append(vt)
         o = np.zeros((T, nh, d))
+        kcl, vcl = k_cache[l], v_cache[l]
         for h in range(nh):
-            kh = np.concatenate([k_cache[l][h // grp][:L], kt[h // grp]], axis=0)
-            vh = np.concatenate([v_cache[l][h // grp][:L], vt[h // grp]], axis=0)
+            kh = np.concatenate([kcl[h // grp][:L], kt[h // grp]], axis=0)
+            vh = np.concatenate([vcl[h // grp][:L], vt[h // grp]], axis=0)
             s = mm(q[:, h, :], kh.T) / np.sqrt(d)           # [T, L+T]
             s[:, L:][~anc] = -np.inf                        # tree part: ancestors only
             o[:, h, :] = mm(softmax_rows(s), vh)
-        o = round_store(o.reshape(T, nh * d), store)
+        o = round_act(o.reshape(T, nh * d), store)
         x = resid(x + mm(o, lay["w_o"].T))
         a, r = normed_rows(x, lay["mlp_norm"], sh.rms_eps, store)
         gu = r[:, None] * mm(a, lay["w_gate_up"].T)
-        act = round_store(silu(gu[:, :sh.ffn]) * gu[:, sh.ffn:], store)
+        act = round_act(silu(gu[:, :sh.ffn]) * gu[:, sh.ffn:], store)
         x = resid(x + mm(act, lay["w_down"].T))
         if l + 1 in taps and l + 1 < sh.n_layers:
             tap_logits[l + 1] = head(x)
@@ -375,7 +384,7 @@ def decode_token(model: Model, k_cache: List[np.ndarray], v_cache: List[np.ndarr
         lay = model.layer(l)
         a, r = normed_rows(x, lay["attn_norm"], sh.rms_eps, store)
         qkv = r[:, None] * (a @ lay["w_qkv"].T)
-        q = round_store(apply_rope(qkv[:, :nh * d].reshape(1, nh, d), cos, sin), store)
+        q = round_act(apply_rope(qkv[:, :nh * d].reshape(1, nh, d), cos, sin), store)
         k = round_store(apply_rope(qkv[:, nh * d:(nh + nkv) * d].reshape(1, nkv, d), cos, sin), store)
         v = round_store(qkv[:, (nh + nkv) * d:].reshape(1, nkv, d), store)
         k_cache[l][:, L, :] = k[0]
@@ -387,11 +396,11 @@ def decode_token(model: Model, k_cache: List[np.ndarray], v_cache: List[np.ndarr
             s = kh @ q[0, h] / np.sqrt(d)
             p = np.exp(s - s.max())
             o[h] = (p / p.sum()) @ vh
-        o = round_store(o.reshape(1, nh * d), store)
+        o = round_act(o.reshape(1, nh * d), store)
         x = x + o @ lay["w_o"].T
         a, r = normed_rows(x, lay["mlp_norm"], sh.rms_eps, store)
         gu = r[:, None] * (a @ lay["w_gate_up"].T)
-        act = round_store(silu(gu[:, :sh.ffn]) * gu[:, sh.ffn:], store)
+        act = round_act(silu(gu[:, :sh.ffn]) * gu[:, sh.ffn:], store)
         x = x + act @ lay["w_down"].T
     a, r = normed_rows(x, model.final_norm, sh.rms_eps, store)
     return (r[:, None] * (a @ model.lm_head.T))[0]

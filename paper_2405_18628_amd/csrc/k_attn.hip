@@ -25,7 +25,8 @@
 // Per 32-key block and query tile, on the matrix cores
 // (v_mfma_f32_16x16x32_bf16):
 //   S^T[key][query] = K Q^T      keys are the 16-row A operand (LDS),
-//                                queries the B operand (registers)
+//                                queries the B operand (registers), as two
+//                                bf16 parts (hi, lo) of the fp32 queries
 //   O^T[d][query]  += V^T P^T    values (stored position-minor, so V^T rows
 //                                are contiguous) are the A operand (LDS);
 //                                P^T comes straight from S^T's accumulator
@@ -78,7 +79,7 @@ __device__ __forceinline__ float quad_sum(float v) {
 
 // one wave's state for one 16-query tile
 struct QTile {
-  u32x4 qf[4];   // queries (B operand), dims 32 ds + 8 (lane / 16) .. + 7
+  u32x4 qh[4], ql[4];  // queries (B operand, hi and lo parts), dims 32 ds + 8 (lane / 16) .. + 7
   uint64_t mk0, mk1;
   floatx4 o[8];  // O^T tiles: dims 16 dt + 4 (lane / 16) + e, query lane % 16
   float m_run;   // reference of the exponentials (log2 domain, scaled)
@@ -124,8 +125,19 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
     const int tq = t0 + tl;
     const bool qlive = tl < T;
 #pragma unroll
-    for (int ds = 0; ds < 4; ++ds)
-      qt[i].qf[ds] = *(qlive ? (const u32x4 *)(p.q + ((size_t)tq * p.nh + h) * 128 + ds * 32 + lg * 8) : zp);
+    for (int ds = 0; ds < 4; ++ds) {
+      const floatx4 *src = qlive ? (const floatx4 *)(p.q + ((size_t)tq * p.nh + h) * 128 + ds * 32 + lg * 8)
+                                 : (const floatx4 *)zp;
+      const floatx4 a = src[0], b = src[1];
+      const float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+      float lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) lo[e] = v[e] - bf16_to_f32(f32_to_bf16(v[e]));
+      qt[i].qh[ds] = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                           pack_bf16x2(v[6], v[7])};
+      qt[i].ql[ds] = u32x4{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]), pack_bf16x2(lo[4], lo[5]),
+                           pack_bf16x2(lo[6], lo[7])};
+    }
     qt[i].mk0 = qlive ? p.mask[2 * tq] : 0ull;
     qt[i].mk1 = qlive ? p.mask[2 * tq + 1] : 0ull;
 #pragma unroll
@@ -224,7 +236,8 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
 #pragma unroll
       for (int ds = 0; ds < 4; ++ds) {
         const u32x4 ka = *(const u32x4 *)(ks_l + (kt * 16 + lr) * 256 + (((ds * 4 + lg) ^ lr) * 16));
-        s[kt] = mfma16x16x32(as_bf16x8(ka), as_bf16x8(Q.qf[ds]), s[kt]);
+        s[kt] = mfma16x16x32(as_bf16x8(ka), as_bf16x8(Q.ql[ds]), s[kt]);
+        s[kt] = mfma16x16x32(as_bf16x8(ka), as_bf16x8(Q.qh[ds]), s[kt]);
       }
     }
     // mask and block max: this lane holds keys key0 + 8 lg + 4 kt + e of its
@@ -369,12 +382,9 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
       const size_t t = (size_t)t0 + tl;
       if (KS == 1) {
         const float inv = 1.f / l;
-        bf16_t *dst = p.out + t * p.nh * 128 + h * 128 + lg * 4;
+        float *dst = p.out + t * p.nh * 128 + h * 128 + lg * 4;
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) {
-          const floatx4 v = o[dt] * inv;
-          *(u32x2 *)(dst + dt * 16) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        }
+        for (int dt = 0; dt < 8; ++dt) *(floatx4 *)(dst + dt * 16) = o[dt] * inv;
       } else {
         float *row = p.part + (((size_t)h * p.max_splits + ks) * p.T_pad + t) * OROW;
 #pragma unroll
@@ -430,7 +440,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
     }
   }
   const float inv = 1.f / lsum;
-  *(uint32_t *)(p.out + t * p.nh * 128 + h * 128 + d2) = pack_bf16x2(acc.x * inv, acc.y * inv);
+  *(float2 *)(p.out + t * p.nh * 128 + h * 128 + d2) = make_float2(acc.x * inv, acc.y * inv);
 }
 
 }  // namespace

@@ -1,88 +1,69 @@
-// Skinny-M bfloat16 GEMMs of the verification forward pass, with fused
-// epilogues.  out[row][t] = sum_k W[row][k] * A[t][k] for the T <= 128 tree
-// tokens t, fp32 accumulation on the gfx950 matrix cores
-// (v_mfma_f32_16x16x32_bf16: weight rows are the 16-row A operand, tokens the
-// 16-column B operand).
+// Skinny-M GEMMs of the verification forward pass with fused epilogues.
+// out[row][t] = sum_k W[row][k] * A[t][k] for the T <= 128 tree tokens t, on
+// the gfx950 matrix cores (v_mfma_f32_16x16x32_bf16: weight rows are the
+// 16-row A operand, tokens the 16-column B operand), fp32 accumulation.
 //
-// The step is bound by streaming the weights from HBM once (arithmetic
-// intensity ~T flop/byte, far below the MI355X ridge), so the kernel is built
-// around the weight stream:
-//  * weights are pre-packed (launch_pack_weight) so that every MFMA operand
-//    fragment -- 16 rows x 32 columns, in the lane order the instruction
-//    reads it -- is one contiguous 1 KB; a wave loads its fragments straight
-//    into registers with 16-byte non-temporal loads, PPD_GEMM_RING chunks
-//    ahead, with no LDS on the weight path (weights are not shared between
-//    waves);
-//  * the activations (the same for every workgroup, served from L2) follow
-//    the same register ring and are staged per chunk in a double-buffered,
-//    XOR-swizzled LDS slot read by the four waves;
-//  * a compute unit's load path sustains only ~35 GB/s, so a GEMM needs
-//    (nearly) every CU streaming to approach the HBM rate.  GEMMs with enough
-//    tiles (128 rows; QKV: 64, half a head) run one whole tile per workgroup
-//    and finish it in place (fused epilogue).  The others are cut Stream-K
-//    style: the (tile, chunk) units are split into equal contiguous ranges,
-//    one per compute unit; a workgroup streams across tile boundaries and
-//    stores the partial sums of each tile segment, and a small finish kernel
-//    (one workgroup per tile and 16-token block) adds a tile's partials in
-//    workgroup order and runs the epilogue -- the kernel boundary orders the
-//    two, so no cross-workgroup synchronisation is needed and results never
-//    depend on timing;
-//  * the epilogue: RMSNorm row scale, RoPE + query/key/value stores into the
-//    cache (QKV), residual add + next norm operand + sum of squares (output /
-//    down projection), SwiGLU (gate/up), logits + argmax partials (LM head).
+// Precision.  Weights are bf16.  Activations are kept in fp32 in memory and
+// enter the matrix cores as the sum of two bf16 parts (hi = bf16(a),
+// lo = bf16(a - hi): about 16 significant bits), two products per weight
+// fragment.  A bf16 rounding of every activation between layers would make
+// two correct implementations drift apart layer after layer (each rounding
+// flip is a full bf16 ulp); with the pair the drift stays near fp32 noise at
+// any depth.
+//
+// The step is bound by streaming the weights from HBM once (~T flop per byte
+// at bf16, far below the MI355X ridge), so the kernel is organised around
+// the weight stream and around what else each compute unit must load:
+//  * weights are pre-packed group-major (launch_pack_weight): a group is 16
+//    output rows (gate/up: 16 gate rows and the matching 16 up rows), and
+//    each 64-column chunk of a group is a run of 1 KB fragments in the lane
+//    order of the instruction's A operand; a wave loads them straight into a
+//    register ring with 16-byte non-temporal loads (no LDS on this path);
+//  * the groups are dealt to eight workgroup sets b % 8 (each runs on one
+//    XCD: the dispatcher deals workgroups round-robin over the XCDs) and,
+//    within a set, to TX tiles x s K-slices over its 32 workgroups: a
+//    tall tile over a slice of K keeps the activation bytes each compute unit
+//    must read small next to its weight bytes (a compute unit's load path,
+//    not HBM, is the limit when every workgroup re-reads the whole T x K
+//    activation block);
+//  * the activation chunk (fp32, the same for all of a slice's workgroups,
+//    an L2 hit) is staged per chunk in a double-buffered, XOR-swizzled LDS
+//    slot as the two bf16 parts; norm consumers form RMSNorm's x * gain here
+//    (the row scale is applied to the output rows in the epilogue);
+//  * a tile's s slices finish in the same kernel: each stores its partial
+//    sums (to L2: all of a tile's workgroups share one XCD), arrives at the
+//    tile's counter (an atomic), waits for the others (bounded spin) and
+//    finishes 1/s of the tile's token blocks, adding the partials in slice
+//    order (deterministic);
+//  * epilogues: RMSNorm row scale, RoPE + query / key / value stores into the
+//    cache (QKV), residual add + per-tile sum of squares (output / down
+//    projections), SwiGLU (gate/up), logits + per-tile argmax (LM head).
 #include <algorithm>
 
 #include "ppd_internal.h"
 
 namespace {
 
-constexpr int KC = 64;            // K per chunk: two MFMA k-steps
-constexpr int BN = PPD_GEMM_BN;   // rows of a 128-row tile: 8 sub-tiles of 16
-constexpr int R = PPD_GEMM_RING;  // chunks requested ahead
-constexpr int FRAG = 64;          // u32x4 per packed operand fragment (1 KB)
-// Ring depth of 3- and 2-group whole tiles (needs K % 512 == 0).  Measured at 7B:
-// with 3 of 4 waves streaming weights a 4-chunk ring keeps too few bytes in
-// flight (QKV 30.0, gate/up 40.1 us against 28.9 / 37.5 with 4-group tiles);
-// 8 chunks give 28.1 / 35.9 us.  4-group tiles and split GEMMs are slower
-// with 8 (gate/up 38.5, output / down projection 18.9 / 28.2 against 17.3 /
-// 26.2 us).
-constexpr int kRing3 = 8;
+constexpr int KC = 64;    // K per chunk: two MFMA k-steps
+constexpr int FRAG = 64;  // u32x4 per packed operand fragment (1 KB)
 
-// A tile holds NS row groups, each of SUBS sub-tiles of 16 rows: wave w
-// owns group w, i.e. sub-tiles w (QKV: 16 rows, 8 dims of a head and their
-// RoPE partners) or w and w + NS (SwiGLU: 16 gate rows and the matching 16
-// up rows; others: 16 + 16 consecutive rows).  NS = 4 gives 64-row QKV tiles
-// (half a head), 64 features per gate/up tile and 128-row tiles elsewhere.
-// Whole-tile QKV and gate/up GEMMs may take smaller tiles where that spreads
-// them over more CUs: NS = 3 (waves 0-2 own the groups, wave 3 only stages
-// activations; 7B: 256 QKV tiles instead of 192, 230 gate/up tiles instead
-// of 172) or NS = 2 (waves w and w + 2 share group w, each multiplying one of
-// the two k-steps of every chunk, and add their sums through LDS at the end;
-// 1.4B: 176 whole gate/up tiles instead of a split GEMM).
 template <int KIND>
-constexpr int SUBS = KIND == GEMM_QKV ? 1 : 2;
-// u32x4 per packed (tile, chunk): NS SUBS sub-tiles x 2 k-steps
-template <int KIND, int NS>
-constexpr int UNIT = 2 * NS * SUBS<KIND> * FRAG;
+constexpr int SUB = KIND == GEMM_SWIGLU ? 2 : 1;  // 16-row sub-tiles per group
 
-// weight row of tile row r (0 <= r < 16 NS SUBS); rows >= the matrix's are
-// padding (zero weights, no output)
-template <int KIND, int NS>
-__device__ __forceinline__ int tile_row(int tile, int r, int N) {
-  if constexpr (KIND == GEMM_SWIGLU) {
-    // 16 NS features: gate rows f0 .. f0 + 16 NS - 1, then the matching up rows
-    constexpr int FT = 16 * NS;
-    const int f = tile * FT + (r < FT ? r : r - FT);
-    return f >= N ? 2 * N : r < FT ? f : N + f;  // features past F: padding
-  } else if constexpr (KIND == GEMM_QKV) {
-    // global sub-tile gs: sub-tile gs % 8 of head part gs / 8; its rows 0..7
-    // are dims 8 (gs % 8) .. + 7, rows 8..15 their RoPE partners 64 + those
-    // dims, so a pair lies in lanes l and l + 32 of the accumulator
-    const int gs = tile * NS + (r >> 4), rr = r & 15;
-    return (gs >> 3) * 128 + (rr < 8 ? 0 : 64) + 8 * (gs & 7) + (rr & 7);
-  } else {
-    return tile * BN + r;  // consecutive rows
-  }
+// buffer resource over a whole workspace region (raw, untyped loads)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte load that misses L1 (sc0): data written by another compute unit of
+// this XCD is read from the shared L2
+__device__ __forceinline__ floatx4 load_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 1));
+}
+
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 0xf;
 }
 
 __device__ __forceinline__ void amax_merge(float &v, int &i, float v2, int i2) {
@@ -93,17 +74,33 @@ __device__ __forceinline__ void amax_merge(float &v, int &i, float v2, int i2) {
 }
 
 // 16-byte column swizzle of a 128-byte LDS row: logical column c of row r is
-// stored at physical column c ^ ((r >> 1) & 7).  Sixteen consecutive rows
-// read at one logical column then cover all 64 banks exactly once.
+// stored at physical column c ^ ((r >> 1) & 7); sixteen consecutive rows read
+// at one logical column cover all banks once.
 __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
+// weight row held by row r (< 16) of sub-tile q of group grp; rows past the
+// matrix are padding (zero weights, no output)
+template <int KIND>
+__device__ __forceinline__ int group_row(int grp, int q, int r, int N) {
+  if constexpr (KIND == GEMM_SWIGLU) {
+    const int f = grp * 16 + r;  // feature
+    return f >= N ? 2 * N : q == 0 ? f : N + f;
+  } else if constexpr (KIND == GEMM_QKV) {
+    // group gs: dims 8 (gs % 8) .. + 7 of head part gs / 8 in rows 0..7 and
+    // their RoPE partners (+ 64) in rows 8..15, so a pair lies in lanes l
+    // and l + 32 of the accumulator
+    return (grp >> 3) * 128 + (r < 8 ? 0 : 64) + 8 * (grp & 7) + (r & 7);
+  } else {
+    return grp * 16 + r;
+  }
+}
+
 // ---- RMSNorm row scale r[t] = 1/sqrt(mean(x^2) + eps) of tokens
-// tok0 .. tok0 + NT - 1 from the producer's sum-of-squares partials
-// ss[p][T_pad]: two threads per token, thread j adding partials j, j + 2,
-// j + 4, ... in order (the first 16 requested by rs_request, so that a caller
-// can overlap their latency), then the two sums are added.  The order is the
-// same whatever NT, so a token's scale does not depend on the other tokens
-// of the step (a batched step gives each sequence its own step's bits).
+// tok0 .. tok0 + NT - 1 from the producer's per-tile sums of squares
+// ss[p][T_pad]: two threads per token, thread j adding partials j, j + 2, ...
+// in order, then the two sums are added -- the same order whatever NT or the
+// other tokens of the step (a batched step gives each sequence its own
+// step's bits).
 template <int NT>
 __device__ __forceinline__ void rs_request(const GemmLaunch &g, int tok0, float (&ssv)[16]) {
   static_assert(2 * NT <= 256, "two threads per token");
@@ -135,97 +132,61 @@ __device__ __forceinline__ void rs_finish(const GemmLaunch &g, int tok0, const f
   if (tid < NT) rs_s[tok0 + tid] = rsqrtf((gs[tid] + gs[NT + tid]) * g.inv_h + g.eps);
 }
 
-// ---- epilogue operands
-template <int KIND, int MTE>
-struct EpiOperands {
-  floatx4 rope[MTE][2];  // QKV: (cos, sin) of dims i0..i0+3 for each token tile
-  floatx4 x[2][MTE];     // RESID: residual stream of the lane's rows
-  uint2 gain[2];         // RESID: next norm gain of the lane's rows
-};
-
-template <int KIND, int MTE, int NS = 4>
-__device__ __forceinline__ void epi_request(const GemmLaunch &g, int t, int mt0,
-                                            EpiOperands<KIND, MTE> &o) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int lr = lane & 15, r4 = (lane >> 4) * 4;
-  if constexpr (KIND == GEMM_QKV) {
-    // pair indices 8 (gs % 8) + 4 (lane / 16 % 2) + e, e < 4, of the wave's
-    // global sub-tile gs (waves >= NS read a valid pair and do not use it)
-    const int i0 = 8 * ((t * NS + wave) & 7) + 4 * ((lane >> 4) & 1);
-#pragma unroll
-    for (int mt = 0; mt < MTE; ++mt) {
-      const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)((mt0 + mt) * 16 + lr) * 64 + i0);
-      o.rope[mt][0] = rp[0];
-      o.rope[mt][1] = rp[1];
-    }
-  } else if constexpr (KIND == GEMM_RESID) {
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int n = t * BN + (wave + 4 * q) * 16 + r4;
-      o.gain[q] = *(const uint2 *)(g.gain + n);
-#pragma unroll
-      for (int mt = 0; mt < MTE; ++mt)
-        o.x[q][mt] = *(const floatx4 *)(g.x + (size_t)((mt0 + mt) * 16 + lr) * g.N + n);
-    }
-  }
-}
-
-// Epilogue of tile t for token tiles mt0 .. mt0 + MTE - 1 from the complete
-// sums in acc.  Accumulator layout: the lane holds rows 4 (lane / 16) + e of
-// sub-tiles wave (and wave + 4), token (mt0 + mt) 16 + lane % 16.  Called by
-// all 256 threads (it has barriers); rs_s holds the row scales by token.
-template <int KIND, int MTE, int NS = 4>
-__device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
-                                         const floatx4 (&acc)[SUBS<KIND>][MTE],
-                                         const EpiOperands<KIND, MTE> &o, const float *rs_s,
-                                         float (*red_s)[128][2]) {
+// ---- epilogue of token block mt of tile gt (groups [ga, gb)), from the
+// complete sums a[i][q]: the lane holds rows 4 (lane / 16) + e of sub-tile q
+// of its wave's group i (group ga + wave + 4 i), token mt 16 + lane % 16.
+// Called by all threads (it has barriers); rs_s holds the row scales.
+template <int KIND, int GW>
+__device__ __forceinline__ void epilogue(const GemmLaunch &g, int gt, int ga, int gb, int mt,
+                                         const floatx4 (&a)[GW][SUB<KIND>], const float *rs_s,
+                                         float (*red_s)[128][2], unsigned gmask = ~0u) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, r4 = (lane >> 4) * 4;
   const int T = g.T, T_pad = g.MT * 16;
+  const int tk = mt * 16 + lr;
   if constexpr (KIND == GEMM_QKV) {
-    const int gs = t * NS + wave;   // the wave's global sub-tile
     const int nh = g.nh, nkv = g.nkv;
-    if (wave >= NS || gs >= (nh + 2 * nkv) * 8) return;  // no rows (no barriers below)
-    const int hp = gs >> 3;         // head part: q heads, then k, then v
-    const bool upper = lane >= 32;  // rows 8..15: the partner dims (+64)
-    const int i0 = 8 * (gs & 7) + 4 * ((lane >> 4) & 1);
-    const int d0 = i0 + (upper ? 64 : 0);  // this lane's dims d0 .. d0 + 3
+    const bool upper = lane >= 32;  // rows 8..15: the RoPE partner dims (+64)
+    // this token's sequence: its cache and the position L + local index
+    bf16_t *kc = g.sb.k[0], *vc = g.sb.v[0];
+    int cap = g.sb.cap[0], pos = g.sb.L[0] + tk;
+    for (int j = 1; j < g.sb.B; ++j)
+      if (tk >= g.sb.t0[j]) {
+        kc = g.sb.k[j];
+        vc = g.sb.v[j];
+        cap = g.sb.cap[j];
+        pos = g.sb.L[j] + tk - g.sb.t0[j];
+      }
+    const float rs = rs_s[tk];  // finite for padding tokens too
 #pragma unroll
-    for (int mt = 0; mt < MTE; ++mt) {
-      // padding tokens have a finite row scale too: the pair exchange below
-      // runs on all lanes (lanes l and l + 32 hold the same token)
-      const int tk = (mt0 + mt) * 16 + lr;
-      const float rs = rs_s[tk];
+    for (int i = 0; i < GW; ++i) {
+      const int gs = ga + wave + 4 * i;  // uniform in the wave
+      if (!((gmask >> i) & 1u) || gs >= gb || gs >= (nh + 2 * nkv) * 8) continue;
+      const int hp = gs >> 3;  // head part: q heads, then k, then v
+      const int i0 = 8 * (gs & 7) + 4 * ((lane >> 4) & 1);
+      const int d0 = i0 + (upper ? 64 : 0);  // this lane's dims d0 .. d0 + 3
       float v[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = acc[0][mt][e] * rs;
+      for (int e = 0; e < 4; ++e) v[e] = a[i][0][e] * rs;
       if (hp < nh + nkv) {
-        const float cs[8] = {o.rope[mt][0][0], o.rope[mt][0][1], o.rope[mt][0][2], o.rope[mt][0][3],
-                             o.rope[mt][1][0], o.rope[mt][1][1], o.rope[mt][1][2], o.rope[mt][1][3]};
+        const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)tk * 64 + i0);
+        const floatx4 c0 = rp[0], c1 = rp[1];  // (cos, sin) of dims i0 .. i0 + 3
+        const float cs[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           // [0]: lane l % 32's value (dim i), [1]: lane l % 32 + 32's (dim i + 64)
           const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[e]), __float_as_uint(v[e]),
                                                            false, false);
-          const float a = __uint_as_float(pr[0]), b = __uint_as_float(pr[1]);
+          const float x0 = __uint_as_float(pr[0]), x1 = __uint_as_float(pr[1]);
           const float c = cs[2 * e], sn = cs[2 * e + 1];
-          v[e] = upper ? b * c + a * sn : a * c - b * sn;
+          v[e] = upper ? x1 * c + x0 * sn : x0 * c - x1 * sn;
         }
       }
       if (tk >= T) continue;
-      // this token's sequence: its cache and the position L + local index
-      bf16_t *kc = g.sb.k[0], *vc = g.sb.v[0];
-      int cap = g.sb.cap[0], pos = g.sb.L[0] + tk;
-      for (int j = 1; j < g.sb.B; ++j)
-        if (tk >= g.sb.t0[j]) {
-          kc = g.sb.k[j];
-          vc = g.sb.v[j];
-          cap = g.sb.cap[j];
-          pos = g.sb.L[j] + tk - g.sb.t0[j];
-        }
-      if (hp < nh + nkv) {
-        bf16_t *dst = hp < nh ? g.q + ((size_t)tk * nh + hp) * 128
-                              : kc + ((size_t)(hp - nh) * cap + pos) * 128;
+      if (hp < nh) {
+        *(floatx4 *)(g.q + ((size_t)tk * nh + hp) * 128 + d0) = floatx4{v[0], v[1], v[2], v[3]};
+      } else if (hp < nh + nkv) {
+        bf16_t *dst = kc + ((size_t)(hp - nh) * cap + pos) * 128;
         *(u32x2 *)(dst + d0) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
       } else {
         bf16_t *vb = vc + (size_t)(hp - nh - nkv) * 128 * cap + pos;
@@ -234,479 +195,495 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int t, int mt0,
       }
     }
   } else if constexpr (KIND == GEMM_SWIGLU) {
-    const int f0 = t * 16 * NS + wave * 16 + r4;
-    if (wave >= NS || f0 >= g.N) return;  // no features (no barriers below)
-#pragma unroll
-    for (int mt = 0; mt < MTE; ++mt) {
-      const int tk = (mt0 + mt) * 16 + lr;
-      if (tk >= T) continue;
+    if (tk < T) {
       const float rs = rs_s[tk];
-      float a[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float gt = acc[0][mt][e] * rs, up = acc[1][mt][e] * rs;
-        a[e] = gt / (1.f + expf(-gt)) * up;
+      for (int i = 0; i < GW; ++i) {
+        const int grp = ga + wave + 4 * i;
+        const int f0 = grp * 16 + r4;
+        if (!((gmask >> i) & 1u) || grp >= gb || f0 >= g.N) continue;
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float gt_ = a[i][0][e] * rs, up = a[i][1][e] * rs;
+          o[e] = gt_ / (1.f + expf(-gt_)) * up;
+        }
+        *(floatx4 *)(g.act + (size_t)tk * g.N + f0) = floatx4{o[0], o[1], o[2], o[3]};
       }
-      *(u32x2 *)(g.act + (size_t)tk * g.N + f0) =
-          u32x2{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3])};
     }
   } else if constexpr (KIND == GEMM_RESID) {
+    float sq = 0.f;
+    if (tk < T) {
 #pragma unroll
-    for (int mt = 0; mt < MTE; ++mt) {
-      const int tk = (mt0 + mt) * 16 + lr;
-      float sq = 0.f;
-      if (tk < T) {
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const int n = t * BN + (wave + 4 * q) * 16 + r4;
-          const uint2 gw = o.gain[q];
-          const float g0 = bf16_to_f32(gw.x & 0xffff), g1 = bf16_to_f32(gw.x >> 16);
-          const float g2 = bf16_to_f32(gw.y & 0xffff), g3 = bf16_to_f32(gw.y >> 16);
-          floatx4 xv = o.x[q][mt];
-          xv += acc[q][mt];
-          *(floatx4 *)(g.x + (size_t)tk * g.N + n) = xv;
-          *(u32x2 *)(g.xg + (size_t)tk * g.N + n) =
-              u32x2{pack_bf16x2(xv[0] * g0, xv[1] * g1), pack_bf16x2(xv[2] * g2, xv[3] * g3)};
-          sq += (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
-        }
+      for (int i = 0; i < GW; ++i) {
+        const int grp = ga + wave + 4 * i;
+        const int n = grp * 16 + r4;
+        if (grp >= gb || n >= g.N) continue;
+        floatx4 xv = *(const floatx4 *)(g.x + (size_t)tk * g.N + n);
+        xv += a[i][0];
+        *(floatx4 *)(g.x + (size_t)tk * g.N + n) = xv;
+        sq += (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
       }
-      // sum over the 4 lane groups (rows) of this wave
-      sq += __shfl_xor(sq, 16, 64);
-      sq += __shfl_xor(sq, 32, 64);
-      if (lane < 16) red_s[wave][tk][0] = sq;
+    }
+    // sum over the 4 lane groups (rows) of this wave, then over the waves
+    sq += __shfl_xor(sq, 16, 64);
+    sq += __shfl_xor(sq, 32, 64);
+    if (lane < 16) red_s[wave][lane][0] = sq;
+    __syncthreads();
+    if (tid < 16) {
+      const int tok = mt * 16 + tid;
+      const float v = tok < T ? ((red_s[0][tid][0] + red_s[1][tid][0]) + (red_s[2][tid][0] + red_s[3][tid][0]))
+                              : 0.f;
+      g.ss_out[(size_t)gt * T_pad + tok] = v;
     }
     __syncthreads();
-    if (tid < MTE * 16) {
-      const int tk = mt0 * 16 + tid;
-      const float v = tk < T ? ((red_s[0][tk][0] + red_s[1][tk][0]) + (red_s[2][tk][0] + red_s[3][tk][0]))
-                             : 0.f;
-      g.ss_out[(size_t)t * T_pad + tk] = v;
-    }
   } else {  // GEMM_LOGITS
+    const float rs = tk < T ? rs_s[tk] : 0.f;
+    float bv = 0.f;
+    int bi = -1;
 #pragma unroll
-    for (int mt = 0; mt < MTE; ++mt) {
-      const int tk = (mt0 + mt) * 16 + lr;
-      const float rs = tk < T ? rs_s[tk] : 0.f;
-      float bv = 0.f;
-      int bi = -1;
+    for (int i = 0; i < GW; ++i) {
+      const int grp = ga + wave + 4 * i;
+      const int n = grp * 16 + r4;
+      if (grp >= gb || tk >= T) continue;
+      float v[4];
 #pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const int n = t * BN + (wave + 4 * q) * 16 + r4;
-        float v[4];
+      for (int e = 0; e < 4; ++e) v[e] = a[i][0][e] * rs;
+      if (g.logits) {
+        if ((g.N & 3) == 0 && n + 3 < g.N) {
+          *(floatx4 *)(g.logits + (size_t)tk * g.N + n) = floatx4{v[0], v[1], v[2], v[3]};
+        } else {
+          for (int e = 0; e < 4; ++e)
+            if (n + e < g.N) g.logits[(size_t)tk * g.N + n + e] = v[e];
+        }
+      }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[q][mt][e] * rs;
-        if (tk < T) {
-          if (g.logits) {
-            if ((g.N & 3) == 0 && n + 3 < g.N) {
-              *(floatx4 *)(g.logits + (size_t)tk * g.N + n) = floatx4{v[0], v[1], v[2], v[3]};
-            } else {
-              for (int e = 0; e < 4; ++e)
-                if (n + e < g.N) g.logits[(size_t)tk * g.N + n + e] = v[e];
-            }
-          }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (n + e < g.N) {
-              if (v[e] != v[e]) {
-                atomicOr(g.status, PPD_DEV_NAN_LOGIT);
-              } else if (bi < 0 || v[e] > bv) {
-                bv = v[e];
-                bi = n + e;
-              }
-            }
+      for (int e = 0; e < 4; ++e) {
+        if (n + e < g.N) {
+          if (v[e] != v[e]) {
+            atomicOr(g.status, PPD_DEV_NAN_LOGIT);
+          } else if (bi < 0 || v[e] > bv) {
+            bv = v[e];
+            bi = n + e;
           }
         }
       }
-      // merge over the 4 lane groups: larger value, then smaller index
+    }
+    // merge over the 4 lane groups: larger value, then smaller index
 #pragma unroll
-      for (int off = 16; off <= 32; off <<= 1) {
-        const float v2 = __shfl_xor(bv, off, 64);
-        const int i2 = __shfl_xor(bi, off, 64);
-        amax_merge(bv, bi, v2, i2);
-      }
-      if (lane < 16) {
-        red_s[wave][tk][0] = bv;
-        red_s[wave][tk][1] = __int_as_float(bi);
-      }
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float v2 = __shfl_xor(bv, off, 64);
+      const int i2 = __shfl_xor(bi, off, 64);
+      amax_merge(bv, bi, v2, i2);
+    }
+    if (lane < 16) {
+      red_s[wave][lane][0] = bv;
+      red_s[wave][lane][1] = __int_as_float(bi);
     }
     __syncthreads();
-    if (tid < MTE * 16) {
-      const int tk = mt0 * 16 + tid;
-      float v = red_s[0][tk][0];
-      int i = __float_as_int(red_s[0][tk][1]);
-      for (int w = 1; w < 4; ++w) amax_merge(v, i, red_s[w][tk][0], __float_as_int(red_s[w][tk][1]));
-      g.amax[(size_t)t * T_pad + tk] = make_float2(v, __int_as_float(i));
+    if (tid < 16) {
+      float v = red_s[0][tid][0];
+      int i = __float_as_int(red_s[0][tid][1]);
+      for (int w = 1; w < 4; ++w) amax_merge(v, i, red_s[w][tid][0], __float_as_int(red_s[w][tid][1]));
+      g.amax[(size_t)gt * T_pad + mt * 16 + tid] = make_float2(v, __int_as_float(i));
     }
+    __syncthreads();
   }
 }
 
-// partial sums of tile t by its contributor `slot`: [8 sub-tile pairs x MT][64
-// lanes] floatx4, sub-tile pair index (wave 2 + q) MT + mt
-__device__ __forceinline__ floatx4 *partial_of(const GemmLaunch &g, int t, int slot) {
-  return (floatx4 *)g.part + ((size_t)t * g.maxc + slot) * (size_t)(8 * g.MT * 64);
+// tile gt of an XCD holding no group: the outputs other kernels sum over
+// every tile are written neutral (sum of squares 0, no argmax candidate)
+template <int KIND>
+__device__ __forceinline__ void empty_tile(const GemmLaunch &g, int gt) {
+  const int T_pad = g.MT * 16;
+  for (int tk = threadIdx.x; tk < T_pad; tk += blockDim.x) {
+    if constexpr (KIND == GEMM_RESID) g.ss_out[(size_t)gt * T_pad + tk] = 0.f;
+    if constexpr (KIND == GEMM_LOGITS) g.amax[(size_t)gt * T_pad + tk] = make_float2(0.f, __int_as_float(-1));
+  }
 }
 
-// ---- the GEMM.  Workgroup w of G owns the units [u0, u1) (see
-// PPD_GEMM_RING); SPLIT: store the partial of every tile segment, else every
-// segment is a whole tile and is finished in place.
-template <int MT, int KIND, bool SPLIT, int NS, int RING>
+// ---- the GEMM.  Workgroup b: XCD x = b % 8, slot j = b / 8 -> tile
+// t = j / s (groups [ga, gb) of the XCD's range), K slice ks = j % s (chunks
+// [c0, c1)).  Wave w owns groups ga + w + 4 i, i < GW.  RING: weight chunks
+// requested ahead.
+template <int MT, int KIND, int GW, int RING>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
-  static_assert(NS == 4 || (!SPLIT && (KIND == GEMM_QKV || KIND == GEMM_SWIGLU)),
-                "3- and 2-group tiles: whole-tile QKV and gate/up only");
-  static_assert(RING == R || (!SPLIT && RING % R == 0), "whole tiles only take a deeper ring");
+  // activation chunks requested ahead (L2 hits, but ~1 us away under the
+  // weight stream): 4, or 2 where 4 chunks of MT tiles would not fit the
+  // registers
+  constexpr int RA = MT <= 4 ? 4 : 2;
   constexpr int T_pad = MT * 16;
-  constexpr int NAP = (T_pad * 8 + 255) / 256;  // 16-byte activation pieces per thread per chunk
-  __shared__ __attribute__((aligned(16))) unsigned char lds_a[2][T_pad * 128];
+  constexpr int S = SUB<KIND>;
+  constexpr int PLANE = T_pad * 128;          // bytes of one bf16 plane of a chunk
+  constexpr bool kNorm = KIND != GEMM_RESID;  // A operand = x * gain, rows scaled in the epilogue
+  constexpr int UNR = RING > RA ? RING : RA;  // chunks per unrolled trip (both rings wrap)
+  static_assert(UNR % RING == 0 && UNR % RA == 0 && UNR % 2 == 0, "ring depths");
+  __shared__ __attribute__((aligned(16))) unsigned char lds_a[2][2 * PLANE];
   __shared__ float rs_s[128];
   __shared__ float red_s[4][128][2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 15;  // MFMA row (weights) / column (tokens) within a 16-tile
-  const int lg = lane >> 4;  // this lane's 16-byte k group within a 32-step
-  // NS = 3: wave 3 owns no rows (it stages activations, skips the weights);
-  // NS = 2: wave w multiplies k-step w / 2 of group w % 2
-  const bool owns = NS != 3 || __builtin_amdgcn_readfirstlane(wave) < NS;
-  const int kst = __builtin_amdgcn_readfirstlane(wave >> 1);  // NS = 2: this wave's k-step
-  const int K = g.K, kc = g.kc_pad, G = g.G;
-  const long Ng = (long)g.n_tiles * kc / RING;
-  // this workgroup's units [u0, u1) (uniform: kept in scalar registers)
-  const int u0 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x) * RING);
-  const int u1 = __builtin_amdgcn_readfirstlane((int)gemm_group_lo(Ng, G, blockIdx.x + 1) * RING);
+  const int lr = lane & 15, lg = lane >> 4;
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int s = g.s;
+  const int t = __builtin_amdgcn_readfirstlane(j / s), ks = __builtin_amdgcn_readfirstlane(j % s);
+  const int gt = x * g.TX + t;  // global tile index (sum-of-squares / argmax partial rows)
+  const int nx = g.xg0[x + 1] - g.xg0[x];
+  const int ga = __builtin_amdgcn_readfirstlane(g.xg0[x] + nx * t / g.TX);
+  const int gb = __builtin_amdgcn_readfirstlane(g.xg0[x] + nx * (t + 1) / g.TX);
+  const int K = g.K, kc = g.kc;
+  const int c0 = __builtin_amdgcn_readfirstlane(kc * ks / s);
+  const int c1 = __builtin_amdgcn_readfirstlane(kc * (ks + 1) / s);
+  if (ga >= gb) {  // no groups on this tile
+    if (ks == 0) empty_tile<KIND>(g, gt);
+    return;
+  }
+  // groups of this wave that exist (uniform in the wave)
+  const int live = __builtin_amdgcn_readfirstlane(min(GW, max(0, (gb - ga - wave + 3) / 4)));
 
-  // norm row scales, requested before the weight stream starts
-  constexpr bool kScale = !SPLIT && KIND != GEMM_RESID;
   [[maybe_unused]] float ssv[16];
-  if constexpr (kScale) rs_request<T_pad>(g, 0, ssv);
+  if constexpr (kNorm) rs_request<T_pad>(g, 0, ssv);
 
-  // ---- register rings.  Unit u's weight fragments for this wave: sub-tiles
-  // wave (and wave + NS), k-steps 0 and 1.  Its activation pieces: 16-byte piece
-  // e = tid + 256 i of the [T_pad][64] chunk (row e / 8, column e % 8).
-  // Requests past the range read one 16-byte line (lane offsets masked to 0),
+  // ---- register rings.  Weight chunk c of this wave: fragments (group i,
+  // sub-tile q, k-step s) for i < GW.  Past the slice, and for groups the
+  // wave does not own, every lane reads the tile's first 16 bytes (one line),
   // so every iteration issues the same loads.
-  constexpr int S = SUBS<KIND>;
   const u32x4 *wp = (const u32x4 *)g.W;
-  u32x4 wr[RING][2 * S], ar[RING][NAP];
-  auto request_w = [&](int u, u32x4(&dw)[2 * S]) {
-    if (!owns) return;
-    const int live = u < u1 ? 63 : 0;
-    const int uu = u < u1 ? u : u1 - 1;
-    const u32x4 *wu = wp + (size_t)uu * UNIT<KIND, NS> + (lane & live);
-    if constexpr (NS == 2) {
-      // group wave % 2, k-step kst only (held in slot q * 2)
+  u32x4 wr[RING][GW * S * 2];
+  auto request_w = [&](int c, u32x4(&dw)[GW * S * 2]) {
+    const bool cin = c < c1;
 #pragma unroll
-      for (int q = 0; q < S; ++q)
-        dw[q * 2] = __builtin_nontemporal_load(wu + (((wave & 1) + 2 * q) * 2 + kst) * FRAG);
-    } else {
+    for (int i = 0; i < GW; ++i) {
+      const bool use = cin && i < live;
+      const int grp = use ? ga + wave + 4 * i : ga;
+      const int cc = use ? c : c0;
+      const u32x4 *gp = wp + (((size_t)grp * kc + cc) * S) * 2 * FRAG + (use ? lane : 0);
 #pragma unroll
       for (int q = 0; q < S; ++q)
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
-          dw[q * 2 + s] = __builtin_nontemporal_load(wu + ((wave + NS * q) * 2 + s) * FRAG);
+        for (int st = 0; st < 2; ++st)
+          dw[(i * S + q) * 2 + st] = __builtin_nontemporal_load(gp + (q * 2 + st) * FRAG);
     }
   };
-  // per-lane element offsets of the activation pieces within a chunk;
-  // pieces e >= T_pad * 8 (odd MT) load row 0 and are not staged
-  int aoff[NAP];
+  // activation pieces of a chunk: thread tid loads 16 bytes (4 columns
+  // 4 (tid % 16) ..) of rows tid / 16 + 16 r, r < MT; norm kinds also the 4
+  // gains of those columns
+  const int acol = (tid & 15) * 4, arow = tid >> 4;
+  u32x4 ar[RA][MT];
+  [[maybe_unused]] uint2 agn[RA];
+  auto request_a = [&](int c, u32x4(&da)[MT], uint2 &gn) {
+    const bool cin = c < c1;
+    const int k0 = (cin ? c : c0) * KC + acol;
 #pragma unroll
-  for (int i = 0; i < NAP; ++i) {
-    int e = tid + 256 * i;
-    if constexpr (T_pad * 8 % 256 != 0) e = e < T_pad * 8 ? e : 0;
-    aoff[i] = (e >> 3) * K + (e & 7) * 8;
-  }
-  // u: unit to request; cu: its chunk within its tile
-  auto request_a = [&](int u, int cu, u32x4(&da)[NAP]) {
-    const int k0 = cu * KC;
-    const bool kin = k0 < K;  // padding chunks read zeros
-    const bf16_t *base = kin ? g.A + k0 : g.zeros;
-    // past the range and in padding chunks every lane reads the base line.
-    // The mask is opaque to the compiler, so that it issues the same loads
-    // on every path instead of branching on it.
-    int keep = __builtin_amdgcn_readfirstlane((u < u1 && kin) ? -1 : 0);
-    asm volatile("" : "+s"(keep));
-#pragma unroll
-    for (int i = 0; i < NAP; ++i) da[i] = *(const u32x4 *)(base + (aoff[i] & keep));
+    for (int r = 0; r < MT; ++r) da[r] = *(const u32x4 *)(g.A + (size_t)(arow + 16 * r) * K + k0);
+    if constexpr (kNorm) gn = *(const uint2 *)(g.gain + k0);
   };
-  auto stage = [&](const u32x4(&da)[NAP], int slot) {
+  // stage as the two bf16 parts: plane 0 = hi, plane 1 = lo
+  auto stage = [&](const u32x4(&da)[MT], const uint2 &gn, int slot) {
+    float gv[4] = {1.f, 1.f, 1.f, 1.f};
+    if constexpr (kNorm) {
+      gv[0] = bf16_to_f32(gn.x & 0xffff);
+      gv[1] = bf16_to_f32(gn.x >> 16);
+      gv[2] = bf16_to_f32(gn.y & 0xffff);
+      gv[3] = bf16_to_f32(gn.y >> 16);
+    }
 #pragma unroll
-    for (int i = 0; i < NAP; ++i) {
-      const int e = tid + 256 * i;
-      if (T_pad * 8 % 256 == 0 || e < T_pad * 8) {
-        const int r = e >> 3, c = e & 7;
-        *(u32x4 *)(&lds_a[slot][r * 128 + swz(r, c) * 16]) = da[i];
+    for (int r = 0; r < MT; ++r) {
+      const int row = arow + 16 * r;
+      float v[4], lo[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[e] = __uint_as_float(da[r][e]) * gv[e];
+        lo[e] = v[e] - bf16_to_f32(f32_to_bf16(v[e]));
       }
+      const int off = row * 128 + swz(row, acol >> 3) * 16 + (acol & 7) * 2;
+      *(uint2 *)(&lds_a[slot][off]) = uint2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+      *(uint2 *)(&lds_a[slot][PLANE + off]) = uint2{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3])};
     }
   };
 
-  floatx4 acc[S][MT];
-  int tile = u0 / kc;
-  [[maybe_unused]] EpiOperands<KIND, MT> eo;
-  if constexpr (!SPLIT) epi_request<KIND, MT, NS>(g, tile, 0, eo);
-  const int c0 = u0 - tile * kc;  // first unit's chunk (a multiple of RING)
+  floatx4 acc[GW][S][MT];
 #pragma unroll
-  for (int j = 0; j < RING; ++j) {
-    request_w(u0 + j, wr[j]);
-    request_a(u0 + j, c0 + j, ar[j]);
-  }
-  __builtin_amdgcn_sched_barrier(0);
-  if constexpr (kScale) rs_finish<T_pad>(g, 0, ssv, &red_s[0][0][0], rs_s);
-  // rs_s is read by epilogues after the main loop's barriers; red_s is next
-  // written by an epilogue, after them as well
-
-  // ---- main loop over segments (the units of one tile within [u0, u1)),
-  // RING units per trip.  Unit u: stage its activations (requested RING units ago)
-  // into LDS slot (u - u0) & 1 and request unit u + RING's into the freed
-  // registers; barrier; multiply with the weight fragments requested RING units
-  // ago, then request unit u + RING's weights into them.  The slot staged here
-  // was last read for unit u - 2, which every wave finished before unit
-  // u - 1's barrier.  The accumulators are zeroed per segment, so the inner
-  // loop carries them unchanged.
-  int gc = c0;  // chunk of unit gu within its tile
-  for (int gu = u0; gu < u1;) {
-    const int ue = min(u1, (tile + 1) * kc);
+  for (int i = 0; i < GW; ++i)
 #pragma unroll
     for (int q = 0; q < S; ++q)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[q][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (; gu < ue; gu += RING) {
-      // chunk of unit gu + RING + j: gc + RING + j, wrapped into the next tile
-      const int nc = gc + RING < kc ? gc + RING : gc + RING - kc;
+      for (int m = 0; m < MT; ++m) acc[i][q][m] = floatx4{0.f, 0.f, 0.f, 0.f};
+
 #pragma unroll
-      for (int j = 0; j < RING; ++j) {
-        const int u = gu + j;
-        const int slot = (u - u0) & 1;
-        stage(ar[j], slot);
-        __builtin_amdgcn_sched_barrier(0);
-        request_a(u + RING, nc + j, ar[j]);
-        __builtin_amdgcn_sched_barrier(0);
-        __syncthreads();
+  for (int r = 0; r < RING; ++r) request_w(c0 + r, wr[r]);
+#pragma unroll
+  for (int r = 0; r < RA; ++r) request_a(c0 + r, ar[r], agn[r]);
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (kNorm) rs_finish<T_pad>(g, 0, ssv, &red_s[0][0][0], rs_s);
+  // rs_s is read after the main loop's barriers; red_s is next written by an
+  // epilogue, after them as well
+
+  // ---- main loop, RING chunks per trip.  Chunk c: stage its activations
+  // (requested RA chunks ago) into LDS slot (c - c0) & 1, request chunk
+  // c + RA's into the freed registers; barrier; multiply with the weight
+  // fragments requested RING chunks ago, then request chunk c + RING's into
+  // them.  The slot staged here was last read for chunk c - 2, which every
+  // wave finished before chunk c - 1's barrier.  Chunks past the slice
+  // (the last trip) only stage and load one line.
+  for (int cb = c0; cb < c1; cb += UNR) {
+#pragma unroll
+    for (int r = 0; r < UNR; ++r) {
+      const int c = cb + r;
+      const int slot = r & 1;  // (c - c0) & 1: UNR is even
+      stage(ar[r % RA], agn[r % RA], slot);
+      __builtin_amdgcn_sched_barrier(0);
+      request_a(c + RA, ar[r % RA], agn[r % RA]);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      if (c < c1) {
         const unsigned char *al = lds_a[slot];
-        if constexpr (NS == 2) {
-          u32x4 af[MT];
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const int r = mt * 16 + lr;
-            af[mt] = *(const u32x4 *)(al + r * 128 + swz(r, kst * 4 + lg) * 16);
+        for (int st = 0; st < 2; ++st) {
+          u32x4 bh[MT], bl[MT];
+#pragma unroll
+          for (int m = 0; m < MT; ++m) {
+            const int row = m * 16 + lr;
+            const int off = row * 128 + swz(row, st * 4 + lg) * 16;
+            bh[m] = *(const u32x4 *)(al + off);
+            bl[m] = *(const u32x4 *)(al + PLANE + off);
           }
 #pragma unroll
-          for (int q = 0; q < S; ++q)
+          for (int i = 0; i < GW; ++i) {
+            if (i >= live) break;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-              acc[q][mt] = mfma16x16x32(as_bf16x8(wr[j][q * 2]), as_bf16x8(af[mt]), acc[q][mt]);
-        }
+            for (int q = 0; q < S; ++q)
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          if (NS == 2 || !owns) break;
-          u32x4 af[MT];
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const int r = mt * 16 + lr;
-            af[mt] = *(const u32x4 *)(al + r * 128 + swz(r, s * 4 + lg) * 16);
+              for (int m = 0; m < MT; ++m) {
+                const bf16x8 w = as_bf16x8(wr[r % RING][(i * S + q) * 2 + st]);
+                acc[i][q][m] = mfma16x16x32(w, as_bf16x8(bl[m]), acc[i][q][m]);
+                acc[i][q][m] = mfma16x16x32(w, as_bf16x8(bh[m]), acc[i][q][m]);
+              }
           }
-#pragma unroll
-          for (int q = 0; q < S; ++q)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-              acc[q][mt] = mfma16x16x32(as_bf16x8(wr[j][q * 2 + s]), as_bf16x8(af[mt]), acc[q][mt]);
         }
-        __builtin_amdgcn_sched_barrier(0);
-        request_w(u + RING, wr[j]);
-        __builtin_amdgcn_sched_barrier(0);
       }
-      gc = nc;
+      __builtin_amdgcn_sched_barrier(0);
+      request_w(c + RING, wr[r % RING]);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if constexpr (SPLIT) {
-      // this segment's partial, in slot (this workgroup - the tile's first
-      // contributor); plain stores: the finish kernel runs after this grid
-      const int first = gemm_group_owner(Ng, G, (long)tile * kc / RING);
-      floatx4 *dst = partial_of(g, tile, blockIdx.x - first);
+  }
+
+  if (s == 1) {  // whole tile: finish in place
 #pragma unroll
-      for (int q = 0; q < S; ++q)
+    for (int m = 0; m < MT; ++m) {
+      floatx4 am[GW][S];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) dst[((wave * S + q) * MT + mt) * 64 + lane] = acc[q][mt];
-      ++tile;
-    } else {
-      if constexpr (NS == 2) {
-        // wave w + 2 adds its k-step's sums into wave w's through the
-        // activation slots (2 S MT KB <= their 4 MT KB), once every wave is
-        // done reading them
-        floatx4 *red = (floatx4 *)&lds_a[0][0];
-        __syncthreads();
-        if (wave >= 2) {
+      for (int i = 0; i < GW; ++i)
 #pragma unroll
-          for (int q = 0; q < S; ++q)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) red[(((wave - 2) * S + q) * MT + mt) * 64 + lane] = acc[q][mt];
-        }
-        __syncthreads();
-        if (wave < 2) {
-#pragma unroll
-          for (int q = 0; q < S; ++q)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) acc[q][mt] += red[((wave * S + q) * MT + mt) * 64 + lane];
-        }
-      }
-      epilogue<KIND, MT, NS>(g, tile, 0, acc, eo, rs_s, red_s);
-      if (ue < u1) {
-        __syncthreads();  // red_s is written again by the next tile's epilogue
-        epi_request<KIND, MT, NS>(g, ++tile, 0, eo);
-      }
+        for (int q = 0; q < S; ++q) am[i][q] = acc[i][q][m];
+      epilogue<KIND, GW>(g, gt, ga, gb, m, am, rs_s, red_s);
     }
+    return;
+  }
+
+  // ---- split tile: partials to L2, arrive, wait for the tile's other
+  // slices, finish token blocks ks, ks + s, ...  Partial (tile gt, slice
+  // sl): [wave][i][q][m][lane] floatx4.
+  constexpr int PW = GW * S * MT;  // floatx4 per lane per wave
+  float *part = g.part + ((size_t)gt * s + ks) * (4 * PW * 64 * 4);
+#pragma unroll
+  for (int i = 0; i < GW; ++i) {
+    if (i >= live) break;
+#pragma unroll
+    for (int q = 0; q < S; ++q)
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+        *(floatx4 *)(part + ((size_t)((wave * GW + i) * S + q) * MT + m) * 256 + lane * 4) = acc[i][q][m];
+  }
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have reached L2
+  __syncthreads();
+  if (tid == 0) {
+    // Arrival: 1 + 256 o, o = (this XCD - x) mod 8, the dispatcher's offset
+    // (round-robin from wherever the previous dispatch left it: the same
+    // for every workgroup of this one, so the slices of a tile share an XCD
+    // whatever o is).  The counter is read at agent scope: a workgroup-scope
+    // load may be served by this compute unit's L1, which keeps the line of
+    // the first poll.
+    const uint32_t o = (xcc_id() - (unsigned)x) & 7u;
+    uint32_t *ctr = g.ctr + x * 32 + t;  // one 128-byte line of counters per group of XCD slots
+    __hip_atomic_fetch_add(ctr, 1u + (o << 8), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int it = 0;
+    uint32_t v;
+    while (((v = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffu) <
+           (uint32_t)s) {
+      if (++it > g.spin_limit) {
+        atomicOr(g.status, PPD_DEV_SYNC_TIMEOUT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    if ((v >> 8) != o * (uint32_t)s) atomicOr(g.status, PPD_DEV_XCD_PLACEMENT);
+  }
+  __syncthreads();
+  const float *tile_part = g.part + (size_t)gt * s * (4 * PW * 64 * 4);
+  const __amdgpu_buffer_rsrc_t rp = rsrc_of(tile_part, (uint32_t)s * 4 * PW * 64 * 16);
+  // the slices' partials are requested SB at a time (one round trip per
+  // batch; past the last slice the loads repeat slice 0 and are not added)
+  // and added in slice order.  QKV and gate/up: the tile's (group, token
+  // block) items are dealt to the slices in turn (item i MT + m to slice
+  // (i MT + m) % s); the others keep whole token blocks together (their
+  // epilogues reduce over the tile's rows): token block m to slice m % s.
+  constexpr int SB = GW * S <= 2 ? 8 : 4;
+  constexpr bool kItems = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
+  auto finish_block = [&](int m, unsigned gmask) {
+    floatx4 am[GW][S];
+#pragma unroll
+    for (int i = 0; i < GW; ++i)
+#pragma unroll
+      for (int q = 0; q < S; ++q) am[i][q] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int sb = 0; sb < s; sb += SB) {
+      floatx4 buf[SB][GW][S];
+#pragma unroll
+      for (int b = 0; b < SB; ++b) {
+        const int sl = sb + b < s ? sb + b : 0;
+#pragma unroll
+        for (int i = 0; i < GW; ++i)
+#pragma unroll
+          for (int q = 0; q < S; ++q) {
+            const uint32_t off =
+                (uint32_t)((((size_t)sl * 4 * PW + ((wave * GW + i) * S + q) * MT + m) * 64 + lane) * 16);
+            buf[b][i][q] = i < live && ((gmask >> i) & 1u) ? load_l2(rp, off) : floatx4{0.f, 0.f, 0.f, 0.f};
+          }
+      }
+#pragma unroll
+      for (int b = 0; b < SB; ++b)
+        if (sb + b < s) {
+#pragma unroll
+          for (int i = 0; i < GW; ++i)
+#pragma unroll
+            for (int q = 0; q < S; ++q) am[i][q] += buf[b][i][q];
+        }
+    }
+    epilogue<KIND, GW>(g, gt, ga, gb, m, am, rs_s, red_s, gmask);
+  };
+  if constexpr (kItems) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      unsigned gmask = 0;
+#pragma unroll
+      for (int i = 0; i < GW; ++i) gmask |= ((i * MT + m) % s == ks) ? 1u << i : 0u;
+      if (gmask) finish_block(m, gmask);  // uniform: no barriers in these epilogues
+    }
+  } else {
+    for (int m = ks; m < MT; m += s) finish_block(m, ~0u);
   }
 }
 
-// ---- finish of a split GEMM: workgroup (tile, 16-token block mt) adds the
-// tile's partials in contributor (workgroup) order and runs the epilogue for
-// the block's tokens.  The waves and lanes keep the GEMM's accumulator layout.
-template <int KIND>
-__global__ __launch_bounds__(256) void gemm_finish_kernel(GemmLaunch g) {
-  __shared__ float rs_s[128];
-  __shared__ float red_s[4][128][2];
-  const int t = blockIdx.x, mt = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const long Ng = (long)g.n_tiles * g.kc_pad / R;
-  const int first = gemm_group_owner(Ng, g.G, (long)t * g.kc_pad / R);
-  const int n_c = gemm_group_owner(Ng, g.G, (long)(t + 1) * g.kc_pad / R - 1) - first + 1;
+template <int MT, int KIND, int GW>
+hipError_t launch_mt_gw(const GemmLaunch &g, hipStream_t s) {
+  constexpr int WS = GW * SUB<KIND>;  // weight fragment pairs per wave and chunk
+  constexpr int RING = WS >= 4 ? 2 : WS >= 2 ? 4 : 8;
+  const dim3 grid(8 * g.TX * g.s), block(256);
+  hipEvent_t ev0 = (hipEvent_t)g.ev_start, ev1 = (hipEvent_t)g.ev_stop;
+  if (ev0)
+    hipExtLaunchKernelGGL((gemm_bf16_kernel<MT, KIND, GW, RING>), grid, block, 0, s, ev0, ev1, 0, g);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<MT, KIND, GW, RING>), grid, block, 0, s, g);
+  return hipGetLastError();
+}
 
-  [[maybe_unused]] float ssv[16];
-  if constexpr (KIND != GEMM_RESID) rs_request<16>(g, mt * 16, ssv);
-  EpiOperands<KIND, 1> eo;
-  epi_request<KIND, 1>(g, t, mt, eo);
+// groups per wave instantiated for S sub-tiles and MT token tiles: the
+// accumulators (GW S MT floatx4) and one chunk's weight fragments (GW S
+// pairs) must leave room in one wave's registers
+constexpr int gw_limit(int S, int MT) {
+  return S == 1 ? (MT <= 4 ? 6 : MT <= 6 ? 4 : 3) : (MT <= 4 ? 3 : MT <= 6 ? 2 : 1);
+}
 
-  // U contributors' partials are requested together (one round trip), then
-  // added in order
-  constexpr int U = 8, S = SUBS<KIND>;
-  floatx4 acc[S][1];
-#pragma unroll
-  for (int q = 0; q < S; ++q) acc[q][0] = floatx4{0.f, 0.f, 0.f, 0.f};
-  for (int c0 = 0; c0 < n_c; c0 += U) {
-    floatx4 buf[U][S];
-#pragma unroll
-    for (int v = 0; v < U; ++v) {
-      const floatx4 *src = partial_of(g, t, min(c0 + v, n_c - 1));
-#pragma unroll
-      for (int q = 0; q < S; ++q) buf[v][q] = src[((wave * S + q) * g.MT + mt) * 64 + lane];
-    }
-#pragma unroll
-    for (int v = 0; v < U; ++v)
-      if (c0 + v < n_c) {
-#pragma unroll
-        for (int q = 0; q < S; ++q) acc[q][0] += buf[v][q];
-      }
+template <int MT, int KIND>
+hipError_t launch_mt(const GemmLaunch &g, hipStream_t s) {
+  constexpr int LIM = gw_limit(SUB<KIND>, MT);
+  switch (g.gw) {
+    case 1: return launch_mt_gw<MT, KIND, 1>(g, s);
+    case 2:
+      if constexpr (LIM >= 2) return launch_mt_gw<MT, KIND, 2>(g, s);
+      break;
+    case 3:
+      if constexpr (LIM >= 3) return launch_mt_gw<MT, KIND, 3>(g, s);
+      break;
+    case 4:
+      if constexpr (LIM >= 4) return launch_mt_gw<MT, KIND, 4>(g, s);
+      break;
+    case 6:
+      if constexpr (LIM >= 6) return launch_mt_gw<MT, KIND, 6>(g, s);
+      break;
   }
-  if constexpr (KIND != GEMM_RESID) rs_finish<16>(g, mt * 16, ssv, &red_s[0][0][0], rs_s);
-  __syncthreads();  // red_s (used by rs_finish) is reused by the epilogue
-  epilogue<KIND, 1>(g, t, mt, acc, eo, rs_s, red_s);
+  return hipErrorInvalidValue;
 }
 
 template <int KIND>
 hipError_t launch_kind(const GemmLaunch &g, hipStream_t s) {
-  const dim3 grid(g.G), block(256);
-  hipEvent_t ev0 = (hipEvent_t)g.ev_start, ev1 = (hipEvent_t)g.ev_stop;
-  // timed: from the GEMM dispatch's start to the last dispatch's end
-  hipEvent_t gemm_stop = g.split ? nullptr : ev1;
-  constexpr bool kNs3 = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
-  if (g.ns != 4 && !(kNs3 && (g.ns == 3 || g.ns == 2) && !g.split && g.kc_pad % kRing3 == 0))
-    return hipErrorInvalidValue;
   switch (g.MT) {
-#define PPD_LAUNCH(M, SP, NS, RG)                                                            \
-  if (ev0)                                                                                   \
-    hipExtLaunchKernelGGL((gemm_bf16_kernel<M, KIND, SP, NS, RG>), grid, block, 0, s, ev0,   \
-                          gemm_stop, 0, g);                                                  \
-  else                                                                                       \
-    hipLaunchKernelGGL((gemm_bf16_kernel<M, KIND, SP, NS, RG>), grid, block, 0, s, g);
-#define PPD_CASE(M)                                                                          \
-  case M:                                                                                    \
-    if (g.split) {                                                                           \
-      PPD_LAUNCH(M, true, 4, R)                                                              \
-    } else if (g.ns == 3) {                                                                  \
-      if constexpr (kNs3) { PPD_LAUNCH(M, false, (kNs3 ? 3 : 4), kRing3) }                   \
-    } else if (g.ns == 2) {                                                                  \
-      if constexpr (kNs3) { PPD_LAUNCH(M, false, (kNs3 ? 2 : 4), kRing3) }                   \
-    } else {                                                                                 \
-      PPD_LAUNCH(M, false, 4, R)                                                             \
-    }                                                                                        \
-    break;
-    PPD_CASE(1) PPD_CASE(2) PPD_CASE(3) PPD_CASE(4) PPD_CASE(5) PPD_CASE(6) PPD_CASE(7) PPD_CASE(8)
-#undef PPD_CASE
-#undef PPD_LAUNCH
-    default: return hipErrorInvalidValue;
+    case 1: return launch_mt<1, KIND>(g, s);
+    case 2: return launch_mt<2, KIND>(g, s);
+    case 3: return launch_mt<3, KIND>(g, s);
+    case 4: return launch_mt<4, KIND>(g, s);
+    case 5: return launch_mt<5, KIND>(g, s);
+    case 6: return launch_mt<6, KIND>(g, s);
+    case 7: return launch_mt<7, KIND>(g, s);
+    case 8: return launch_mt<8, KIND>(g, s);
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !g.split) return e;
-  const dim3 fgrid(g.n_tiles, g.MT);
-  if (ev1)
-    hipExtLaunchKernelGGL(gemm_finish_kernel<KIND>, fgrid, block, 0, s, nullptr, ev1, 0, g);
-  else
-    hipLaunchKernelGGL(gemm_finish_kernel<KIND>, fgrid, block, 0, s, g);
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
-// ---- weight packing.  Packed 16-byte item (tile, chunk, sub-tile q < 4 SUBS,
+// ---- weight packing.  Packed 16-byte item (group, chunk, sub-tile q < S,
 // k-step s < 2, lane l < 64) holds the 8 bf16 of weight row
-// tile_row(tile, 16 q + l % 16) at columns 64 chunk + 32 s + 8 (l / 16) ..
-// + 7; rows and columns past the matrix (padding) are zero.
-template <int KIND, int NS>
+// group_row(group, q, l % 16) at columns 64 chunk + 32 s + 8 (l / 16) .. + 7;
+// rows past the matrix are zero.
+template <int KIND>
 __global__ __launch_bounds__(256) void pack_kernel(const bf16_t *__restrict__ src, u32x4 *__restrict__ dst,
-                                                   int N, int K, int rows_total, int kc_pad, long n_items) {
+                                                   int N, int K, int rows_total, int kc, long n_items) {
+  constexpr int S = SUB<KIND>;
   for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n_items;
        i += (long)gridDim.x * blockDim.x) {
-    constexpr int NQ = NS * SUBS<KIND>;  // sub-tiles per tile
     const int l = (int)(i & 63);
-    const long f = i >> 6;  // fragment ((tile kc_pad + chunk) NQ + q) 2 + s
-    const int s = (int)(f & 1), q = (int)((f >> 1) % NQ);
-    const long tc = f / (2 * NQ);
-    const int chunk = (int)(tc % kc_pad), tile = (int)(tc / kc_pad);
-    const int row = tile_row<KIND, NS>(tile, 16 * q + (l & 15), N);
-    const int col = chunk * KC + 32 * s + 8 * (l >> 4);
+    const long f = i >> 6;  // fragment ((group kc + chunk) S + q) 2 + s
+    const int st = (int)(f & 1), q = (int)((f >> 1) % S);
+    const long gc = f / (2 * S);
+    const int chunk = (int)(gc % kc), grp = (int)(gc / kc);
+    const int row = group_row<KIND>(grp, q, l & 15, N);
+    const int col = chunk * KC + 32 * st + 8 * (l >> 4);
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (row < rows_total && col < K) v = *(const u32x4 *)(src + (size_t)row * K + col);
     dst[i] = v;
   }
 }
 
-template <int KIND, int NS>
+template <int KIND>
 hipError_t launch_pack_kind(int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s) {
-  const int n_tiles = gemm_tiles_of(KIND, N, NS), kc_pad = gemm_kc_pad_of(K);
-  const long n_items = (long)n_tiles * kc_pad * UNIT<KIND, NS>;
+  const int G = gemm_groups_of(KIND, N), kc = K / KC;
+  const long n_items = (long)G * kc * SUB<KIND> * 2 * FRAG;
   const int rows_total = KIND == GEMM_SWIGLU ? 2 * N : N;
   const dim3 grid((unsigned)std::min<long>(8192, (n_items + 255) / 256)), block(256);
-  hipLaunchKernelGGL((pack_kernel<KIND, NS>), grid, block, 0, s, src, (u32x4 *)dst, N, K, rows_total,
-                     kc_pad, n_items);
+  hipLaunchKernelGGL((pack_kernel<KIND>), grid, block, 0, s, src, (u32x4 *)dst, N, K, rows_total, kc,
+                     n_items);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int gemm_tiles_of(int kind, int N, int ns) {
-  // QKV: N / 16 sub-tiles; gate/up: N / 16 blocks of 16 features
-  return kind == GEMM_SWIGLU || kind == GEMM_QKV ? (N / 16 + ns - 1) / ns : (N + BN - 1) / BN;
+int gemm_groups_of(int kind, int N) {
+  // QKV: N / 16 (head_dim 128); gate/up: 16 features per group; others 16 rows
+  return (N + 15) / 16;
 }
 
-int gemm_tile_rows_of(int kind, int ns) {
-  return kind == GEMM_QKV ? 16 * ns : kind == GEMM_SWIGLU ? 32 * ns : BN;
-}
+int gemm_sub_of(int kind) { return kind == GEMM_SWIGLU ? 2 : 1; }
 
-int gemm_kc_pad_of(int K) { return ((K / KC + R - 1) / R) * R; }
+int gemm_gw_max(int kind, int MT) { return gw_limit(gemm_sub_of(kind), MT); }
 
-hipError_t launch_pack_weight(int kind, int N, int K, int ns, const bf16_t *src, bf16_t *dst,
-                              hipStream_t s) {
-  if (ns == 3) {
-    if (kind == GEMM_QKV) return launch_pack_kind<GEMM_QKV, 3>(N, K, src, dst, s);
-    if (kind == GEMM_SWIGLU) return launch_pack_kind<GEMM_SWIGLU, 3>(N, K, src, dst, s);
-    return hipErrorInvalidValue;
-  }
-  if (ns == 2) {
-    if (kind == GEMM_QKV) return launch_pack_kind<GEMM_QKV, 2>(N, K, src, dst, s);
-    if (kind == GEMM_SWIGLU) return launch_pack_kind<GEMM_SWIGLU, 2>(N, K, src, dst, s);
-    return hipErrorInvalidValue;
-  }
-  if (ns != 4) return hipErrorInvalidValue;
+hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s) {
+  if (K % KC) return hipErrorInvalidValue;
   switch (kind) {
-    case GEMM_QKV: return launch_pack_kind<GEMM_QKV, 4>(N, K, src, dst, s);
-    case GEMM_RESID: return launch_pack_kind<GEMM_RESID, 4>(N, K, src, dst, s);
-    case GEMM_SWIGLU: return launch_pack_kind<GEMM_SWIGLU, 4>(N, K, src, dst, s);
-    case GEMM_LOGITS: return launch_pack_kind<GEMM_LOGITS, 4>(N, K, src, dst, s);
+    case GEMM_QKV: return launch_pack_kind<GEMM_QKV>(N, K, src, dst, s);
+    case GEMM_RESID: return launch_pack_kind<GEMM_RESID>(N, K, src, dst, s);
+    case GEMM_SWIGLU: return launch_pack_kind<GEMM_SWIGLU>(N, K, src, dst, s);
+    case GEMM_LOGITS: return launch_pack_kind<GEMM_LOGITS>(N, K, src, dst, s);
   }
   return hipErrorInvalidValue;
 }

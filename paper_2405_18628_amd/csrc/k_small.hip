@@ -5,25 +5,25 @@
 // ---------------------------------------------------------------------------
 // Embedding (Section 3: prompt tokens are trained embeddings appended to the
 // input).  Row t of the residual stream x is the embedding of ids[t]; for
-// bf16 models the kernel also writes x * gain (the first RMSNorm operand, as
-// bf16) and the row's sum of squares (one partial per row).  Rows
-// T..T_pad-1 are zero.
+// bf16 models the kernel also writes the row's sum of squares (the first
+// RMSNorm's one partial per row; its x * gain is formed by the consumer
+// GEMM) and, spread over the blocks, zeroes the step's GEMM tile counters.
+// Rows T..T_pad-1 are zero.
 
 template <typename WT>
 __global__ __launch_bounds__(256) void embed_kernel(const WT *__restrict__ tok_emb,
                                                     const WT *__restrict__ prompt_emb,
                                                     const int32_t *__restrict__ ids, int T,
                                                     int vocab, int n_prompt, int H,
-                                                    const WT *__restrict__ gain,
-                                                    float *__restrict__ x, bf16_t *__restrict__ xg,
-                                                    float *__restrict__ ss, uint32_t *status) {
+                                                    float *__restrict__ x, float *__restrict__ ss,
+                                                    uint32_t *__restrict__ ctr, size_t n_ctr,
+                                                    uint32_t *status) {
   const int t = blockIdx.x;
+  for (size_t i = (size_t)t * blockDim.x + threadIdx.x; i < n_ctr; i += (size_t)gridDim.x * blockDim.x)
+    ctr[i] = 0u;
   float *xr = x + (size_t)t * H;
   if (t >= T) {
-    for (int k = threadIdx.x; k < H; k += blockDim.x) {
-      xr[k] = 0.f;
-      if (xg) xg[(size_t)t * H + k] = 0;
-    }
+    for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = 0.f;
     if (ss && threadIdx.x == 0) ss[t] = 0.f;
     return;
   }
@@ -43,11 +43,6 @@ __global__ __launch_bounds__(256) void embed_kernel(const WT *__restrict__ tok_e
     }
     xr[k] = v;
     acc += v * v;
-    if (xg) {
-      float g;
-      if constexpr (sizeof(WT) == 2) g = bf16_to_f32(gain[k]); else g = gain[k];
-      xg[(size_t)t * H + k] = f32_to_bf16(v * g);
-    }
   }
   if (ss) {
     __shared__ float red[4];
@@ -59,17 +54,17 @@ __global__ __launch_bounds__(256) void embed_kernel(const WT *__restrict__ tok_e
 }
 
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
-                        int T, int vocab, int n_prompt, int H, const void *gain, float *x,
-                        void *xg, float *ss, uint32_t *status, hipStream_t s) {
+                        int T, int vocab, int n_prompt, int H, float *x, float *ss, uint32_t *ctr,
+                        size_t n_ctr, uint32_t *status, hipStream_t s) {
   int T_pad = (T + 15) & ~15;
   if (dtype == PPD_BF16) {
     hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(T_pad), dim3(256), 0, s,
                        (const bf16_t *)tok_emb, (const bf16_t *)prompt_emb, ids, T, vocab,
-                       n_prompt, H, (const bf16_t *)gain, x, (bf16_t *)xg, ss, status);
+                       n_prompt, H, x, ss, ctr, n_ctr, status);
   } else {
     hipLaunchKernelGGL(embed_kernel<float>, dim3(T_pad), dim3(256), 0, s,
                        (const float *)tok_emb, (const float *)prompt_emb, ids, T, vocab, n_prompt,
-                       H, (const float *)nullptr, x, (bf16_t *)nullptr, (float *)nullptr, status);
+                       H, x, (float *)nullptr, (uint32_t *)nullptr, (size_t)0, status);
   }
   return hipGetLastError();
 }

@@ -108,67 +108,83 @@ int qkv_rows(const ppd_model *m) { return (m->n_heads + 2 * m->n_kv_heads) * m->
 
 // ---- launch shapes (also used to size the workspace)
 
-// Partition of one skinny GEMM (see GemmLaunch).  A compute unit's load path
-// streams ~35 GB/s, so one whole 128-row tile per workgroup reaches the HBM
-// rate only with at least ~160 tiles; smaller GEMMs are split over all CUs.
-constexpr int kWholeTileMin = 160;
+// Compute units of the current device (one workgroup per compute unit; the
+// XCD-local tile finish needs the MI355X layout of 8 XCDs x 32 CUs with
+// round-robin dispatch, else every tile is finished whole, without waits).
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return n;
+}
 
 struct GemmShape {
   int kind, N, K;
-  int n_tiles, kc_pad, G, maxc, split, ns;
 };
 
-// Row groups per tile of a GEMM with N outputs (gate/up: features): 4, or
-// for QKV and gate/up GEMMs 3 when the smaller whole tiles leave every CU
-// fewer groups to stream (one whole tile per workgroup, one workgroup per CU
-// and round: 7B QKV 768 groups as 256 tiles of 3 instead of 192 of 4,
-// gate/up 688 as 230 of 3 instead of 172 of 4), or, for gate/up, 2 when
-// tiles of 4 would be too few to stay whole and tiles of 2 fill one round
-// (1.4B: 352 groups as 176 tiles instead of a split GEMM and its finish
-// kernel: 20.0 against 22.0 us).  QKV stays split there: a 2-group QKV tile
-// streams 32 weight rows per read of the whole activation operand (320 KB at
-// T = 80 for 128 KB of weights), and took 18.7 against 18.3 us split.  A
-// function of the matrix shape alone, so the packed weight does not depend
-// on T or L.
-int gemm_ns_of(int kind, int N, int K) {
-  if (kind != GEMM_QKV && kind != GEMM_SWIGLU) return 4;
-  if (K % 512) return 4;  // their 8-chunk ring needs 8 | K / 64
-  const int groups = N / 16;
-  const int t4 = (groups + 3) / 4, t3 = (groups + 2) / 3;
-  if (t4 < kWholeTileMin) {
-    const int t2 = (groups + 1) / 2;
-    return kind == GEMM_SWIGLU && t2 >= kWholeTileMin && t2 <= kCUs ? 2 : 4;  // else split
-  }
-  const int rounds4 = (t4 + kCUs - 1) / kCUs, rounds3 = (t3 + kCUs - 1) / kCUs;
-  return 3 * rounds3 < 4 * rounds4 ? 3 : 4;
-}
+// Partition of one GEMM for MT token tiles (see GemmLaunch): for each
+// candidate number s of K slices (the XCD's 32 workgroups then take 32 / s
+// tiles of h groups), a model of the slowest workgroup's time, taken from
+// measurements on MI355X: its weight bytes plus 0.4 x its fp32 activation
+// bytes (L2 hits, read while the weights stream) at a compute unit's ~35
+// GB/s, or its matrix-core time at 70 % of peak if larger; with s > 1 a
+// tail that does not overlap the stream -- ~1.5 us of hand-off plus writing
+// and reading its partial sums at ~25 GB/s.  The cheapest is taken.  Groups
+// per wave come from the instantiated set {1, 2, 3, 4, 6} (bounded by the
+// registers).
+struct GemmPlan {
+  int gw = 1, TX = 32, s = 1;
+  int xg0[9] = {0};
+};
 
-GemmShape gemm_shape(int kind, int N, int K) {
-  const int ns = gemm_ns_of(kind, N, K);
-  GemmShape g{kind, N, K, gemm_tiles_of(kind, N, ns), gemm_kc_pad_of(K), 0, 1, 0, ns};
-  const long Ng = (long)g.n_tiles * g.kc_pad / PPD_GEMM_RING;
-  g.split = g.n_tiles < kWholeTileMin;
-  g.G = g.split ? (int)std::min<long>(kCUs, Ng) : g.n_tiles;
-  for (int t = 0; t < g.n_tiles; ++t) {
-    const long x0 = (long)t * g.kc_pad / PPD_GEMM_RING, x1 = (long)(t + 1) * g.kc_pad / PPD_GEMM_RING;
-    g.maxc = std::max(g.maxc, gemm_group_owner(Ng, g.G, x1 - 1) - gemm_group_owner(Ng, g.G, x0) + 1);
+GemmPlan plan_gemm(const GemmShape &sh, int MT, bool xcd_sync) {
+  GemmPlan best;
+  const int G = gemm_groups_of(sh.kind, sh.N), S = gemm_sub_of(sh.kind), kc = sh.K / 64;
+  for (int x = 0; x <= 8; ++x) best.xg0[x] = (int)((long)G * x / 8);
+  const int nx = (G + 7) / 8;
+  const int gmax = gemm_gw_max(sh.kind, MT);
+  double best_t = 1e30;
+  for (int s = 1; s <= 16; s *= 2) {
+    if (s > kc || (s > 1 && !xcd_sync)) break;
+    const int TX = 32 / s;
+    const int h = std::max(1, (nx + TX - 1) / TX);
+    int gw = (h + 3) / 4;
+    if (gw == 5) gw = 6;
+    if (gw > gmax) continue;
+    const double kch = (double)((kc + s - 1) / s);
+    const double wb = (double)h * 16 * S * kch * 64 * 2;
+    const double ab = (double)MT * 16 * kch * 64 * 4;
+    const double pb = (double)h * 16 * S * MT * 16 * 4;
+    const double flops = 4.0 * MT * 16 * h * 16 * S * kch * 64;
+    const double t = std::max((wb + 0.4 * ab) / 35e9, flops / (0.7 * 2.5e15 / 256)) +
+                     (s > 1 ? 1.5e-6 + 2 * pb / 25e9 : 0.0);
+    if (t < best_t) {
+      best_t = t;
+      best.gw = gw;
+      best.TX = TX;
+      best.s = s;
+    }
   }
-  if (g.G == g.n_tiles) g.split = 0;  // one whole tile per workgroup
-  return g;
+  return best;
 }
 
 enum { SH_QKV = 0, SH_O = 1, SH_GATE_UP = 2, SH_DOWN = 3, SH_LM = 4 };
 
 void gemm_shapes(const ppd_model *m, GemmShape out[5]) {
-  out[SH_QKV] = gemm_shape(GEMM_QKV, qkv_rows(m), m->hidden);        // half a head per tile
-  out[SH_O] = gemm_shape(GEMM_RESID, m->hidden, m->n_heads * 128);  // output projection
-  out[SH_GATE_UP] = gemm_shape(GEMM_SWIGLU, m->ffn, m->hidden);     // 64 features per tile
-  out[SH_DOWN] = gemm_shape(GEMM_RESID, m->hidden, m->ffn);         // down projection
-  out[SH_LM] = gemm_shape(GEMM_LOGITS, m->vocab, m->hidden);        // LM head
+  out[SH_QKV] = {GEMM_QKV, qkv_rows(m), m->hidden};
+  out[SH_O] = {GEMM_RESID, m->hidden, m->n_heads * 128};
+  out[SH_GATE_UP] = {GEMM_SWIGLU, m->ffn, m->hidden};
+  out[SH_DOWN] = {GEMM_RESID, m->hidden, m->ffn};
+  out[SH_LM] = {GEMM_LOGITS, m->vocab, m->hidden};
 }
 
-// bytes of a tile partial of T_pad tokens: 128 rows x T_pad fp32
-size_t tile_partial_floats(int Tp) { return (size_t)128 * Tp; }
+// bytes of the partial sums of a plan (0 when every tile is whole)
+size_t plan_part_bytes(const GemmShape &sh, const GemmPlan &p, int MT) {
+  if (p.s == 1) return 0;
+  return (size_t)8 * p.TX * p.s * 4 * p.gw * gemm_sub_of(sh.kind) * MT * 64 * 16;
+}
+
+constexpr int kSpinLimit = 1 << 14;  // bounded wait of a tile's slices (~10-20 ms)
 
 // Key splits of the attention: a workgroup per (head, split) reads each
 // key/value block once, so the splits spread the cache over the compute
@@ -189,7 +205,7 @@ void attn_splits(const ppd_model *m, int L, int T, int *splits, int *chunk) {
 WsLayout layout_of(const ppd_model *m, int T) {
   WsLayout w{};
   const int Tp = t_pad_of(T);
-  const size_t es = m->dtype == PPD_BF16 ? 2 : 4;
+  const bool bf16 = m->dtype == PPD_BF16;
   const int H = m->hidden, F = m->ffn, nh = m->n_heads, d = m->head_dim;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -199,33 +215,43 @@ WsLayout layout_of(const ppd_model *m, int T) {
   };
   w.status = take(16);
   w.x = take(sizeof(float) * Tp * H);
-  w.xg = take(es * Tp * H + sizeof(float) * Tp);
-  w.max_ss = std::max(1, H / PPD_GEMM_BN);
+  // activations are fp32 on both paths; the fp32 path also keeps x * gain
+  // and the row scales (the bf16 GEMMs form x * gain while staging)
+  w.xg = take(bf16 ? 0 : sizeof(float) * (Tp * H + Tp));
+  w.max_ss = 1;
+  w.max_amax_tiles = 1;
+  size_t part = 0;
+  if (bf16) {
+    GemmShape gs[5];
+    gemm_shapes(m, gs);
+    const bool sync = device_cus() == 256;
+    for (int mt = 1; mt <= Tp / 16; ++mt)
+      for (int i = 0; i < 5; ++i) {
+        const GemmPlan p = plan_gemm(gs[i], mt, sync);
+        part = std::max(part, plan_part_bytes(gs[i], p, mt));
+        if (gs[i].kind == GEMM_RESID) w.max_ss = std::max(w.max_ss, 8 * p.TX);
+        if (gs[i].kind == GEMM_LOGITS) w.max_amax_tiles = std::max(w.max_amax_tiles, 8 * p.TX);
+      }
+  }
   w.ss = take(sizeof(float) * w.max_ss * Tp);
-  w.q = take(es * Tp * nh * d);
-  w.attn_o = take(es * Tp * nh * d);
-  w.act = take(es * Tp * F);
-  if (m->dtype == PPD_F32) {
+  w.q = take(sizeof(float) * Tp * nh * d);
+  w.attn_o = take(sizeof(float) * Tp * nh * d);
+  w.act = take(sizeof(float) * Tp * F);
+  if (!bf16) {
     const size_t wide = std::max({(size_t)qkv_rows(m), (size_t)2 * F, (size_t)H, (size_t)m->vocab});
     w.tmp = take(sizeof(float) * Tp * wide);
   } else {
     w.tmp = take(0);
   }
-  w.max_splits = m->dtype == PPD_BF16 ? attn_max_splits(nh) : 0;
+  w.max_splits = bf16 ? attn_max_splits(nh) : 0;
   w.attn_part = take(sizeof(float) * (size_t)nh * w.max_splits * Tp * PPD_ATTN_OROW);
-  size_t part = 0;
-  if (m->dtype == PPD_BF16) {
-    GemmShape gs[5];
-    gemm_shapes(m, gs);
-    for (int i = 0; i < 5; ++i)
-      if (gs[i].split)
-        part = std::max(part, (size_t)gs[i].n_tiles * gs[i].maxc * tile_partial_floats(Tp));
-  }
-  w.max_part_floats = part;
-  w.gemm_part = take(sizeof(float) * part);
-  w.max_amax_tiles = (m->vocab + 127) / 128;
+  w.max_part_floats = part / sizeof(float);
+  w.gemm_part = take(part);
   w.amax = take(sizeof(float2) * w.max_amax_tiles * Tp);
   w.rope = take(sizeof(float2) * Tp * (d / 2));
+  // tile counters: one 1 KB block (8 XCDs x one 128-byte line) per GEMM launch
+  w.n_ctr = bf16 ? (size_t)(4 * m->n_layers + 1) * 256 : 0;
+  w.ctr = take(sizeof(uint32_t) * w.n_ctr);
   w.total = off;
   return w;
 }
@@ -274,32 +300,37 @@ ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t
   const int Tp = t_pad_of(T), MT = Tp / 16;
   uint32_t *status = at<uint32_t>(ws, w.status);
   float *x = at<float>(ws, w.x);
-  bf16_t *xg = at<bf16_t>(ws, w.xg);
   float *ss = at<float>(ws, w.ss);
-  bf16_t *q = at<bf16_t>(ws, w.q);
-  bf16_t *attn_o = at<bf16_t>(ws, w.attn_o);
-  bf16_t *act = at<bf16_t>(ws, w.act);
+  float *q = at<float>(ws, w.q);
+  float *attn_o = at<float>(ws, w.attn_o);
+  float *act = at<float>(ws, w.act);
   float *part = at<float>(ws, w.gemm_part);
   float2 *amax = at<float2>(ws, w.amax);
   float2 *rope = at<float2>(ws, w.rope);
+  uint32_t *ctr = at<uint32_t>(ws, w.ctr);
   GemmShape gs[5];
   gemm_shapes(m, gs);
-  auto shape = [&](GemmLaunch &g, const GemmShape &sh) {
-    g.kind = sh.kind;
-    g.N = sh.N;
-    g.K = sh.K;
-    g.n_tiles = sh.n_tiles;
-    g.kc_pad = sh.kc_pad;
-    g.G = sh.G;
-    g.maxc = sh.maxc;
-    g.split = sh.split;
-    g.ns = sh.ns;
+  const bool sync = device_cus() == 256;
+  GemmPlan plan[5];
+  for (int i = 0; i < 5; ++i) plan[i] = plan_gemm(gs[i], MT, sync);
+  int launch = 0;  // GEMM launches of this step: counter block `launch`
+  auto setup = [&](GemmLaunch &g, int i) {
+    g.kind = gs[i].kind;
+    g.N = gs[i].N;
+    g.K = gs[i].K;
+    g.kc = gs[i].K / 64;
+    g.gw = plan[i].gw;
+    g.TX = plan[i].TX;
+    g.s = plan[i].s;
+    for (int xx = 0; xx <= 8; ++xx) g.xg0[xx] = plan[i].xg0[xx];
+    g.ctr = ctr + (size_t)launch++ * 256;
   };
 
   PPD_TRY_HIP(launch_rope_table(depth, seq_batch(m, B, kvs, Ls, Ts, 0), m->head_dim,
                                 m->rope_base, rope, s));
+  // embedding, its sum of squares (one partial per row), zeroed counters
   PPD_TRY_HIP(launch_embed(PPD_BF16, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
-                           m->attn_norm[0], x, xg, ss, status, s));
+                           x, ss, ctr, w.n_ctr, status, s));
   int n_ss = 1;
   // attention work per sequence: nh x splits workgroups
   int splits[PPD_BATCH_MAX], chunk[PPD_BATCH_MAX], wg0[PPD_BATCH_MAX + 1] = {0};
@@ -318,27 +349,29 @@ ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t
     g.inv_h = inv_h;
     g.eps = m->rms_eps;
     g.status = status;
-    g.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
-    // QKV + RoPE + cache stores
-    shape(g, gs[SH_QKV]);
-    g.W = (const bf16_t *)m->w_qkv[l];
-    g.A = xg;
-    g.ss = ss;
-    g.n_ss = n_ss;
-    g.rope = rope;
-    g.q = q;
-    g.nh = nh;
-    g.nkv = nkv;
-    g.sb = sb;
-    timer_events(TK_QKV, &g.ev_start, &g.ev_stop);
-    PPD_TRY_HIP(launch_gemm_bf16(g, s));
+    g.spin_limit = kSpinLimit;
+    // QKV + RoPE + cache stores; A = x * attn_norm
+    GemmLaunch qg = g;
+    setup(qg, SH_QKV);
+    qg.W = (const bf16_t *)m->w_qkv[l];
+    qg.A = x;
+    qg.gain = (const bf16_t *)m->attn_norm[l];
+    qg.ss = ss;
+    qg.n_ss = n_ss;
+    qg.rope = rope;
+    qg.q = q;
+    qg.nh = nh;
+    qg.nkv = nkv;
+    qg.sb = sb;
+    timer_events(TK_QKV, &qg.ev_start, &qg.ev_stop);
+    PPD_TRY_HIP(launch_gemm_bf16(qg, s));
     // tree attention
     AttnLaunch a{};
     a.q = q;
     a.mask = mask;
     a.out = attn_o;
     a.part = at<float>(ws, w.attn_part);
-    a.zeros = g.zeros;
+    a.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
     a.T_pad = Tp;
     a.nh = nh;
     a.nkv = nkv;
@@ -353,46 +386,44 @@ ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt(128.0));
     timer_events(TK_ATTN, &a.ev_start, &a.ev_stop);
     PPD_TRY_HIP(launch_attn_bf16(a, s));
-    // O projection + residual; operand of the MLP norm
+    // O projection + residual; sums of squares for the MLP norm
     GemmLaunch o = g;
-    shape(o, gs[SH_O]);
+    setup(o, SH_O);
     o.W = (const bf16_t *)m->w_o[l];
     o.A = attn_o;
     o.x = x;
-    o.xg = xg;
-    o.gain = (const bf16_t *)m->mlp_norm[l];
     o.ss_out = ss;
     timer_events(TK_O, &o.ev_start, &o.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(o, s));
-    n_ss = gs[SH_O].n_tiles;
-    // gate/up + SwiGLU
+    n_ss = 8 * plan[SH_O].TX;
+    // gate/up + SwiGLU; A = x * mlp_norm
     GemmLaunch u = g;
-    shape(u, gs[SH_GATE_UP]);
+    setup(u, SH_GATE_UP);
     u.W = (const bf16_t *)m->w_gate_up[l];
-    u.A = xg;
+    u.A = x;
+    u.gain = (const bf16_t *)m->mlp_norm[l];
     u.ss = ss;
     u.n_ss = n_ss;
     u.act = act;
     timer_events(TK_GATEUP, &u.ev_start, &u.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(u, s));
-    // down projection + residual; operand of the next norm
+    // down projection + residual; sums of squares for the next norm
     GemmLaunch dn = g;
-    shape(dn, gs[SH_DOWN]);
+    setup(dn, SH_DOWN);
     dn.W = (const bf16_t *)m->w_down[l];
     dn.A = act;
     dn.x = x;
-    dn.xg = xg;
-    dn.gain = (const bf16_t *)(l + 1 < m->n_layers ? m->attn_norm[l + 1] : m->final_norm);
     dn.ss_out = ss;
     timer_events(TK_DOWN, &dn.ev_start, &dn.ev_stop);
     PPD_TRY_HIP(launch_gemm_bf16(dn, s));
-    n_ss = gs[SH_DOWN].n_tiles;
+    n_ss = 8 * plan[SH_DOWN].TX;
   }
-  // final norm + LM head + greedy partials
+  // final norm + LM head + greedy partials; A = x * final_norm
   GemmLaunch lm{};
-  shape(lm, gs[SH_LM]);
+  setup(lm, SH_LM);
   lm.W = (const bf16_t *)m->lm_head;
-  lm.A = xg;
+  lm.A = x;
+  lm.gain = (const bf16_t *)m->final_norm;
   lm.T = T;
   lm.MT = MT;
   lm.part = part;
@@ -403,10 +434,10 @@ ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t
   lm.logits = logits;
   lm.amax = amax;
   lm.status = status;
-  lm.zeros = (const bf16_t *)((const char *)ws + PPD_WS_ZEROS);
+  lm.spin_limit = kSpinLimit;
   timer_events(TK_LM, &lm.ev_start, &lm.ev_stop);
   PPD_TRY_HIP(launch_gemm_bf16(lm, s));
-  PPD_TRY_HIP(launch_argmax_final(amax, gs[SH_LM].n_tiles, T, Tp, pred, status, s));
+  PPD_TRY_HIP(launch_argmax_final(amax, 8 * plan[SH_LM].TX, T, Tp, pred, status, s));
   return PPD_OK;
 }
 
@@ -432,7 +463,7 @@ ppd_status step_f32(const ppd_model *m, const ppd_kv *kv, int L, int T, const in
   one.L[0] = L;
   PPD_TRY_HIP(launch_rope_table(depth, one, d, m->rope_base, rope, s));
   PPD_TRY_HIP(launch_embed(PPD_F32, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
-                           nullptr, x, nullptr, nullptr, status, s));
+                           x, nullptr, nullptr, 0, status, s));
   for (int l = 0; l < m->n_layers; ++l) {
     float *kc = (float *)kv->k + (size_t)l * nkv * cap * d;
     float *vc = (float *)kv->v + (size_t)l * nkv * d * cap;
@@ -698,9 +729,7 @@ const char *ppd_last_error(void) { return g_err.c_str(); }
 size_t ppd_packed_weight_bytes(int32_t kind, int32_t rows, int32_t cols) {
   int gk, N;
   if (pack_args(kind, rows, cols, &gk, &N) != PPD_OK) return 0;
-  const int ns = gemm_ns_of(gk, N, cols);
-  return (size_t)gemm_tiles_of(gk, N, ns) * gemm_kc_pad_of(cols) * gemm_tile_rows_of(gk, ns) * 64 *
-         sizeof(bf16_t);
+  return (size_t)gemm_groups_of(gk, N) * gemm_sub_of(gk) * 16 * cols * sizeof(bf16_t);
 }
 
 ppd_status ppd_pack_weight(int32_t kind, int32_t rows, int32_t cols, const void *src, void *dst,
@@ -709,8 +738,7 @@ ppd_status ppd_pack_weight(int32_t kind, int32_t rows, int32_t cols, const void 
   ppd_status st = pack_args(kind, rows, cols, &gk, &N);
   if (st != PPD_OK) return st;
   if (!src || !dst) return fail(PPD_EINVAL, "NULL weight pointer");
-  PPD_TRY_HIP(launch_pack_weight(gk, N, cols, gemm_ns_of(gk, N, cols), (const bf16_t *)src, (bf16_t *)dst,
-                                 (hipStream_t)stream));
+  PPD_TRY_HIP(launch_pack_weight(gk, N, cols, (const bf16_t *)src, (bf16_t *)dst, (hipStream_t)stream));
   return PPD_OK;
 }
 

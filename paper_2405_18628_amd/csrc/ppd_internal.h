@@ -62,16 +62,18 @@ __device__ __forceinline__ float wave_max(float v) {
 struct WsLayout {
   size_t status;      // uint32 [4]
   size_t x;           // float  [T_pad][H]        residual stream
-  size_t xg;          // act    [T_pad][H]        x * gain (next norm's operand)
+  size_t xg;          // fp32 path: float [T_pad][H] x * gain, then [T_pad] row scales
   size_t ss;          // float  [max_ss][T_pad]   sum-of-squares partials
-  size_t q;           // act    [T_pad][nh][d]    queries after RoPE
-  size_t attn_o;      // act    [T_pad][nh d]     attention output
-  size_t act;         // act    [T_pad][F]        SwiGLU output
+  size_t q;           // float  [T_pad][nh][d]    queries after RoPE
+  size_t attn_o;      // float  [T_pad][nh d]     attention output
+  size_t act;         // float  [T_pad][F]        SwiGLU output
   size_t tmp;         // float  [T_pad][max(qkv_rows, 2F, V)]  (fp32 path only)
   size_t attn_part;   // float  [nh][max_splits][T_pad][d + 2]
   size_t gemm_part;   // float  [max_part_floats]
   size_t amax;        // float2 [max_amax_tiles][T_pad]
   size_t rope;        // float2 [T_pad][d/2]      (cos, sin)
+  size_t ctr;         // uint32 [n_ctr]           GEMM tile counters (zeroed per step)
+  size_t n_ctr;
   size_t total;
   int max_ss, max_splits, max_amax_tiles;
   size_t max_part_floats;
@@ -82,27 +84,16 @@ struct WsLayout {
 // ---------------------------------------------------------------------------
 // kernel launchers (defined in the .hip files, called by the host driver)
 
-// Skinny GEMM partition.  Tiles of ns row groups of 16 (QKV) or 32 rows
-// (ns = 4: 128 rows, QKV 64, half a head; ns = 3 for whole-tile QKV and
-// gate/up where that spreads them over more CUs, see gemm_ns_of);
-// each tile's K is cut in 64-column chunks, padded with zero chunks to
-// kc_pad, a multiple of PPD_GEMM_RING; a group is PPD_GEMM_RING consecutive
-// chunks of one tile.
-// Unit u = tile * kc_pad + chunk.  Workgroup w of G owns the contiguous
-// groups [Ng w / G, Ng (w + 1) / G), Ng = n_tiles * kc_pad / PPD_GEMM_RING,
-// so every workgroup streams an equal share and tile boundaries fall between
-// groups.  G = n_tiles: one whole tile per workgroup, finished in place;
-// otherwise (split) every workgroup stores the partial sums of its tile
-// segments and a finish kernel adds them in workgroup order.
-#ifndef PPD_GEMM_RING
-#define PPD_GEMM_RING 4
-#endif
+// Skinny GEMM partition (k_gemm.hip).  Weights are packed group-major: a
+// group is 16 output rows (gate/up: 16 features, i.e. 16 gate and 16 up
+// rows), each of its K / 64 chunks a run of 1 KB MFMA fragments.  The groups
+// are dealt to the 8 XCDs (XCD x: groups [xg0[x], xg0[x + 1])); on each XCD,
+// TX tiles (consecutive groups, at most 4 gw) x s K-slices take its TX s
+// workgroups (workgroup b runs on XCD b % 8, slot b / 8 = tile s + slice).
+// A tile split over s > 1 slices is finished inside the kernel: partial sums
+// to L2, an XCD-local counter, each slice finishing token blocks ks, ks + s,
+// ...  Grid = 8 TX s <= 256, one workgroup per compute unit.
 #define PPD_GEMM_BN 128
-__host__ __device__ inline long gemm_group_lo(long Ng, int G, int w) { return Ng * w / G; }
-// workgroup owning group x
-__host__ __device__ inline int gemm_group_owner(long Ng, int G, long x) {
-  return (int)(((x + 1) * G - 1) / Ng);
-}
 
 // The sequences of one (batched) step: their tree tokens are packed in
 // sequence order, sequence s owning tokens [t0[s], t0[s + 1]); each has its
@@ -119,55 +110,53 @@ struct SeqBatch {
 struct GemmLaunch {
   // operands
   const bf16_t *W;      // packed weight (ppd_pack_weight)
-  const bf16_t *A;      // [T_pad][K]
-  const bf16_t *zeros;  // 16 zero bytes in global memory
+  const float *A;       // [T_pad][K] fp32 activations (norm consumers: the residual x)
+  const bf16_t *gain;   // norm consumers (QKV, gate/up, LM head): the norm gain [K]
   int N, K, T, MT;      // N = output rows (SwiGLU: F), MT = T_pad / 16
   int kind;             // GemmKind
-  int n_tiles, kc_pad, G, maxc;  // partition (see above); maxc: max workgroups per tile
-  int ns;               // row groups (waves with rows) per tile: 4, or 3 (whole QKV / gate/up)
-  int split;            // G != n_tiles: partial sums + finish kernel
-  float *part;          // split: [n_tiles][maxc][8 MT 64][4] partial sums
+  // partition (see above)
+  int kc;               // K / 64
+  int gw;               // groups per wave (a tile holds at most 4 gw groups)
+  int TX, s;            // tiles per XCD, K slices per tile
+  int xg0[9];
+  float *part;          // s > 1: [8 TX][s][4 gw S MT][64] floatx4 partial sums
+  uint32_t *ctr;        // s > 1: tile counters, XCD x's at ctr + 32 x (zeroed per step)
+  int spin_limit;       // bounded wait for a tile's other slices
   // epilogue inputs
-  const float *ss;  // norm partials for row scaling (QKV, SwiGLU, LOGITS)
+  const float *ss;      // norm partials for row scaling (QKV, SwiGLU, LOGITS)
   int n_ss;
   float inv_h, eps;
-  const float2 *rope;  // [T_pad][64]
+  const float2 *rope;   // [T_pad][64]
   // QKV outputs
-  bf16_t *q;           // [T_pad][nh][128]
+  float *q;             // [T_pad][nh][128] fp32
   int nh, nkv;
-  SeqBatch sb;         // caches, positions: token t of sequence s goes to L[s] + t - t0[s]
+  SeqBatch sb;          // caches, positions: token t of sequence s goes to L[s] + t - t0[s]
   // RESID
   float *x;
-  bf16_t *xg;
-  const bf16_t *gain;  // next norm's gain [N]
-  float *ss_out;       // [n_tiles][T_pad]
+  float *ss_out;        // [8 TX][T_pad]
   // SWIGLU
-  bf16_t *act;         // [T_pad][N]
+  float *act;           // [T_pad][N] fp32
   // LOGITS
-  float *logits;       // [T][N] or null
-  float2 *amax;        // [n_tiles][T_pad]
+  float *logits;        // [T][N] or null
+  float2 *amax;         // [8 TX][T_pad]
   uint32_t *status;
-  void *ev_start, *ev_stop;  // optional events at the first dispatch's start / last one's end
+  void *ev_start, *ev_stop;  // optional events at the dispatch's start / end
 };
 
 enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_SWIGLU = 2, GEMM_LOGITS = 3 };
 
-// packed layout of a weight for GEMM kind `kind` with N output rows (SwiGLU:
-// F features, 2F rows) and K columns
-// with ns row groups per tile
-int gemm_tiles_of(int kind, int N, int ns);
-int gemm_tile_rows_of(int kind, int ns);  // 16 ns (QKV), 32 ns (gate/up) or 128
-int gemm_kc_pad_of(int K);
-hipError_t launch_pack_weight(int kind, int N, int K, int ns, const bf16_t *src, bf16_t *dst,
-                              hipStream_t s);
+int gemm_groups_of(int kind, int N);  // groups of a GEMM with N output rows (gate/up: features)
+int gemm_sub_of(int kind);            // 16-row sub-tiles per group (2 for gate/up)
+int gemm_gw_max(int kind, int MT);    // largest groups-per-wave instantiated for MT token tiles
+hipError_t launch_pack_weight(int kind, int N, int K, const bf16_t *src, bf16_t *dst, hipStream_t s);
 hipError_t launch_gemm_bf16(const GemmLaunch &g, hipStream_t s);
 
 #define PPD_ATTN_OROW 132  // floats per partial row: 128 dims, m, l, padding
 
 struct AttnLaunch {
-  const bf16_t *q;      // [T_pad][nh][d]
+  const float *q;       // [T_pad][nh][d] fp32
   const uint64_t *mask; // [T][2], bits over the token's own tree
-  bf16_t *out;          // [T_pad][nh d]
+  float *out;           // [T_pad][nh d] fp32
   float *part;          // [nh][max_splits][T_pad][PPD_ATTN_OROW] (splits > 1)
   const bf16_t *zeros;  // >= 16 zero bytes
   int T_pad, nh, nkv, max_splits;
@@ -202,9 +191,11 @@ hipError_t launch_next_tree(const NextTreeLaunch &p, int n_depths, hipStream_t s
 // records the thread's error message (ppd_last_error) and returns s
 ppd_status ppd_fail(ppd_status s, const char *fmt, ...);
 
+// embedding rows into x (fp32), rows T..T_pad-1 zero; bf16 models also write
+// each row's sum of squares to ss and zero the n_ctr GEMM tile counters
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
-                        int T, int vocab, int n_prompt, int H, const void *gain, float *x,
-                        void *xg, float *ss, uint32_t *status, hipStream_t s);
+                        int T, int vocab, int n_prompt, int H, float *x, float *ss, uint32_t *ctr,
+                        size_t n_ctr, uint32_t *status, hipStream_t s);
 hipError_t launch_rope_table(const int32_t *depth, const SeqBatch &sb, int d, float base, float2 *rope,
                              hipStream_t s);
 hipError_t launch_argmax_final(const float2 *amax, int n_tiles, int T, int T_pad, int32_t *pred,

@@ -39,6 +39,8 @@ class LazyCache:
         self.t, self.tr, self.L = t, transposed, L
 
     def __getitem__(self, l):
+        if self.tr and l % 8 == 7:  # progress of long oracle runs (one line per 8 layers)
+            say(f"    oracle: layer {l + 1}")
         x = self.t[l]
         x = x[:, :, :self.L] if self.tr else x[:, :self.L, :]
         x = O.to_f64(x)

@@ -123,21 +123,18 @@ def test_accept_and_compact_reject_before_enqueue():
 
 
 def test_packed_weight_sizes_and_rejections():
-    """Packed size = tiles x (64-column chunks rounded up to a multiple of 4)
-    x tile rows x 64 columns x 2 bytes; rows past the matrix (the LM head's
-    last tile, the last 48-feature gate/up tile at 7B) and padding chunks are
-    counted, nothing else.  Sizes below in 128-row x 64-column units."""
+    """Packed size = groups of 16 output rows (gate/up: 16 features, i.e. 32
+    rows) x columns x 2 bytes: the matrix itself, plus zero rows up to a
+    whole group (the LM head's vocabulary, a ragged feature count)."""
     L = ppd.lib()
-    unit = 128 * 64 * 2
-    cases = [(ppd.PPD_W_QKV, 3 * 4096, 4096, 96 * 64), (ppd.PPD_W_O, 4096, 4096, 32 * 64),
-             (ppd.PPD_W_GATE_UP, 2 * 11008, 4096, 230 * 64 * 96 // 128),
-             (ppd.PPD_W_GATE_UP, 2 * 13824, 5120, 216 * 80), (ppd.PPD_W_QKV, 3 * 5120, 5120, 120 * 80),
-             (ppd.PPD_W_GATE_UP, 2 * 11008, 256, 172 * 4), (ppd.PPD_W_QKV, 3 * 2048, 2048, 48 * 32),
-             (ppd.PPD_W_GATE_UP, 2 * 5632, 2048, 176 * 32 // 2), (ppd.PPD_W_GATE_UP, 2 * 5632, 1024, 88 * 16), (ppd.PPD_W_DOWN, 4096, 11008, 32 * 172),
-             (ppd.PPD_W_LM_HEAD, 32000, 4096, 250 * 64), (ppd.PPD_W_LM_HEAD, 1000, 512, 8 * 8),
-             (ppd.PPD_W_DOWN, 512, 1344, 4 * 24), (ppd.PPD_W_GATE_UP, 2 * 1344, 512, 21 * 8)]
-    for kind, rows, cols, units in cases:
-        assert ppd.ppd_packed_weight_bytes(kind, rows, cols) == units * unit, (kind, rows, cols)
+    cases = [(ppd.PPD_W_QKV, 3 * 4096, 4096, 3 * 4096), (ppd.PPD_W_O, 4096, 4096, 4096),
+             (ppd.PPD_W_GATE_UP, 2 * 11008, 4096, 2 * 11008), (ppd.PPD_W_GATE_UP, 2 * 13824, 5120, 2 * 13824),
+             (ppd.PPD_W_QKV, 3 * 5120, 5120, 3 * 5120), (ppd.PPD_W_DOWN, 4096, 11008, 4096),
+             (ppd.PPD_W_LM_HEAD, 32000, 4096, 32000), (ppd.PPD_W_LM_HEAD, 1000, 512, 1008),
+             (ppd.PPD_W_LM_HEAD, 37, 64, 48), (ppd.PPD_W_DOWN, 512, 1344, 512),
+             (ppd.PPD_W_GATE_UP, 2 * 1344, 512, 2 * 1344)]
+    for kind, rows, cols, padded_rows in cases:
+        assert ppd.ppd_packed_weight_bytes(kind, rows, cols) == padded_rows * cols * 2, (kind, rows, cols)
     for kind, rows, cols in [(ppd.PPD_W_QKV, 3 * 4096, 4000), (ppd.PPD_W_QKV, 3 * 4096 - 64, 4096),
                              (ppd.PPD_W_O, 4000, 4096), (ppd.PPD_W_GATE_UP, 2 * 1000, 512),
                              (ppd.PPD_W_LM_HEAD, 0, 512), (5, 128, 128), (-1, 128, 128)]:

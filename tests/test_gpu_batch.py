@@ -2,9 +2,13 @@
 with its own cache, cached length and tree, share one pass over the weights.
 The sequences are independent, so the reference for each is the oracle's
 single-sequence step on it (there is no other arithmetic to check), and the
-batched GPU rows must equal the GPU's own single-sequence step bit for bit
-(same kernels, same per-token arithmetic).  Acceptance and compaction run
-per sequence on slices of the packed arrays, bit-exact against the oracle."""
+batched GPU rows must equal the GPU's own single-sequence step up to the
+order of fp32 sums (the GEMMs' K split and tiling follow the step's total
+token count, so a batch may add the same products in another order): logits
+within 1e-4 + 1e-4 |x|, stored keys / values within one bf16 ulp (+ 1e-4), greedy
+tokens equal wherever the single step's top-2 margin exceeds 2e-3.
+Acceptance and compaction run per sequence on slices of the packed arrays,
+bit-exact against the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -59,6 +63,21 @@ def _run_batch(case, seqs):
     return trees, parts, logits, pred, ws
 
 
+def _same_step(lb, ls, pb, ps, kb, ks, vb, vs, what):
+    """A sequence's rows of a batched step against its own single step."""
+    a, b = lb.double().cpu().numpy(), ls.double().cpu().numpy()
+    err = np.abs(a - b)
+    assert (err <= 1e-4 + 1e-4 * np.abs(b)).all(), f"{what}: logits differ by {err.max():.3e}"
+    srt = np.sort(b, axis=1)
+    decided = srt[:, -1] - srt[:, -2] > 2e-3
+    assert np.array_equal(pb.cpu().numpy()[decided], ps.cpu().numpy()[decided]), what
+    for x, y in ((kb, ks), (vb, vs)):
+        # one bf16 ulp, plus the fp32 reordering noise of a K = 4096 sum
+        # (~1e-5 of values of order 1) for keys near zero after RoPE
+        xf, yf = x.float(), y.float()
+        assert ((xf - yf).abs() <= 2 ** -7 * yf.abs() + 1e-4).all(), f"{what}: cache rows differ"
+
+
 def _run_single(case, s):
     tt = tree_tensors(s["tree"])
     T = s["tree"].T
@@ -94,9 +113,8 @@ def test_batch_equals_single_sequences_and_oracle(small_case, Ls, specs):
         kb = s["k"][:, :, s["L"]:s["L"] + T].clone()
         vb = s["v"][:, :, :, s["L"]:s["L"] + T].clone()
         ls, ps = _run_single(case, s)
-        assert torch.equal(lb, ls) and torch.equal(pb, ps), f"sequence {j} differs from its own step"
-        assert torch.equal(kb, s["k"][:, :, s["L"]:s["L"] + T])
-        assert torch.equal(vb, s["v"][:, :, :, s["L"]:s["L"] + T])
+        _same_step(lb, ls, pb, ps, kb, s["k"][:, :, s["L"]:s["L"] + T], vb,
+                   s["v"][:, :, :, s["L"]:s["L"] + T], f"sequence {j}")
         if j < 3:  # the oracle on a few sequences (it is the slow part)
             ref = O.verify_forward(case.oracle_model, LazyCache(s["k"], False, s["L"]),
                                    LazyCache(s["v"], True, s["L"]), s["L"], s["tree"].ids,
@@ -125,7 +143,8 @@ def test_batch_equals_single_sequences_and_oracle(small_case, Ls, specs):
 def test_batch_full_width_7b_layer():
     """The 7B shape at full width (one decoder layer): four sequences of 16
     tree tokens with different cache lengths, in the benchmark's launch
-    configuration; every sequence equals its own single-sequence step."""
+    configuration; every sequence equals its own single-sequence step (up to
+    the order of fp32 sums)."""
     case = make_case(workload("7b", n_layers=1), L=64)
     seqs = _sequences(case, [2048, 1024, 4000, 100], ["total:16"] * 4, 9100)
     say("[batch-7b] B=4 T=16 each")
@@ -133,8 +152,10 @@ def test_batch_full_width_7b_layer():
     t0 = 0
     for j, s in enumerate(seqs):
         T = s["tree"].T
+        kb = s["k"][:, :, s["L"]:s["L"] + T].clone()
+        vb = s["v"][:, :, :, s["L"]:s["L"] + T].clone()
         ls, ps = _run_single(case, s)
-        assert torch.equal(logits[t0:t0 + T], ls), f"sequence {j}"
-        assert torch.equal(pred[t0:t0 + T], ps)
+        _same_step(logits[t0:t0 + T], ls, pred[t0:t0 + T], ps, kb, s["k"][:, :, s["L"]:s["L"] + T],
+                   vb, s["v"][:, :, :, s["L"]:s["L"] + T], f"sequence {j}")
         assert torch.isfinite(ls).all()
         t0 += T

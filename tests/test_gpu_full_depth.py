@@ -93,18 +93,6 @@ def _run(name, taps=()):
     return case, ws, gpu_taps, ref
 
 
-# Measured at the 7B shape with every activation stored in bf16: at 32
-# layers the GPU's logits differ from the oracle's by rms 2.2e-2, max 0.12
-# (399k of 2.05M logits outside the tolerance), exactly as far as a second
-# independently rounded bf16 computation (the float32-sum oracle: rms 2.2e-2,
-# max 0.13, 395k) -- the storage roundings' own noise floor; greedy tokens
-# agree on every node the tolerance decides.
-FLOOR_XFAIL = pytest.mark.xfail(
-    strict=True, reason="bf16 activation roundings: the noise floor of any two bf16 "
-    "computations exceeds the tolerance past ~2 layers (rms 2.2e-2 at 32 layers)")
-
-
-@FLOOR_XFAIL
 def test_7b_benchmark_step_full_depth_vs_oracle():
     """The benchmark configuration: every node's logits and greedy token at
     full depth; the error at depths 1..32 next to the float32-sum oracle."""
@@ -128,7 +116,6 @@ def test_7b_benchmark_step_full_depth_vs_oracle():
     say(f"  greedy tokens: {n_strict} of {tree.T} nodes strictly determined, all equal")
 
 
-@FLOOR_XFAIL
 @pytest.mark.parametrize("name", ["1.4b", "13b", "7b-32k"])
 def test_full_depth_vs_oracle(name):
     case, ws, gpu_taps, ref = _run(name)

@@ -272,52 +272,37 @@ def test_root_only_tree_is_vanilla_decode(name, tiny_case, small_case):
 
 def _expected_packing(w, kind):
     """The packed layout of include/ppd.h, written out with numpy indexing:
-    item (tile, chunk, q, s, lane) = row r(tile, 16 q + lane % 16), columns
-    64 chunk + 32 s + 8 (lane // 16) .. + 7; zeros past the matrix.  QKV
-    tiles are half a head: sub-tile q of half f holds dims 32 f + 8 q .. + 7
-    in its rows 0..7 and their RoPE partners (+64) in rows 8..15."""
+    item (group, chunk, q, s, lane) = row r(group, q, lane % 16), columns
+    64 chunk + 32 s + 8 (lane // 16) .. + 7; zeros past the matrix.  A group
+    is 16 rows (gate/up: 16 features: q = 0 their gate rows, q = 1 their up
+    rows); a QKV group holds dims 8 (g % 8) .. + 7 of head part g // 8 in
+    rows 0..7 and their RoPE partners (+64) in rows 8..15."""
     rows, cols = w.shape
-    kc = -(-(cols // 64) // 4) * 4
-    if kind in (ppd.PPD_W_GATE_UP, ppd.PPD_W_QKV):
-        # ns groups of 16 features (gate/up) or 16 QKV rows per tile: 4, or
-        # (cols % 512 == 0) 3 when every tile stays whole (>= 160 tiles of 4)
-        # and 3-group tiles need fewer groups per CU over 256 CUs, or (gate/up)
-        # 2 when tiles of 4 are fewer than 160 and tiles of 2 number 160..256
-        groups = rows // 32 if kind == ppd.PPD_W_GATE_UP else rows // 16
-        t4, t3, t2 = -(-groups // 4), -(-groups // 3), -(-groups // 2)
-        ns = 4
-        if cols % 512 == 0:
-            if t4 >= 160:
-                ns = 3 if 3 * -(-t3 // 256) < 4 * -(-t4 // 256) else 4
-            elif kind == ppd.PPD_W_GATE_UP and 160 <= t2 <= 256:
-                ns = 2
-        n_tiles = -(-groups // ns)
+    kc = cols // 64
+    r = np.arange(16)
     if kind == ppd.PPD_W_GATE_UP:
         F = rows // 2
-        f = 16 * ns * np.arange(n_tiles)[:, None] + np.arange(16 * ns)[None, :]
-        tr = np.concatenate([f, F + f], axis=1)
-        tr = np.where(np.concatenate([f, f], axis=1) < F, tr, rows)   # padding features
+        G, S = -(-F // 16), 2
+        f = 16 * np.arange(G)[:, None] + r[None, :]                  # [G][16]
+        tr = np.stack([np.where(f < F, f, rows), np.where(f < F, F + f, rows)], axis=1)
     elif kind == ppd.PPD_W_QKV:
-        r = np.arange(16 * ns)
-        gs = ns * np.arange(n_tiles)[:, None] + (r // 16)[None, :]   # global 16-row group
-        # group gs: dims 8 (gs % 8) .. + 7 of head part gs // 8 in rows 0..7,
-        # their RoPE partners (+64) in rows 8..15
-        tr = 128 * (gs // 8) + np.where(r % 16 < 8, 0, 64)[None, :] + 8 * (gs % 8) + (r % 8)[None, :]
+        G, S = rows // 16, 1
+        g = np.arange(G)[:, None]
+        tr = (128 * (g // 8) + np.where(r < 8, 0, 64)[None, :] + 8 * (g % 8) + (r % 8)[None, :])[:, None, :]
     else:
-        n_tiles = -(-rows // 128)
-        tr = np.arange(128)[None, :] + 128 * np.arange(n_tiles)[:, None]
-    nq = tr.shape[1] // 16
-    wp = np.zeros((n_tiles * 128 + rows, kc * 64), dtype=w.dtype)
-    wp[:rows, :cols] = w
-    tr = np.where(tr < rows, tr, rows + 1)          # padding rows read the zero block
+        G, S = -(-rows // 16), 1
+        tr = (16 * np.arange(G)[:, None] + r[None, :])[:, None, :]
+        tr = np.where(tr < rows, tr, rows)
+    wp = np.zeros((rows + 1, cols), dtype=w.dtype)               # row `rows`: zeros
+    wp[:rows] = w
     lane = np.arange(64)
-    out = np.zeros((n_tiles, kc, nq, 2, 64, 8), dtype=w.dtype)
-    for q in range(nq):
-        rr = tr[:, 16 * q + lane % 16]              # [tiles][64]
+    out = np.zeros((G, kc, S, 2, 64, 8), dtype=w.dtype)
+    for q in range(S):
+        rr = tr[:, q, lane % 16]                                  # [G][64]
         for s in range(2):
             for c in range(kc):
                 col = 64 * c + 32 * s + 8 * (lane // 16)
-                idx = col[:, None] + np.arange(8)[None, :]      # [64][8]
+                idx = col[:, None] + np.arange(8)[None, :]        # [64][8]
                 out[:, c, q, s] = wp[rr[:, :, None], idx[None, :, :]]
     return out
 
