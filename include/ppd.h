@@ -247,6 +247,26 @@ ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids,
                       int32_t *next_tok, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture that forbids allocation, serving loops that must not allocate,
+ * harnesses that forbid it): ppd_verify_step with the workspace taken from a
+ * static device array of the library, PPD_STATIC_WS_BYTES (64 MiB) on each
+ * GPU it runs on, held until the process ends; the call allocates nothing.
+ * Arguments as ppd_verify_step, without ws / ws_bytes; status_out (optional
+ * device uint32) receives the step's device status word (ppd_device_status
+ * bits), the header of the array being cleared at the start of every call.
+ * PPD_EWORKSPACE when the step needs more than PPD_STATIC_WS_BYTES
+ * (ppd_workspace_bytes(model, T, capacity); a Vicuna-13B-shaped step with a
+ * 64-node tree needs about 36 MiB), nothing enqueued.  All calls on one GPU
+ * share the array: calls that may overlap on one GPU (unordered streams,
+ * several threads) race and must not be made.
+ */
+#define PPD_STATIC_WS_BYTES (64u << 20)
+ppd_status ppd_verify_step_static(const ppd_model *model, const ppd_kv *kv, int32_t L, int32_t T,
+                                  const int32_t *ids, const int32_t *depth, const uint64_t *mask,
+                                  float *logits, int32_t *pred, uint32_t *status_out, void *stream);
+
+/*
  * Commit accepted keys/values (Section 5.3: one cache shared by guessing and
  * verification; prompt-token entries are never committed):
  * cache[L + k] <- cache[L + path[k]] for k < *n_path, every layer and kv head.

@@ -72,6 +72,8 @@ def lib() -> C.CDLL:
                                       vp, vp]
         L.ppd_verify_batch.argtypes = [P(ppd_model), i32, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp,
                                        vp]
+        L.ppd_verify_step_static.argtypes = [P(ppd_model), P(ppd_kv), i32, i32, vp, vp, vp, vp, vp,
+                                             vp, vp]
         L.ppd_accept.argtypes = [i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
         L.ppd_kv_compact.argtypes = [P(ppd_model), P(ppd_kv), i32, vp, i32, vp, vp]
         L.ppd_device_status.argtypes = [vp, sz, P(C.c_uint32), i32, vp]
@@ -84,7 +86,7 @@ def lib() -> C.CDLL:
         L.ppd_packed_weight_bytes.argtypes = [i32, i32, i32]
         L.ppd_packed_weight_bytes.restype = sz
         L.ppd_pack_weight.argtypes = [i32, i32, i32, vp, vp, vp]
-        for f in ("ppd_next_tree", "ppd_sparse_template", "ppd_verify_batch", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
+        for f in ("ppd_verify_step_static", "ppd_next_tree", "ppd_sparse_template", "ppd_verify_batch", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
                   "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -257,6 +259,20 @@ def ppd_verify_step(model: Model, kv: KVCache, L: int, T: int, ids, depth, mask,
                                  _ptr(pred), _stream(stream)))
 
 
+def ppd_verify_step_static(model: Model, kv: KVCache, L: int, T: int, ids, depth, mask, logits,
+                           pred, status_out=None, stream=None):
+    """ppd_verify_step with the library's static workspace (no allocation)."""
+    import torch
+    for t, n in ((ids, "ids"), (depth, "depth"), (pred, "pred")):
+        _dev(t, torch.int32, n)
+    _dev(mask, None, "mask")
+    _dev(logits, torch.float32, "logits")
+    _dev(status_out, torch.int32, "status_out")
+    _check(lib().ppd_verify_step_static(C.byref(model.desc), C.byref(kv.desc), int(L), int(T),
+                                        _ptr(ids), _ptr(depth), _ptr(mask), _ptr(logits) or None,
+                                        _ptr(pred), _ptr(status_out) or None, _stream(stream)))
+
+
 def ppd_verify_batch(model: Model, kvs: Sequence[KVCache], L: Sequence[int], T: Sequence[int],
                      ids, depth, mask, ws, logits, pred, stream=None):
     """One step over len(kvs) sequences whose trees are packed in sequence
@@ -367,6 +383,6 @@ def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):
     return st, sp
 
 
-__all__ = ["ppd_verify_batch", "ppd_next_tree", "ppd_sparse_template", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
+__all__ = ["ppd_verify_step_static", "ppd_verify_batch", "ppd_next_tree", "ppd_sparse_template", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
            "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept", "ppd_kv_compact",
            "ppd_device_status", "ppd_last_error"]
