@@ -16,7 +16,9 @@ from typing import Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libppd.so")
+# PPD_LIBRARY selects another build of the same library (the host-sanitizer
+# build that the CPU tests load); by default the one next to this file
+LIB_PATH = os.environ.get("PPD_LIBRARY") or os.path.join(_HERE, "libppd.so")
 
 PPD_OK, PPD_EINVAL, PPD_ETREE, PPD_ECAPACITY, PPD_EDEVICE, PPD_EUNSUPPORTED, PPD_EWORKSPACE = range(7)
 PPD_F32, PPD_BF16 = 0, 1
