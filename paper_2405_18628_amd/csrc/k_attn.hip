@@ -19,8 +19,11 @@
 // wave w takes the pair's block w / 4 with its 16-query tiles w % 4 (and
 // w % 4 + 4), keeping one online softmax per query; the two blocks' waves
 // are merged through LDS at the end.  With KS > 1 each query's (O, m, l) is
-// stored and a merge kernel adds the splits in split order; with KS = 1 the
-// workgroup writes the output itself.
+// stored and the splits are added in split order: for a single sequence
+// inside the kernel (a head's splits share an XCD, so they meet in its L2:
+// each split, once all have arrived at the head's counter, merges 1 / KS of
+// the queries), for a batch by a merge kernel; with KS = 1 the workgroup
+// writes the output itself.
 //
 // Per 32-key block and query tile, on the matrix cores
 // (v_mfma_f32_16x16x32_bf16):
@@ -86,11 +89,47 @@ struct QTile {
   float l_run;
 };
 
+// Merge of one query's KS split rows, 4 dims of a row: the rows are read 8
+// at a time (one round trip per batch) and added in split order, scaled to
+// the running maximum.  rows(s0, ml, r) loads splits s0 .. s0 + 7 (those
+// below KS): ml[v] = (m, l, -, -), r[v] = the 4 dims.
+constexpr int MERGE_B = 8;
+template <typename ROWS>
+__device__ __forceinline__ floatx4 merge_splits(int KS, ROWS rows) {
+  constexpr int B = MERGE_B;
+  float M = -INFINITY, lsum = 0.f;
+  floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < KS; s0 += B) {
+    floatx4 ml[B], r[B];
+    rows(s0, ml, r);
+    float mb = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < B; ++v)
+      if (s0 + v < KS) mb = fmaxf(mb, ml[v][0]);
+    if (mb > M) {
+      const float f = exp2f(M - mb);  // 0 while M = -inf (nothing accumulated)
+      acc *= f;
+      lsum *= f;
+      M = mb;
+    }
+#pragma unroll
+    for (int v = 0; v < B; ++v) {
+      if (s0 + v < KS) {
+        const float sc = ml[v][0] == -INFINITY ? 0.f : exp2f(ml[v][0] - M);
+        lsum += sc * ml[v][1];
+        acc += sc * r[v];
+      }
+    }
+  }
+  return acc * (1.f / lsum);
+}
+
 // Eight waves: wave w works on query tiles (w % 4) + 4 i (i < NQ) and on the
 // blocks of parity w / 4, so two waves share each SIMD and hide each other's
 // latencies; the two parities are merged at the end.  RING: block pairs
-// requested ahead.
-template <int NQ, int RING>
+// requested ahead.  XM: one sequence, heads dealt to the XCDs, splits merged
+// in the kernel.
+template <int NQ, int RING, bool XM>
 __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[4 * SLOT];
 
@@ -100,11 +139,24 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
   const int qw = wave & 3, par = wave >> 2;
   const int lr = lane & 15, lg = lane >> 4;
   // this workgroup's sequence (uniform), head and key split
-  int sq = 0;
-  for (int j = 1; j < p.sb.B; ++j) sq = (int)blockIdx.x >= p.wg0[j] ? j : sq;
+  int sq = 0, h, ks;
+  [[maybe_unused]] int xs = 0, h0 = 0;  // XM: the XCD set and its first head
+  if constexpr (XM) {
+    const int KS = p.splits[0];
+    xs = blockIdx.x & 7;
+    const int j = blockIdx.x >> 3;
+    h0 = p.nh * xs / 8;
+    h = h0 + j / KS;
+    ks = j % KS;
+    if (h >= p.nh * (xs + 1) / 8) return;  // a slot past the XCD's heads
+  } else {
+    for (int j = 1; j < p.sb.B; ++j) sq = (int)blockIdx.x >= p.wg0[j] ? j : sq;
+    const int KS = p.splits[sq];
+    const int wl = blockIdx.x - p.wg0[sq];
+    h = wl / KS;
+    ks = wl % KS;
+  }
   const int KS = p.splits[sq];
-  const int wl = blockIdx.x - p.wg0[sq];
-  const int h = wl / KS, ks = wl % KS;
   const int kvh = h / (p.nh / p.nkv);
   const int t0 = p.sb.t0[sq], T = p.sb.t0[sq + 1] - t0, L = p.sb.L[sq], cap = p.sb.cap[sq];
   const int n_keys = L + T;
@@ -393,75 +445,76 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
       }
     }
   }
+  if constexpr (XM) {
+    if (KS == 1) return;
+    // every split of the head stores its rows (in this XCD's L2) and arrives
+    // at the head's counter; then each merges queries [T ks / KS,
+    // T (ks + 1) / KS), thread -> query tid / 32, dims 4 (tid % 32) .. + 3
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's row stores have reached L2
+    __syncthreads();
+    if (tid == 0) xcd_arrive_wait(p.ctr + xs * 32 + (h - h0), xs, (uint32_t)KS, p.spin_limit, p.status);
+    __syncthreads();
+    const size_t split_floats = (size_t)p.T_pad * OROW;
+    const float *hp = p.part + (size_t)h * p.max_splits * split_floats;
+    const __amdgpu_buffer_rsrc_t rp = rsrc_of(hp, (uint32_t)(KS * split_floats * 4));
+    const int d4 = (tid & 31) * 4;
+    for (int tl = T * ks / KS + (tid >> 5); tl < T * (ks + 1) / KS; tl += 16) {
+      const floatx4 o = merge_splits(KS, [&](int s0, floatx4(&ml)[MERGE_B], floatx4(&r)[MERGE_B]) {
+#pragma unroll
+        for (int v = 0; v < MERGE_B; ++v) {
+          const size_t row = (size_t)min(s0 + v, KS - 1) * split_floats + (size_t)tl * OROW;
+          ml[v] = load_l2(rp, (uint32_t)((row + 128) * 4));
+          r[v] = load_l2(rp, (uint32_t)((row + d4) * 4));
+        }
+      });
+      *(floatx4 *)(p.out + (size_t)(t0 + tl) * p.nh * 128 + h * 128 + d4) = o;
+    }
+  }
 }
 
-// ---- merge of the KS splits: workgroup (sequence s and head h, query tile
-// qt, 32-dim quarter dq); thread -> query tq = tid / 16, dims 32 dq + 2 (tid
-// % 16) and + 1.  The splits' rows are read 8 at a time (one round trip per
-// batch) and added in split order, scaled to the running maximum.
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnLaunch p) {
-  const int sq = blockIdx.x / p.nh, h = blockIdx.x % p.nh, qt = blockIdx.y, dq = blockIdx.z;
-  const int tq = threadIdx.x >> 4, d2 = dq * 32 + (threadIdx.x & 15) * 2;
+// ---- merge of the KS splits of a batch (after the attention kernel):
+// workgroup (sequence s and head h, query tile qt); thread -> query
+// tq = tid / 32, dims 4 (tid % 32) .. + 3.
+__global__ __launch_bounds__(512) void attn_merge_kernel(AttnLaunch p) {
+  const int sq = blockIdx.x / p.nh, h = blockIdx.x % p.nh, qt = blockIdx.y;
+  const int tq = threadIdx.x >> 5, d4 = (threadIdx.x & 31) * 4;
   const int KS = p.splits[sq];
   const int tl = qt * 16 + tq;
   if (KS == 1 || tl >= p.sb.t0[sq + 1] - p.sb.t0[sq]) return;  // one split: already final
   const size_t t = (size_t)p.sb.t0[sq] + tl;
-  auto row_of = [&](int s) { return p.part + (((size_t)h * p.max_splits + s) * p.T_pad + t) * OROW; };
-  constexpr int B = 8;
-  float M = -INFINITY, lsum = 0.f;
-  float2 acc = float2{0.f, 0.f};
-  for (int s0 = 0; s0 < KS; s0 += B) {
-    float2 ml[B], r[B];
+  const floatx4 o = merge_splits(KS, [&](int s0, floatx4(&ml)[MERGE_B], floatx4(&r)[MERGE_B]) {
 #pragma unroll
-    for (int v = 0; v < B; ++v) {
-      const float *row = row_of(min(s0 + v, KS - 1));
-      ml[v] = *(const float2 *)(row + 128);
-      r[v] = *(const float2 *)(row + d2);
+    for (int v = 0; v < MERGE_B; ++v) {
+      const float *row = p.part + (((size_t)h * p.max_splits + min(s0 + v, KS - 1)) * p.T_pad + t) * OROW;
+      ml[v] = *(const floatx4 *)(row + 128);
+      r[v] = *(const floatx4 *)(row + d4);
     }
-    float mb = -INFINITY;
-#pragma unroll
-    for (int v = 0; v < B; ++v)
-      if (s0 + v < KS) mb = fmaxf(mb, ml[v].x);
-    if (mb > M) {
-      const float f = exp2f(M - mb);  // 0 while M = -inf (nothing accumulated)
-      acc.x *= f;
-      acc.y *= f;
-      lsum *= f;
-      M = mb;
-    }
-#pragma unroll
-    for (int v = 0; v < B; ++v) {
-      if (s0 + v < KS) {
-        const float sc = ml[v].x == -INFINITY ? 0.f : exp2f(ml[v].x - M);
-        lsum += sc * ml[v].y;
-        acc.x += sc * r[v].x;
-        acc.y += sc * r[v].y;
-      }
-    }
-  }
-  const float inv = 1.f / lsum;
-  *(float2 *)(p.out + t * p.nh * 128 + h * 128 + d2) = make_float2(acc.x * inv, acc.y * inv);
+  });
+  *(floatx4 *)(p.out + t * p.nh * 128 + h * 128 + d4) = o;
 }
 
 }  // namespace
 
 hipError_t launch_attn_bf16(const AttnLaunch &a, hipStream_t s) {
-  const dim3 grid(a.wg0[a.sb.B]), block(512), mblock(256);
+  const dim3 grid(a.wg0[a.sb.B]), block(512), mblock(512);
   hipEvent_t ev0 = (hipEvent_t)a.ev_start, ev1 = (hipEvent_t)a.ev_stop;
   int max_ks = 1;
   for (int j = 0; j < a.sb.B; ++j) max_ks = std::max(max_ks, a.splits[j]);
-  hipEvent_t main_stop = max_ks > 1 ? nullptr : ev1;
+  const bool merge_kernel = max_ks > 1 && !a.xcd_merge;
+  hipEvent_t main_stop = merge_kernel ? nullptr : ev1;
   // one pair requested ahead: deeper rings put every workgroup's whole split
   // in flight at once, and the first pairs then arrive later (measured at
   // 7B: 19.2 us per layer with one pair ahead, 22.5 with five)
-  auto kernel = a.MT > 4 ? attn_bf16_kernel<2, 1> : attn_bf16_kernel<1, 1>;
+  auto kernel = a.xcd_merge ? (a.MT > 4 ? attn_bf16_kernel<2, 1, true> : attn_bf16_kernel<1, 1, true>)
+                            : (a.MT > 4 ? attn_bf16_kernel<2, 1, false> : attn_bf16_kernel<1, 1, false>);
   if (ev0)
     hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev0, main_stop, 0, a);
   else
     hipLaunchKernelGGL(kernel, grid, block, 0, s, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || max_ks == 1) return e;
-  const dim3 mgrid(a.nh * a.sb.B, a.MT, 4);
+  if (e != hipSuccess || !merge_kernel) return e;
+  const dim3 mgrid(a.nh * a.sb.B, a.MT, 1);
   if (ev1)
     hipExtLaunchKernelGGL(attn_merge_kernel, mgrid, mblock, 0, s, nullptr, ev1, 0, a);
   else

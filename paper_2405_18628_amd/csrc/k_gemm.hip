@@ -50,22 +50,6 @@ constexpr int FRAG = 64;  // u32x4 per packed operand fragment (1 KB)
 template <int KIND>
 constexpr int SUB = KIND == GEMM_SWIGLU ? 2 : 1;  // 16-row sub-tiles per group
 
-// buffer resource over a whole workspace region (raw, untyped loads)
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
-}
-// 16-byte load that misses L1 (sc0): data written by another compute unit of
-// this XCD is read from the shared L2
-__device__ __forceinline__ floatx4 load_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 1));
-}
-
-__device__ __forceinline__ unsigned xcc_id() {
-  unsigned v;
-  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
-  return v & 0xf;
-}
-
 __device__ __forceinline__ void amax_merge(float &v, int &i, float v2, int i2) {
   if (i2 >= 0 && (i < 0 || v2 > v || (v2 == v && i2 < i))) {
     v = v2;
@@ -132,14 +116,57 @@ __device__ __forceinline__ void rs_finish(const GemmLaunch &g, int tok0, const f
   if (tid < NT) rs_s[tok0 + tid] = rsqrtf((gs[tid] + gs[NT + tid]) * g.inv_h + g.eps);
 }
 
+// ---- inputs of an epilogue that come from memory, requested ahead of it
+// (one round trip, overlapped with the wait for the partial sums): the
+// residual rows (output / down projections) and the RoPE angles (QKV) of the
+// lane's rows and token
+template <int KIND, int GW>
+struct EpiIn {};
+template <int GW>
+struct EpiIn<GEMM_QKV, GW> {
+  floatx4 cs[GW][2];  // (cos, sin) of dims i0 .. i0 + 3
+};
+template <int GW>
+struct EpiIn<GEMM_RESID, GW> {
+  floatx4 x[GW];
+};
+
+template <int KIND, int GW>
+__device__ __forceinline__ void epi_load(const GemmLaunch &g, int ga, int gb, int mt, EpiIn<KIND, GW> &in,
+                                         unsigned gmask = ~0u) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tk = mt * 16 + (lane & 15);
+  if constexpr (KIND == GEMM_QKV) {
+#pragma unroll
+    for (int i = 0; i < GW; ++i) {
+      const int gs = ga + wave + 4 * i;
+      const int i0 = 8 * (gs & 7) + 4 * ((lane >> 4) & 1);
+      const bool use = ((gmask >> i) & 1u) && gs < gb && (gs >> 3) < g.nh + g.nkv;
+      const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)(use ? tk : 0) * 64 + (use ? i0 : 0));
+      in.cs[i][0] = rp[0];
+      in.cs[i][1] = rp[1];
+    }
+  } else if constexpr (KIND == GEMM_RESID) {
+#pragma unroll
+    for (int i = 0; i < GW; ++i) {
+      const int grp = ga + wave + 4 * i;
+      const int n = grp * 16 + (lane >> 4) * 4;
+      const bool use = grp < gb && n < g.N && tk < g.T;
+      in.x[i] = use ? *(const floatx4 *)(g.x + (size_t)tk * g.N + n) : floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+}
+
 // ---- epilogue of token block mt of tile gt (groups [ga, gb)), from the
 // complete sums a[i][q]: the lane holds rows 4 (lane / 16) + e of sub-tile q
 // of its wave's group i (group ga + wave + 4 i), token mt 16 + lane % 16.
-// Called by all threads (it has barriers); rs_s holds the row scales.
+// Called by all threads (it has barriers); rs_s holds the row scales, in the
+// inputs epi_load requested.
 template <int KIND, int GW>
 __device__ __forceinline__ void epilogue(const GemmLaunch &g, int gt, int ga, int gb, int mt,
                                          const floatx4 (&a)[GW][SUB<KIND>], const float *rs_s,
-                                         float (*red_s)[128][2], unsigned gmask = ~0u) {
+                                         float (*red_s)[128][2], const EpiIn<KIND, GW> &in,
+                                         unsigned gmask = ~0u) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, r4 = (lane >> 4) * 4;
   const int T = g.T, T_pad = g.MT * 16;
@@ -169,8 +196,7 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int gt, int ga, in
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] = a[i][0][e] * rs;
       if (hp < nh + nkv) {
-        const floatx4 *rp = (const floatx4 *)(g.rope + (size_t)tk * 64 + i0);
-        const floatx4 c0 = rp[0], c1 = rp[1];  // (cos, sin) of dims i0 .. i0 + 3
+        const floatx4 c0 = in.cs[i][0], c1 = in.cs[i][1];  // (cos, sin) of dims i0 .. i0 + 3
         const float cs[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -219,7 +245,7 @@ __device__ __forceinline__ void epilogue(const GemmLaunch &g, int gt, int ga, in
         const int grp = ga + wave + 4 * i;
         const int n = grp * 16 + r4;
         if (grp >= gb || n >= g.N) continue;
-        floatx4 xv = *(const floatx4 *)(g.x + (size_t)tk * g.N + n);
+        floatx4 xv = in.x[i];
         xv += a[i][0];
         *(floatx4 *)(g.x + (size_t)tk * g.N + n) = xv;
         sq += (xv[0] * xv[0] + xv[1] * xv[1]) + (xv[2] * xv[2] + xv[3] * xv[3]);
@@ -394,7 +420,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
       float v[4], lo[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        v[e] = __uint_as_float(da[r][e]) * gv[e];
+        // padding tokens (rows past T, whatever the workspace holds there)
+        // enter as zeros, so their sums are finite
+        v[e] = row < g.T ? __uint_as_float(da[r][e]) * gv[e] : 0.f;
         lo[e] = v[e] - bf16_to_f32(f32_to_bf16(v[e]));
       }
       const int off = row * 128 + swz(row, acol >> 3) * 16 + (acol & 7) * 2;
@@ -477,7 +505,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
       for (int i = 0; i < GW; ++i)
 #pragma unroll
         for (int q = 0; q < S; ++q) am[i][q] = acc[i][q][m];
-      epilogue<KIND, GW>(g, gt, ga, gb, m, am, rs_s, red_s);
+      EpiIn<KIND, GW> in;
+      epi_load<KIND, GW>(g, ga, gb, m, in);
+      epilogue<KIND, GW>(g, gt, ga, gb, m, am, rs_s, red_s, in);
     }
     return;
   }
@@ -496,42 +526,42 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
       for (int m = 0; m < MT; ++m)
         *(floatx4 *)(part + ((size_t)((wave * GW + i) * S + q) * MT + m) * 256 + lane * 4) = acc[i][q][m];
   }
+  constexpr bool kItems = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
+  // the items of token block m this slice finishes: QKV and gate/up deal the
+  // tile's (group, token block) items to the slices in turn (item i MT + m
+  // to slice (i MT + m) % s); the others keep whole token blocks together
+  // (their epilogues reduce over the tile's rows): token block m to slice
+  // m % s
+  auto mine = [&](int m) {
+    unsigned gm = 0;
+#pragma unroll
+    for (int i = 0; i < GW; ++i) gm |= (kItems ? (i * MT + m) % s == ks : m % s == ks) ? 1u << i : 0u;
+    return gm;
+  };
+  // the epilogue inputs of this slice's first token block, requested now:
+  // they arrive while the partial sums are stored and the slices meet
+  int m0 = -1;
+  unsigned gm0 = 0;
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+    if (m0 < 0 && mine(m)) {
+      m0 = m;
+      gm0 = mine(m);
+    }
+  EpiIn<KIND, GW> in0;
+  if (m0 >= 0) epi_load<KIND, GW>(g, ga, gb, m0, in0, gm0);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have reached L2
   __syncthreads();
-  if (tid == 0) {
-    // Arrival: 1 + 256 o, o = (this XCD - x) mod 8, the dispatcher's offset
-    // (round-robin from wherever the previous dispatch left it: the same
-    // for every workgroup of this one, so the slices of a tile share an XCD
-    // whatever o is).  The counter is read at agent scope: a workgroup-scope
-    // load may be served by this compute unit's L1, which keeps the line of
-    // the first poll.
-    const uint32_t o = (xcc_id() - (unsigned)x) & 7u;
-    uint32_t *ctr = g.ctr + x * 32 + t;  // one 128-byte line of counters per group of XCD slots
-    __hip_atomic_fetch_add(ctr, 1u + (o << 8), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    int it = 0;
-    uint32_t v;
-    while (((v = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffu) <
-           (uint32_t)s) {
-      if (++it > g.spin_limit) {
-        atomicOr(g.status, PPD_DEV_SYNC_TIMEOUT);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-    if ((v >> 8) != o * (uint32_t)s) atomicOr(g.status, PPD_DEV_XCD_PLACEMENT);
-  }
+  // one 128-byte line of counters per group of XCD slots
+  if (tid == 0) xcd_arrive_wait(g.ctr + x * 32 + t, x, (uint32_t)s, g.spin_limit, g.status);
   __syncthreads();
   const float *tile_part = g.part + (size_t)gt * s * (4 * PW * 64 * 4);
   const __amdgpu_buffer_rsrc_t rp = rsrc_of(tile_part, (uint32_t)s * 4 * PW * 64 * 16);
   // the slices' partials are requested SB at a time (one round trip per
   // batch; past the last slice the loads repeat slice 0 and are not added)
-  // and added in slice order.  QKV and gate/up: the tile's (group, token
-  // block) items are dealt to the slices in turn (item i MT + m to slice
-  // (i MT + m) % s); the others keep whole token blocks together (their
-  // epilogues reduce over the tile's rows): token block m to slice m % s.
+  // and added in slice order
   constexpr int SB = GW * S <= 2 ? 8 : 4;
-  constexpr bool kItems = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
   auto finish_block = [&](int m, unsigned gmask) {
     floatx4 am[GW][S];
 #pragma unroll
@@ -561,14 +591,17 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
             for (int q = 0; q < S; ++q) am[i][q] += buf[b][i][q];
         }
     }
-    epilogue<KIND, GW>(g, gt, ga, gb, m, am, rs_s, red_s, gmask);
+    EpiIn<KIND, GW> in;
+    if (m == m0)
+      in = in0;
+    else
+      epi_load<KIND, GW>(g, ga, gb, m, in, gmask);
+    epilogue<KIND, GW>(g, gt, ga, gb, m, am, rs_s, red_s, in, gmask);
   };
   if constexpr (kItems) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-      unsigned gmask = 0;
-#pragma unroll
-      for (int i = 0; i < GW; ++i) gmask |= ((i * MT + m) % s == ks) ? 1u << i : 0u;
+      const unsigned gmask = mine(m);
       if (gmask) finish_block(m, gmask);  // uniform: no barriers in these epilogues
     }
   } else {

@@ -1,26 +1,46 @@
 // Small kernels of the verification step: embedding gather, rotary tables,
 // final greedy argmax, acceptance, KV compaction and workspace reset.
+#include <algorithm>
+
 #include "ppd_internal.h"
 
 // ---------------------------------------------------------------------------
-// Embedding (Section 3: prompt tokens are trained embeddings appended to the
-// input).  Row t of the residual stream x is the embedding of ids[t]; for
-// bf16 models the kernel also writes the row's sum of squares (the first
-// RMSNorm's one partial per row; its x * gain is formed by the consumer
-// GEMM) and, spread over the blocks, zeroes the step's GEMM tile counters.
-// Rows T..T_pad-1 are zero.
+// Embedding and rotary tables, one launch.  Row t of the residual stream x
+// is the embedding of ids[t] (Section 3: prompt tokens are trained
+// embeddings appended to the input); for bf16 models the kernel also writes
+// the row's sum of squares (the first RMSNorm's one partial per row; its
+// x * gain is formed by the consumer GEMM) and, spread over the blocks,
+// zeroes the step's tile and head counters.  Rows T..T_pad-1 are zero.
+// Rotary table row t: node t sits at position L + depth[t] (Section 3.1);
+// the angle of frequency i is pos * base^(-2i/d), evaluated in double
+// precision and rounded to float; padding rows get position 0.  Rows of a
+// width that is a multiple of 16 bytes are read 16 bytes at a time.
 
 template <typename WT>
 __global__ __launch_bounds__(256) void embed_kernel(const WT *__restrict__ tok_emb,
                                                     const WT *__restrict__ prompt_emb,
-                                                    const int32_t *__restrict__ ids, int T,
+                                                    const int32_t *__restrict__ ids,
+                                                    const int32_t *__restrict__ depth, SeqBatch sb,
+                                                    int d, float base, float2 *__restrict__ rope,
                                                     int vocab, int n_prompt, int H,
                                                     float *__restrict__ x, float *__restrict__ ss,
                                                     uint32_t *__restrict__ ctr, size_t n_ctr,
                                                     uint32_t *status) {
-  const int t = blockIdx.x;
+  const int t = blockIdx.x, T = sb.t0[sb.B];
   for (size_t i = (size_t)t * blockDim.x + threadIdx.x; i < n_ctr; i += (size_t)gridDim.x * blockDim.x)
     ctr[i] = 0u;
+  // rotary row t
+  {
+    int L = sb.L[0];  // the cached length of token t's sequence
+    for (int j = 1; j < sb.B; ++j) L = t >= sb.t0[j] ? sb.L[j] : L;
+    for (int i = threadIdx.x; i < d / 2; i += blockDim.x) {
+      const double pos = t < T ? (double)L + (double)depth[t] : 0.0;
+      const double inv = exp(-(2.0 * i / d) * log((double)base));
+      double sn, c;
+      sincos(pos * inv, &sn, &c);
+      rope[(size_t)t * (d / 2) + i] = make_float2((float)c, (float)sn);
+    }
+  }
   float *xr = x + (size_t)t * H;
   if (t >= T) {
     for (int k = threadIdx.x; k < H; k += blockDim.x) xr[k] = 0.f;
@@ -33,16 +53,41 @@ __global__ __launch_bounds__(256) void embed_kernel(const WT *__restrict__ tok_e
     id = 0;
   }
   const WT *src = id < vocab ? tok_emb + (size_t)id * H : prompt_emb + (size_t)(id - vocab) * H;
+  // 16-byte pieces, several in flight per thread (rows of any other width:
+  // one element at a time)
+  constexpr int E = 16 / sizeof(WT);
   float acc = 0.f;
-  for (int k = threadIdx.x; k < H; k += blockDim.x) {
-    float v;
-    if constexpr (sizeof(WT) == 2) {
-      v = bf16_to_f32(src[k]);
-    } else {
-      v = src[k];
+  if (H % E) {
+    for (int k = threadIdx.x; k < H; k += blockDim.x) {
+      float v;
+      if constexpr (sizeof(WT) == 2) {
+        v = bf16_to_f32(src[k]);
+      } else {
+        v = src[k];
+      }
+      xr[k] = v;
+      acc += v * v;
     }
-    xr[k] = v;
-    acc += v * v;
+  }
+#pragma unroll 4
+  for (int c = threadIdx.x; H % E == 0 && c < H / E; c += blockDim.x) {
+    const u32x4 w = *(const u32x4 *)(src + (size_t)c * E);
+    float v[E];
+    if constexpr (sizeof(WT) == 2) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[2 * e] = bf16_to_f32(w[e] & 0xffffu);
+        v[2 * e + 1] = bf16_to_f32(w[e] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(w[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < E; e += 4) {
+      *(floatx4 *)(xr + (size_t)c * E + e) = floatx4{v[e], v[e + 1], v[e + 2], v[e + 3]};
+      acc += (v[e] * v[e] + v[e + 1] * v[e + 1]) + (v[e + 2] * v[e + 2] + v[e + 3] * v[e + 3]);
+    }
   }
   if (ss) {
     __shared__ float red[4];
@@ -54,46 +99,19 @@ __global__ __launch_bounds__(256) void embed_kernel(const WT *__restrict__ tok_e
 }
 
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
-                        int T, int vocab, int n_prompt, int H, float *x, float *ss, uint32_t *ctr,
+                        const int32_t *depth, const SeqBatch &sb, int d, float base, float2 *rope,
+                        int vocab, int n_prompt, int H, float *x, float *ss, uint32_t *ctr,
                         size_t n_ctr, uint32_t *status, hipStream_t s) {
-  int T_pad = (T + 15) & ~15;
+  const int T_pad = (sb.t0[sb.B] + 15) & ~15;
   if (dtype == PPD_BF16) {
-    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(T_pad), dim3(256), 0, s,
-                       (const bf16_t *)tok_emb, (const bf16_t *)prompt_emb, ids, T, vocab,
-                       n_prompt, H, x, ss, ctr, n_ctr, status);
+    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(T_pad), dim3(256), 0, s, (const bf16_t *)tok_emb,
+                       (const bf16_t *)prompt_emb, ids, depth, sb, d, base, rope, vocab, n_prompt, H, x,
+                       ss, ctr, n_ctr, status);
   } else {
-    hipLaunchKernelGGL(embed_kernel<float>, dim3(T_pad), dim3(256), 0, s,
-                       (const float *)tok_emb, (const float *)prompt_emb, ids, T, vocab, n_prompt,
-                       H, x, (float *)nullptr, (uint32_t *)nullptr, (size_t)0, status);
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(T_pad), dim3(256), 0, s, (const float *)tok_emb,
+                       (const float *)prompt_emb, ids, depth, sb, d, base, rope, vocab, n_prompt, H, x,
+                       (float *)nullptr, (uint32_t *)nullptr, (size_t)0, status);
   }
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// Rotary tables: node t sits at position L + depth[t] (Section 3.1); the
-// angle of frequency i is pos * base^(-2i/d), evaluated in double precision
-// and rounded to float.  Padding rows get position 0.
-
-__global__ void rope_table_kernel(const int32_t *__restrict__ depth, SeqBatch sb, int d,
-                                  float base, float2 *__restrict__ rope) {
-  const int t = blockIdx.x;
-  const int half = d / 2;
-  int L = sb.L[0];  // the cached length of token t's sequence
-  for (int j = 1; j < sb.B; ++j) L = t >= sb.t0[j] ? sb.L[j] : L;
-  const int T = sb.t0[sb.B];
-  for (int i = threadIdx.x; i < half; i += blockDim.x) {
-    double pos = t < T ? (double)L + (double)depth[t] : 0.0;
-    double inv = exp(-(2.0 * i / d) * log((double)base));
-    double s, c;
-    sincos(pos * inv, &s, &c);
-    rope[(size_t)t * half + i] = make_float2((float)c, (float)s);
-  }
-}
-
-hipError_t launch_rope_table(const int32_t *depth, const SeqBatch &sb, int d, float base,
-                             float2 *rope, hipStream_t s) {
-  int T_pad = (sb.t0[sb.B] + 15) & ~15;
-  hipLaunchKernelGGL(rope_table_kernel, dim3(T_pad), dim3(64), 0, s, depth, sb, d, base, rope);
   return hipGetLastError();
 }
 

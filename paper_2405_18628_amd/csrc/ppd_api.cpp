@@ -202,6 +202,20 @@ void attn_splits(const ppd_model *m, int L, int T, int *splits, int *chunk) {
   *chunk = c;
 }
 
+// One sequence on 256 CUs: the heads are dealt to the 8 XCDs (at most
+// ceil(nh / 8) per XCD) and each head's splits take that XCD's 32 CUs
+// together (they merge through its L2), so a head gets up to
+// 32 / ceil(nh / 8) splits.  Returns the workgroup count (8 x heads per XCD
+// x splits).
+int attn_splits_xcd(const ppd_model *m, int L, int T, int *splits, int *chunk) {
+  const int nblk = (L + T + 31) / 32, hpx = (m->n_heads + 7) / 8;
+  const int ks = std::max(1, std::min(std::min(PPD_ATTN_MAX_SPLITS, 32 / hpx), nblk / 4));
+  const int c = ((nblk + ks - 1) / ks + 1) & ~1;  // even: splits start on 64-key pairs
+  *splits = (nblk + c - 1) / c;
+  *chunk = c;
+  return 8 * hpx * *splits;
+}
+
 WsLayout layout_of(const ppd_model *m, int T) {
   WsLayout w{};
   const int Tp = t_pad_of(T);
@@ -249,8 +263,9 @@ WsLayout layout_of(const ppd_model *m, int T) {
   w.gemm_part = take(part);
   w.amax = take(sizeof(float2) * w.max_amax_tiles * Tp);
   w.rope = take(sizeof(float2) * Tp * (d / 2));
-  // tile counters: one 1 KB block (8 XCDs x one 128-byte line) per GEMM launch
-  w.n_ctr = bf16 ? (size_t)(4 * m->n_layers + 1) * 256 : 0;
+  // counters: one 1 KB block (8 XCDs x one 128-byte line) per GEMM launch
+  // (tiles) and per attention launch (heads)
+  w.n_ctr = bf16 ? (size_t)(5 * m->n_layers + 1) * 256 : 0;
   w.ctr = take(sizeof(uint32_t) * w.n_ctr);
   w.total = off;
   return w;
@@ -326,17 +341,25 @@ ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t
     g.ctr = ctr + (size_t)launch++ * 256;
   };
 
-  PPD_TRY_HIP(launch_rope_table(depth, seq_batch(m, B, kvs, Ls, Ts, 0), m->head_dim,
-                                m->rope_base, rope, s));
-  // embedding, its sum of squares (one partial per row), zeroed counters
-  PPD_TRY_HIP(launch_embed(PPD_BF16, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
-                           x, ss, ctr, w.n_ctr, status, s));
+  // embedding, its sum of squares (one partial per row), rotary table,
+  // zeroed counters
+  PPD_TRY_HIP(launch_embed(PPD_BF16, m->tok_emb, m->prompt_emb, ids, depth,
+                           seq_batch(m, B, kvs, Ls, Ts, 0), m->head_dim, m->rope_base, rope,
+                           m->vocab, m->n_prompt, H, x, ss, ctr, w.n_ctr, status, s));
   int n_ss = 1;
   // attention work per sequence: nh x splits workgroups
+  // (one sequence on 256 CUs: heads dealt to the XCDs, splits merged in the
+  // kernel; a batch: a merge kernel)
   int splits[PPD_BATCH_MAX], chunk[PPD_BATCH_MAX], wg0[PPD_BATCH_MAX + 1] = {0};
-  for (int j = 0; j < B; ++j) {
-    attn_splits(m, Ls[j], Ts[j], &splits[j], &chunk[j]);
-    wg0[j + 1] = wg0[j] + nh * splits[j];
+  const bool xcd_merge = B == 1 && sync && nh <= 256;
+  uint32_t *attn_ctr = ctr + (size_t)(4 * m->n_layers + 1) * 256;
+  if (xcd_merge) {
+    wg0[1] = attn_splits_xcd(m, Ls[0], Ts[0], &splits[0], &chunk[0]);
+  } else {
+    for (int j = 0; j < B; ++j) {
+      attn_splits(m, Ls[j], Ts[j], &splits[j], &chunk[j]);
+      wg0[j + 1] = wg0[j] + nh * splits[j];
+    }
   }
   const float inv_h = 1.0f / (float)H;
 
@@ -383,6 +406,10 @@ ppd_status step_bf16(const ppd_model *m, int B, const ppd_kv *kvs, const int32_t
       a.chunk[j] = chunk[j];
     }
     for (int j = 0; j <= B; ++j) a.wg0[j] = wg0[j];
+    a.xcd_merge = xcd_merge;
+    a.ctr = attn_ctr + (size_t)l * 256;
+    a.spin_limit = kSpinLimit;
+    a.status = status;
     a.scale_log2 = (float)(1.4426950408889634 / std::sqrt(128.0));
     timer_events(TK_ATTN, &a.ev_start, &a.ev_stop);
     PPD_TRY_HIP(launch_attn_bf16(a, s));
@@ -461,9 +488,8 @@ ppd_status step_f32(const ppd_model *m, const ppd_kv *kv, int L, int T, const in
   one.B = 1;
   one.t0[1] = T;
   one.L[0] = L;
-  PPD_TRY_HIP(launch_rope_table(depth, one, d, m->rope_base, rope, s));
-  PPD_TRY_HIP(launch_embed(PPD_F32, m->tok_emb, m->prompt_emb, ids, T, m->vocab, m->n_prompt, H,
-                           x, nullptr, nullptr, 0, status, s));
+  PPD_TRY_HIP(launch_embed(PPD_F32, m->tok_emb, m->prompt_emb, ids, depth, one, d, m->rope_base, rope,
+                           m->vocab, m->n_prompt, H, x, nullptr, nullptr, 0, status, s));
   for (int l = 0; l < m->n_layers; ++l) {
     float *kc = (float *)kv->k + (size_t)l * nkv * cap * d;
     float *vc = (float *)kv->v + (size_t)l * nkv * d * cap;

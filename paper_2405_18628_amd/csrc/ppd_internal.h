@@ -40,6 +40,49 @@ __device__ __forceinline__ floatx4 mfma16x16x32(bf16x8 a, bf16x8 b, floatx4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// buffer resource over a whole workspace region (raw, untyped loads)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte load at device scope (sc1): it misses this compute unit's L1 and
+// is served by the XCD's L2, where another compute unit of the XCD stored
+// the data
+__device__ __forceinline__ floatx4 load_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 16));
+}
+
+// the XCD this wave runs on
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 0xf;
+}
+
+// Arrival at an XCD-local counter shared by n workgroups of one dispatch
+// (one thread per workgroup, after its results have reached L2), then a
+// bounded wait for the other n - 1.  Workgroup b runs on XCD (b + o) % 8, o
+// being the dispatcher's offset (round-robin from wherever the previous
+// dispatch left it: the same for every workgroup of this one), so each
+// arrival adds 1 + 256 o, o = (this XCD - set) mod 8; a final count whose
+// high part is not n o means the workgroups did not share an XCD.  Agent
+// scope: a workgroup-scope load may be served by this compute unit's L1,
+// which keeps the line of the first poll.
+__device__ __forceinline__ void xcd_arrive_wait(uint32_t *ctr, int set, uint32_t n, int spin_limit,
+                                                uint32_t *status) {
+  const uint32_t o = (xcc_id() - (unsigned)set) & 7u;
+  __hip_atomic_fetch_add(ctr, 1u + (o << 8), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  int it = 0;
+  uint32_t v;
+  while (((v = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) & 0xffu) < n) {
+    if (++it > spin_limit) {
+      atomicOr(status, PPD_DEV_SYNC_TIMEOUT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+  if ((v >> 8) != o * n) atomicOr(status, PPD_DEV_XCD_PLACEMENT);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, PPD_WAVE);
@@ -72,7 +115,7 @@ struct WsLayout {
   size_t gemm_part;   // float  [max_part_floats]
   size_t amax;        // float2 [max_amax_tiles][T_pad]
   size_t rope;        // float2 [T_pad][d/2]      (cos, sin)
-  size_t ctr;         // uint32 [n_ctr]           GEMM tile counters (zeroed per step)
+  size_t ctr;         // uint32 [n_ctr]           tile / head counters (zeroed per step)
   size_t n_ctr;
   size_t total;
   int max_ss, max_splits, max_amax_tiles;
@@ -165,6 +208,15 @@ struct AttnLaunch {
   // sequence s: workgroups [wg0[s], wg0[s + 1]) = nh x splits[s], chunk[s]
   // 32-key blocks per split
   int wg0[PPD_BATCH_MAX + 1], splits[PPD_BATCH_MAX], chunk[PPD_BATCH_MAX];
+  // xcd_merge (one sequence): the heads are dealt to the 8 XCDs (XCD x:
+  // heads [nh x / 8, nh (x + 1) / 8), workgroup b runs on XCD b % 8, slot
+  // b / 8 = local head splits + split), and each head's splits merge inside
+  // the kernel through L2 behind the head's counter, ctr + 32 x + local head
+  // (zeroed per step); otherwise a merge kernel adds them
+  int xcd_merge;
+  uint32_t *ctr;
+  int spin_limit;
+  uint32_t *status;
   float scale_log2;     // log2(e) / sqrt(d)
   void *ev_start, *ev_stop;  // optional events at the first dispatch's start / last one's end
 };
@@ -191,13 +243,13 @@ hipError_t launch_next_tree(const NextTreeLaunch &p, int n_depths, hipStream_t s
 // records the thread's error message (ppd_last_error) and returns s
 ppd_status ppd_fail(ppd_status s, const char *fmt, ...);
 
-// embedding rows into x (fp32), rows T..T_pad-1 zero; bf16 models also write
-// each row's sum of squares to ss and zero the n_ctr GEMM tile counters
+// embedding rows into x (fp32), rows T..T_pad-1 zero, and the rotary
+// table [T_pad][d / 2] (cos, sin); bf16 models also write each row's sum of
+// squares to ss and zero the n_ctr tile / head counters
 hipError_t launch_embed(int dtype, const void *tok_emb, const void *prompt_emb, const int32_t *ids,
-                        int T, int vocab, int n_prompt, int H, float *x, float *ss, uint32_t *ctr,
+                        const int32_t *depth, const SeqBatch &sb, int d, float base, float2 *rope,
+                        int vocab, int n_prompt, int H, float *x, float *ss, uint32_t *ctr,
                         size_t n_ctr, uint32_t *status, hipStream_t s);
-hipError_t launch_rope_table(const int32_t *depth, const SeqBatch &sb, int d, float base, float2 *rope,
-                             hipStream_t s);
 hipError_t launch_argmax_final(const float2 *amax, int n_tiles, int T, int T_pad, int32_t *pred,
                                uint32_t *status, hipStream_t s);
 hipError_t launch_accept(int T, const int32_t *parent, const int32_t *ids, const int32_t *pred,
