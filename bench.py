@@ -3,6 +3,7 @@
     python bench.py [--steps K] [--warmup W] [--workload 7b] [--T 64] [--graph]
     python bench.py --sweep [--workload 13b]     # hardware-aware tree size
     python bench.py --batch-sweep                # several sequences per step
+    python bench.py --stream-ceiling             # plain HBM read rates
 
 A step is one pass of the whole hot path on one synthetic batch:
 ppd_verify_step (forward over the T tree nodes, fp32 logits, greedy tokens)
@@ -23,6 +24,19 @@ then acceptance and compaction per sequence) for B = 1, 2, 4, 8 and T_s =
 16, 32, next to vanilla batches (T_s = 1), and prints one JSON line each:
 the speedup of PPD over vanilla decoding at the same batch size is
 tau(T_s) x L(vanilla, B) / L(PPD, B).
+
+The default line also times a planted-path step: the model's own greedy
+continuation is planted along the deepest candidate chain of the same tree
+(a node's id = its parent's greedy token), so acceptance takes that whole
+chain and the compaction moves its rows inside the timed region; emitted
+tokens per second there are the accepted tokens per step over its latency.
+kernel_us are per-dispatch event times (each dispatch's own start to end,
+start-up included), so they do not add up to the step.
+
+--stream-ceiling reads 14.3 GB (the 7B step's algorithmic bytes) with the
+library's read probe: as four launches over a 3.6 GB buffer, and as 80
+launches over 179 MB slices (a gate/up weight), and prints the achieved
+read rates next to the 8 TB/s peak.
 
 The default workload is the Vicuna-7B-shaped decoder (32 layers, hidden 4096,
 32 heads x 128, ffn 11008, vocab 32000, bf16, random weights) with a
@@ -88,6 +102,8 @@ def main():
                     help="tree-size sweep: L_fp(T) of the best sparse trees and the speedup")
     ap.add_argument("--batch-sweep", action="store_true",
                     help="batched steps: B sequences per step, PPD against vanilla")
+    ap.add_argument("--stream-ceiling", action="store_true",
+                    help="plain HBM read rates (reductions over 14.3 GB)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (calibrates the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -100,6 +116,9 @@ def main():
     import numpy as np
     import torch
 
+    if args.stream_ceiling:
+        stream_ceiling()
+        return
     if args.copy_bytes:
         n = args.copy_bytes // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -262,6 +281,37 @@ def main():
     ppd.ppd_set_kernel_timer("next_tree")
     del keep
 
+    # planted path: the greedy continuation along the deepest candidate's
+    # root path (changing a node leaves its ancestors' logits alone, so the
+    # chain is planted top-down, one verify per node, untimed)
+    depth_h = depth
+    cand = [i for i in range(T) if tree.ids[i] < sh.vocab]
+    deep = max(cand, key=lambda i: depth_h[i])
+    chain = [deep]
+    while chain[-1] != 0:
+        chain.append(int(tree.parent[chain[-1]]))
+    chain = chain[::-1]
+    ids_p = tree.ids.copy()
+    for node in chain[1:]:
+        ppd.ppd_verify_step(model, kv, L, T, todev(ids_p), dep_d, mask_d, ws, logits, pred)
+        ids_p[node] = int(pred[int(tree.parent[node])].item())
+    ids_pd = todev(ids_p)
+
+    def planted_step():
+        ppd.ppd_verify_step(model, kv, L, T, ids_pd, dep_d, mask_d, ws, logits, pred)
+        ppd.ppd_accept(T, par_d, ids_pd, pred, sh.vocab, path, n_path, nxt, ws)
+        ppd.ppd_kv_compact(model, kv, L, path, n_path)
+    for _ in range(args.warmup):
+        planted_step()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        planted_step()
+    e1.record()
+    torch.cuda.synchronize()
+    planted_ms = e0.elapsed_time(e1) / args.steps
+    planted_n = int(n_path.item())
+
     alg = step_bytes(sh, L, T, n_acc)
     flops = step_flops(sh, L, T)
     gu_us = kernels["gate_up"]
@@ -291,7 +341,11 @@ def main():
         "step_us_p10_p50_p90": [round(float(np.percentile(per_step_us, q)), 1) for q in (10, 50, 90)],
         "tree_tokens_per_s": round(T / (ms * 1e-3), 1),
         "emitted_tokens_per_s": round(n_acc / (ms * 1e-3), 1),
+        "planted_path": {"accepted_per_step": planted_n, "chain_nodes": len(chain),
+                         "step_us": round(planted_ms * 1e3, 1),
+                         "emitted_tokens_per_s": round(planted_n / (planted_ms * 1e-3), 1)},
         "kernel_us": {k2: round(v2, 2) for k2, v2 in kernels.items()},
+        "kernel_us_note": "per-dispatch HIP events (start-up included; not additive)",
         "next_tree_us": round(next_us, 2),
         "next_tree_ept2_us": round(next_ept_us, 2),
         "device_status": status,
@@ -491,53 +545,108 @@ def recorded_traffic(workload_name, T, L):
 
 
 def cpu_baseline(sh, W, k, v, L, tree, n_sample):
-    """The oracle (float64 numpy, BLAS threads = host cores) on a bounded
-    sample of the same step: forward + acceptance over the same tree with
-    n_sample/2 and n_sample of the model's decoder layers (plus embedding and
-    LM head), each repeated for about 6 s; the per-layer cost is scaled to
-    the full layer count.  Weights
-    and caches are copied from the device and converted to float64 before
-    timing.  Returns the estimated full-step latency in us."""
+    """The oracle (float64 numpy, BLAS threads = host cores) on the same step:
+    the full-depth forward + acceptance over the same tree and cache, median
+    of 3 runs (the weights and caches are copied from the device and
+    converted to float64 before timing; n_sample is unused: the whole step
+    is the sample).  Beside it, single-thread latencies of the oracle on the
+    tiny fp32 decoder and the MobileLLaMA-1.4B shape (configurations 0 and 1
+    with their own trees and caches), one run each after a warm-up run for
+    the tiny one."""
     import numpy as np
     import oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=os.cpu_count())
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count()
-    half = max(1, n_sample // 2)
-    times, reps = {}, {}
-    for n in (half, n_sample):
-        Wn = {key: W[key] for key in ("tok_emb", "prompt_emb", "final_norm", "lm_head")}
-        Wn["layers"] = W["layers"][:n]
-        m = O.Model(sh.with_layers(n), Wn, keep_layers=True)
-        for l in range(n):
-            m.layer(l)
-        _ = m.lm_head
-        kc = [O.to_f64(k[l, :, :L, :]) for l in range(n)]
-        vc = [O.to_f64(v[l, :, :, :L]).transpose(0, 2, 1) for l in range(n)]
-        runs = []
-        while True:  # repeat the sample until about 6 s of CPU time per size
-            t0 = time.perf_counter()
-            res = O.verify_forward(m, kc, vc, L, tree.ids, tree.parent, sh.dtype)
-            pred = O.argmax_first(res["logits"])
-            O.accept(tree.parent, tree.ids, pred, sh.vocab)
-            runs.append(time.perf_counter() - t0)
-            if sum(runs) >= 6.0 or len(runs) >= 50:
-                break
-        times[n] = sum(runs) / len(runs)
-        reps[n] = len(runs)
-        del m, kc, vc, res
-    per_layer = (times[n_sample] - times[half]) / (n_sample - half)
-    fixed = max(0.0, times[half] - half * per_layer)
-    est = fixed + sh.n_layers * per_layer
-    return {"value": round(est * 1e6, 1), "unit": "us", "cores": int(cores), "kind": "oracle",
-            "sample": (f"oracle forward+accept over the same {tree.T}-node tree and {L}-token "
-                       f"cache with {half} and {n_sample} of the {sh.n_layers} decoder layers "
-                       f"(+ embedding, LM head), mean of {reps[half]} and {reps[n_sample]} runs: "
-                       f"{times[half]:.2f} s and {times[n_sample]:.2f} s per run; per-layer "
-                       f"cost scaled to {sh.n_layers} layers")}
+    from threadpoolctl import threadpool_info, threadpool_limits
+    cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=os.cpu_count())
 
+    def timed(shape, Wd, kd, vd, Ld, tr, runs):
+        m = O.Model(shape, Wd, keep_layers=True)
+        for l in range(shape.n_layers):
+            m.layer(l)
+            if l % 8 == 7:
+                print(f"[bench] oracle {shape.name}: {l + 1} layers converted", file=sys.stderr, flush=True)
+        _ = m.lm_head
+        kc = [O.to_f64(kd[l, :, :Ld, :]) for l in range(shape.n_layers)]
+        vc = [O.to_f64(vd[l, :, :, :Ld]).transpose(0, 2, 1) for l in range(shape.n_layers)]
+        out = []
+        for _ in range(runs):
+            t0 = time.perf_counter()
+            res = O.verify_forward(m, kc, vc, Ld, tr.ids, tr.parent, shape.dtype)
+            pred = O.argmax_first(res["logits"])
+            O.accept(tr.parent, tr.ids, pred, shape.vocab)
+            out.append(time.perf_counter() - t0)
+            print(f"[bench] oracle {shape.name}: run {len(out)} {out[-1]:.2f} s", file=sys.stderr, flush=True)
+        del m, kc, vc
+        return out
+
+    full = timed(sh, W, k, v, L, tree, 3)
+    single = {}
+    with threadpool_limits(1):
+        from synth import workload
+        from synth.model import empty_kv, fill_kv_normal, make_weights
+        from synth.trees import make_tree
+        for name in ("tiny", "1.4b"):
+            wl = workload(name)
+            shp = wl.shape
+            Wt = make_weights(shp, wl.seeds["weights"], device="cpu")
+            kt, vt = empty_kv(shp, wl.cache_len + 64, device="cpu")
+            fill_kv_normal(kt, vt, wl.cache_len, wl.seeds["kv"])
+            tr = make_tree(wl.tree, shp.vocab, shp.n_prompt, wl.max_depth, wl.seeds["tree"], 1,
+                           wl.max_fanout)
+            r = timed(shp, Wt, kt, vt, wl.cache_len, tr, 2 if name == "tiny" else 1)
+            single[shp.name] = {"us": round(r[-1] * 1e6, 1), "tree_tokens": tr.T,
+                                "cache_len": wl.cache_len, "layers": shp.n_layers}
+            del Wt, kt, vt
+    return {"value": round(float(np.median(full)) * 1e6, 1), "unit": "us", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"the whole step: oracle forward over all {sh.n_layers} decoder layers + "
+                       f"acceptance, the same {tree.T}-node tree and {L}-token cache, median of 3 "
+                       f"runs ({', '.join(f'{t:.2f}' for t in full)} s)"),
+            "single_thread_us": single}
+
+
+def stream_ceiling():
+    """Plain read rates of HBM with the library's read probe (one workgroup
+    per compute unit streaming its contiguous piece with 16-byte
+    non-temporal loads): 14.3 GB read as four launches over one 3.6 GB
+    buffer, and as 80 launches over 179 MB slices of it (the size of a
+    gate/up weight, launched back to back like the step's kernels); each
+    timed with events around the launches, median of repeats."""
+    import numpy as np
+    import torch
+    import paper_2405_18628_amd as ppd
+    n = 900 * (1 << 20)  # floats: 3.77 GB
+    buf = torch.ones(n, dtype=torch.float32, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sl = 179 * (1 << 20) // 4
+    nsl = n // sl
+
+    def rate(fn, nbytes, reps):
+        ts = []
+        for _ in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e-3)
+        return nbytes / float(np.median(ts[1:])) / 1e9
+
+    def big():
+        for _ in range(4):
+            ppd.ppd_read_probe(buf, sink)
+
+    def chain():
+        for i in range(80):
+            ppd.ppd_read_probe(buf[(i % nsl) * sl:(i % nsl + 1) * sl], sink)
+    r_big = rate(big, 4 * n * 4, 3)
+    r_chain = rate(chain, 80 * sl * 4, 3)
+    print(json.dumps({"stream_ceiling": {"big_launch_gbs": round(r_big, 1), "big_launch_bytes": n * 4,
+                                         "chain_80x179MB_gbs": round(r_chain, 1),
+                                         "chain_launch_bytes": sl * 4, "peak_gbs": HBM_PEAK_GBS,
+                                         "big_frac": round(r_big / HBM_PEAK_GBS, 4),
+                                         "chain_frac": round(r_chain / HBM_PEAK_GBS, 4),
+                                         "method": "ppd_read_probe launches, HIP events"}}),
+          flush=True)
 
 if __name__ == "__main__":
     main()

@@ -373,6 +373,17 @@ ppd_status ppd_sparse_template(const double *p_table, int32_t depth_max, int32_t
 ppd_status ppd_set_kernel_timer(int32_t kind, void *const *start_events, void *const *stop_events,
                                 int32_t n_events);
 
+/*
+ * Measurement aid, not needed for correctness: the practical HBM read rate
+ * the step's weight streams are compared with.  One launch of 256
+ * workgroups (one per compute unit, 16-byte non-temporal loads, several in
+ * flight per thread) reads `bytes` bytes of device buffer `buf` once
+ * (`bytes` a multiple of 16, buf 16-byte aligned) and writes a 32-bit XOR of
+ * everything read to device `sink` (so the loads cannot be dropped).
+ * Enqueued on `stream`; PPD_EINVAL for a null pointer or a misaligned size.
+ */
+ppd_status ppd_read_probe(const void *buf, size_t bytes, uint32_t *sink, void *stream);
+
 /* Synchronously read (and optionally clear) the workspace status word. */
 ppd_status ppd_device_status(void *ws, size_t ws_bytes, uint32_t *status_out, int32_t clear,
                              void *stream);

@@ -88,8 +88,9 @@ def lib() -> C.CDLL:
         L.ppd_packed_weight_bytes.argtypes = [i32, i32, i32]
         L.ppd_packed_weight_bytes.restype = sz
         L.ppd_pack_weight.argtypes = [i32, i32, i32, vp, vp, vp]
+        L.ppd_read_probe.argtypes = [vp, sz, vp, vp]
         for f in ("ppd_verify_step_static", "ppd_next_tree", "ppd_sparse_template", "ppd_verify_batch", "ppd_pack_weight", "ppd_workspace_init", "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept",
-                  "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer"):
+                  "ppd_kv_compact", "ppd_device_status", "ppd_set_kernel_timer", "ppd_read_probe"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -363,6 +364,14 @@ def ppd_device_status(ws, clear: bool = False, stream=None) -> int:
     return int(out.value)
 
 
+def ppd_read_probe(buf, sink, stream=None):
+    """One read of the whole device tensor buf by the HBM read probe; the XOR
+    of what it read lands in the device uint32 tensor sink."""
+    _dev(buf, None, "buf")
+    _dev(sink, None, "sink")
+    _check(lib().ppd_read_probe(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)))
+
+
 KERNEL_KINDS = {"qkv": 0, "attention": 1, "o_proj": 2, "gate_up": 3, "down": 4, "lm_head": 5,
                 "next_tree": 6}
 
@@ -387,4 +396,4 @@ def ppd_set_kernel_timer(kind, start_events=(), stop_events=()):
 
 __all__ = ["ppd_verify_step_static", "ppd_verify_batch", "ppd_next_tree", "ppd_sparse_template", "ppd_packed_weight_bytes", "ppd_pack_weight", "ppd_set_kernel_timer", "Model", "KVCache", "PPDError", "lib", "ppd_workspace_bytes", "ppd_workspace_init",
            "ppd_build_tree_mask", "ppd_verify_step", "ppd_accept", "ppd_kv_compact",
-           "ppd_device_status", "ppd_last_error"]
+           "ppd_device_status", "ppd_last_error", "ppd_read_probe"]

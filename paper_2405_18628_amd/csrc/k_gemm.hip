@@ -372,10 +372,13 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   if constexpr (kNorm) rs_request<T_pad>(g, 0, ssv);
 
   // ---- register rings.  Weight chunk c of this wave: fragments (group i,
-  // sub-tile q, k-step s) for i < GW.  Past the slice, and for groups the
-  // wave does not own, every lane reads the tile's first 16 bytes (one line),
-  // so every iteration issues the same loads.
+  // sub-tile q, k-step s) for i < GW, read through a buffer resource with
+  // the non-temporal hint (offsets from the weight's base; a packed weight
+  // is below 2 GB).  Past the slice, and for groups the wave does not own,
+  // every lane reads the tile's first 16 bytes (one line), so every
+  // iteration issues the same loads.
   const u32x4 *wp = (const u32x4 *)g.W;
+  const __amdgpu_buffer_rsrc_t wrs = rsrc_of(g.W, 0x7ffffff0u);
   u32x4 wr[RING][GW * S * 2];
   auto request_w = [&](int c, u32x4(&dw)[GW * S * 2]) {
     const bool cin = c < c1;
@@ -389,7 +392,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
       for (int q = 0; q < S; ++q)
 #pragma unroll
         for (int st = 0; st < 2; ++st)
-          dw[(i * S + q) * 2 + st] = __builtin_nontemporal_load(gp + (q * 2 + st) * FRAG);
+          dw[(i * S + q) * 2 + st] =
+              __builtin_amdgcn_raw_buffer_load_b128(wrs, (int)((gp + (q * 2 + st) * FRAG - wp) * 16), 0, 2);
     }
   };
   // activation pieces of a chunk: thread tid loads 16 bytes (4 columns

@@ -305,6 +305,36 @@ hipError_t launch_kv_compact(int dtype, void *k, void *v, int n_layers, int nkv,
 
 // ---------------------------------------------------------------------------
 
+// ---------------------------------------------------------------------------
+// HBM read probe: workgroup b reads the b-th of 256 contiguous pieces of the
+// buffer (16-byte non-temporal loads, RP per thread in flight), XORs them,
+// and adds its XOR into the sink with an atomic.
+constexpr int RP = 8;
+__global__ __launch_bounds__(256, 1) void read_probe_kernel(const u32x4 *__restrict__ buf, size_t n16,
+                                                            uint32_t *sink) {
+  const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const size_t b0 = min(n16, blockIdx.x * per), b1 = min(n16, b0 + per);
+  u32x4 acc = u32x4{0u, 0u, 0u, 0u};
+  for (size_t i = b0 + threadIdx.x; i < b1; i += (size_t)RP * blockDim.x) {
+    u32x4 r[RP];
+#pragma unroll
+    for (int j = 0; j < RP; ++j) {
+      const size_t k = i + (size_t)j * blockDim.x;
+      r[j] = __builtin_nontemporal_load(buf + (k < b1 ? k : b0));
+    }
+#pragma unroll
+    for (int j = 0; j < RP; ++j)
+      if (i + (size_t)j * blockDim.x < b1) acc ^= r[j];  // the clamped repeats are not added
+  }
+  const uint32_t v = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+  if (v) atomicXor(sink, v);
+}
+
+hipError_t launch_read_probe(const void *buf, size_t bytes, uint32_t *sink, hipStream_t s) {
+  hipLaunchKernelGGL(read_probe_kernel, dim3(256), dim3(256), 0, s, (const u32x4 *)buf, bytes / 16, sink);
+  return hipGetLastError();
+}
+
 __global__ void ws_init_kernel(uint32_t *w, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x)

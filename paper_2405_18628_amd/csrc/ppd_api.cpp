@@ -72,9 +72,12 @@ namespace {
 
 constexpr int kCUs = 256;          // MI355X compute units
 constexpr size_t kAlign = 256;
+constexpr size_t kMaxPackedBytes = 0x7ffffff0u;  // one buffer resource per packed weight
 
 size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
 int t_pad_of(int T) { return (T + 15) & ~15; }
+
+ppd_status pack_args(int kind, int rows, int cols, int *gk, int *N);
 
 ppd_status check_model(const ppd_model *m) {
   if (!m) return fail(PPD_EINVAL, "model is NULL");
@@ -91,6 +94,16 @@ ppd_status check_model(const ppd_model *m) {
     if (m->head_dim != 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need head_dim 128");
     if (m->hidden % 128) return fail(PPD_EUNSUPPORTED, "bf16 kernels need hidden %% 128 == 0");
     if (m->ffn % 64) return fail(PPD_EUNSUPPORTED, "bf16 kernels need ffn %% 64 == 0");
+    const int shapes[5][3] = {{PPD_W_QKV, (m->n_heads + 2 * m->n_kv_heads) * 128, m->hidden},
+                              {PPD_W_O, m->hidden, m->n_heads * 128},
+                              {PPD_W_GATE_UP, 2 * m->ffn, m->hidden},
+                              {PPD_W_DOWN, m->hidden, m->ffn},
+                              {PPD_W_LM_HEAD, m->vocab, m->hidden}};
+    for (const auto &w : shapes) {
+      int gk, N;
+      const ppd_status st = pack_args(w[0], w[1], w[2], &gk, &N);
+      if (st != PPD_OK) return st;
+    }
   }
   if (!m->tok_emb || !m->lm_head || !m->final_norm || (m->n_prompt > 0 && !m->prompt_emb))
     return fail(PPD_EINVAL, "embedding, LM head and final norm pointers must be set");
@@ -523,21 +536,27 @@ ppd_status pack_args(int kind, int rows, int cols, int *gk, int *N) {
     case PPD_W_QKV:
       if (rows % 128) return fail(PPD_EUNSUPPORTED, "w_qkv needs rows %% 128 == 0 (head_dim 128)");
       *gk = GEMM_QKV, *N = rows;
-      return PPD_OK;
+      break;
     case PPD_W_O:
     case PPD_W_DOWN:
       if (rows % 128) return fail(PPD_EUNSUPPORTED, "w_o / w_down need rows (hidden) %% 128 == 0");
       *gk = GEMM_RESID, *N = rows;
-      return PPD_OK;
+      break;
     case PPD_W_GATE_UP:
       if (rows % 128) return fail(PPD_EUNSUPPORTED, "w_gate_up needs rows (2 ffn) %% 128 == 0");
       *gk = GEMM_SWIGLU, *N = rows / 2;
-      return PPD_OK;
+      break;
     case PPD_W_LM_HEAD:
       *gk = GEMM_LOGITS, *N = rows;
-      return PPD_OK;
+      break;
+    default:
+      return fail(PPD_EINVAL, "unknown weight kind %d", kind);
   }
-  return fail(PPD_EINVAL, "unknown weight kind %d", kind);
+  // the GEMM reads a packed weight through one buffer resource: < 2 GB
+  const size_t bytes = (size_t)gemm_groups_of(*gk, *N) * gemm_sub_of(*gk) * 16 * cols * sizeof(bf16_t);
+  if (bytes > kMaxPackedBytes)
+    return fail(PPD_EUNSUPPORTED, "a packed weight of %zu bytes exceeds %zu", bytes, kMaxPackedBytes);
+  return PPD_OK;
 }
 
 }  // namespace
@@ -721,6 +740,13 @@ ppd_status ppd_next_tree(int32_t T, const int32_t *parent, const int32_t *ids, i
   if (g_timer.kind == TK_NEXT) g_timer.next = 0;  // one timed launch per call
   timer_events(TK_NEXT, &p.ev_start, &p.ev_stop);
   PPD_TRY_HIP(launch_next_tree(p, n_depths, (hipStream_t)stream));
+  return PPD_OK;
+}
+
+ppd_status ppd_read_probe(const void *buf, size_t bytes, uint32_t *sink, void *stream) {
+  if (!buf || !sink) return fail(PPD_EINVAL, "NULL argument");
+  if (bytes % 16 || ((uintptr_t)buf & 15)) return fail(PPD_EINVAL, "buf and bytes must be 16-byte aligned");
+  PPD_TRY_HIP(launch_read_probe(buf, bytes, sink, (hipStream_t)stream));
   return PPD_OK;
 }
 

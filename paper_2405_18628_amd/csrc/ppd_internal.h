@@ -44,11 +44,11 @@ __device__ __forceinline__ floatx4 mfma16x16x32(bf16x8 a, bf16x8 b, floatx4 c) {
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
 }
-// 16-byte load at device scope (sc1): it misses this compute unit's L1 and
-// is served by the XCD's L2, where another compute unit of the XCD stored
-// the data
+// 16-byte load that misses L1 (sc0): data written by another compute unit of
+// this XCD is read from the shared L2 (each address is read once per
+// dispatch, after the writers' arrival)
 __device__ __forceinline__ floatx4 load_l2(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 16));
+  return __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 1));
 }
 
 // the XCD this wave runs on
@@ -259,6 +259,7 @@ hipError_t launch_kv_compact(int dtype, void *k, void *v, int n_layers, int nkv,
                              int L, const int32_t *path, int path_len, const int32_t *n_path,
                              int32_t *len_dev, hipStream_t s);
 hipError_t launch_ws_init(void *ws, size_t n_words, hipStream_t s);
+hipError_t launch_read_probe(const void *buf, size_t bytes, uint32_t *sink, hipStream_t s);
 
 // fp32 path (simple kernels for float32 models)
 // xg = x * gain and r[t] = 1/sqrt(mean(x^2)+eps); r is stored after xg's T_pad rows

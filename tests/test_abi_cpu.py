@@ -145,6 +145,12 @@ def test_packed_weight_sizes_and_rejections():
     assert L.ppd_pack_weight(ppd.PPD_W_O, 512, 512, f, None, None) == ppd.PPD_EINVAL
     assert L.ppd_pack_weight(ppd.PPD_W_O, 500, 512, f, f, None) == ppd.PPD_EUNSUPPORTED
     assert L.ppd_pack_weight(9, 512, 512, f, f, None) == ppd.PPD_EINVAL
+    # a packed weight is read through one buffer resource: at most 0x7ffffff0
+    # bytes (2^30 - 8 rows of 1024 bf16 columns fit, 2^30 do not)
+    ok_rows = (0x7ffffff0 // (2 * 1024)) // 16 * 16
+    assert ppd.ppd_packed_weight_bytes(ppd.PPD_W_LM_HEAD, ok_rows, 1024) == ok_rows * 1024 * 2
+    assert L.ppd_packed_weight_bytes(ppd.PPD_W_LM_HEAD, 1 << 20, 1024) == 0
+    assert L.ppd_pack_weight(ppd.PPD_W_LM_HEAD, 1 << 20, 1024, f, f, None) == ppd.PPD_EUNSUPPORTED
 
 
 def test_next_tree_rejects_before_enqueue():
@@ -243,3 +249,13 @@ def test_verify_batch_rejects_before_enqueue():
     assert call([0, 0], [64, 64], wsb=ws_bytes - 1) == ppd.PPD_EWORKSPACE
     mf, kf = _fake_model(ppd.PPD_F32, head_dim=64, hidden=256, ffn=688)
     assert call([0, 0], [8, 8], model=mf) == ppd.PPD_EUNSUPPORTED       # batches need bf16
+
+
+def test_read_probe_rejects_before_enqueue():
+    """The HBM read probe checks its arguments on the host."""
+    L = ppd.lib()
+    f = 0x4000
+    assert L.ppd_read_probe(None, 16, f, None) == ppd.PPD_EINVAL
+    assert L.ppd_read_probe(f, 16, None, None) == ppd.PPD_EINVAL
+    assert L.ppd_read_probe(f, 24, f, None) == ppd.PPD_EINVAL
+    assert L.ppd_read_probe(f + 4, 16, f, None) == ppd.PPD_EINVAL

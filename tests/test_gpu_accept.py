@@ -281,3 +281,18 @@ def test_compact_clamps_count_to_path_length():
     assert torch.equal(k[:, :, L + 3:], k0[:, :, L + 3:])
     assert torch.equal(v[:, :, :, L + 3:], v0[:, :, :, L + 3:])
     assert torch.equal(k[:, :, :L], k0[:, :, :L])
+
+
+def test_read_probe_reads_every_byte():
+    """The HBM read probe (the measurement aid behind bench.py
+    --stream-ceiling) reads the whole buffer: its XOR sink equals the XOR of
+    every 32-bit word, for sizes that leave ragged pieces."""
+    rng = np.random.default_rng(5)
+    for n_words in (4, 4 * 1000, 4 * 65537, 4 * (1 << 20) + 12):
+        host = rng.integers(0, 2 ** 32, size=n_words, dtype=np.uint64).astype(np.uint32)
+        buf = torch.from_numpy(host.view(np.int32)).cuda()
+        sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+        ppd.ppd_read_probe(buf, sink)
+        torch.cuda.synchronize()
+        want = np.bitwise_xor.reduce(host)
+        assert np.uint32(sink.cpu().numpy().view(np.uint32)[0]) == want, n_words
