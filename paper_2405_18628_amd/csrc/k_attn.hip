@@ -39,8 +39,8 @@
 //                                valid B operand.
 // Softmax runs in fp32 in the log2 domain against a lazily moved reference
 // (rescaling only when a block's maximum exceeds it by more than 2^8); P
-// enters the PV product as the sum of three bf16 parts (hi, mid, lo), i.e. to
-// about 24 significant bits.
+// enters the PV product as the sum of two bf16 parts (hi, lo), i.e. to about
+// 16 significant bits.
 #include <algorithm>
 
 #include "ppd_internal.h"
@@ -353,26 +353,20 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnLaunch p) {
       psum += pv[e];
     }
     Q.l_run += psum;
-    // P = hi + mid + lo, all bf16 (each the rounding of what the earlier
-    // parts leave): the PV product carries P to ~24 significant bits, close
-    // to fp32 (three MFMAs per tile, the smallest part first)
-    float plo[8], pll[8];
+    // P = hi + lo, both bf16 (lo the rounding of what hi leaves): the PV
+    // product carries P to ~16 significant bits, as the activations are
+    // carried (two MFMAs per tile, the smaller part first)
+    float plo[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      plo[e] = pv[e] - bf16_to_f32(f32_to_bf16(pv[e]));
-      pll[e] = plo[e] - bf16_to_f32(f32_to_bf16(plo[e]));
-    }
+    for (int e = 0; e < 8; ++e) plo[e] = pv[e] - bf16_to_f32(f32_to_bf16(pv[e]));
     const u32x4 pb = u32x4{pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
                            pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
     const u32x4 pl = u32x4{pack_bf16x2(plo[0], plo[1]), pack_bf16x2(plo[2], plo[3]),
                            pack_bf16x2(plo[4], plo[5]), pack_bf16x2(plo[6], plo[7])};
-    const u32x4 pz = u32x4{pack_bf16x2(pll[0], pll[1]), pack_bf16x2(pll[2], pll[3]),
-                           pack_bf16x2(pll[4], pll[5]), pack_bf16x2(pll[6], pll[7])};
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
       const int r = dt * 16 + lr;
       const u32x4 va = *(const u32x4 *)(vs_l + (r ^ (par << 1)) * 64 + ((lg ^ ((lr >> 2) & 3)) * 16));
-      Q.o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pz), Q.o[dt]);
       Q.o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pl), Q.o[dt]);
       Q.o[dt] = mfma16x16x32(as_bf16x8(va), as_bf16x8(pb), Q.o[dt]);
     }

@@ -517,9 +517,16 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   }
 
   // ---- split tile: partials to L2, arrive, wait for the tile's other
-  // slices, finish token blocks ks, ks + s, ...  Partial (tile gt, slice
-  // sl): [wave][i][q][m][lane] floatx4.
+  // slices, finish this slice's items.  Item (group i, token block m) is
+  // finished by slice fin(i, m): QKV and gate/up deal the tile's items to the
+  // slices in turn ((i MT + m) % s); the others keep whole token blocks
+  // together (their epilogues reduce over the tile's rows): m % s.  A slice
+  // stores the partial sums of the items other slices finish and keeps its
+  // own in registers.  Partial (tile gt, slice sl): [wave][i][q][m][lane]
+  // floatx4.
   constexpr int PW = GW * S * MT;  // floatx4 per lane per wave
+  constexpr bool kItems = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
+  auto fin = [&](int i, int m) { return kItems ? (i * MT + m) % s : m % s; };
   float *part = g.part + ((size_t)gt * s + ks) * (4 * PW * 64 * 4);
 #pragma unroll
   for (int i = 0; i < GW; ++i) {
@@ -528,18 +535,14 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
     for (int q = 0; q < S; ++q)
 #pragma unroll
       for (int m = 0; m < MT; ++m)
-        *(floatx4 *)(part + ((size_t)((wave * GW + i) * S + q) * MT + m) * 256 + lane * 4) = acc[i][q][m];
+        if (fin(i, m) != ks)
+          *(floatx4 *)(part + ((size_t)((wave * GW + i) * S + q) * MT + m) * 256 + lane * 4) = acc[i][q][m];
   }
-  constexpr bool kItems = KIND == GEMM_QKV || KIND == GEMM_SWIGLU;
-  // the items of token block m this slice finishes: QKV and gate/up deal the
-  // tile's (group, token block) items to the slices in turn (item i MT + m
-  // to slice (i MT + m) % s); the others keep whole token blocks together
-  // (their epilogues reduce over the tile's rows): token block m to slice
-  // m % s
+  // the items of token block m this slice finishes
   auto mine = [&](int m) {
     unsigned gm = 0;
 #pragma unroll
-    for (int i = 0; i < GW; ++i) gm |= (kItems ? (i * MT + m) % s == ks : m % s == ks) ? 1u << i : 0u;
+    for (int i = 0; i < GW; ++i) gm |= fin(i, m) == ks ? 1u << i : 0u;
     return gm;
   };
   // the epilogue inputs of this slice's first token block, requested now:
@@ -562,9 +565,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
   __syncthreads();
   const float *tile_part = g.part + (size_t)gt * s * (4 * PW * 64 * 4);
   const __amdgpu_buffer_rsrc_t rp = rsrc_of(tile_part, (uint32_t)s * 4 * PW * 64 * 16);
-  // the slices' partials are requested SB at a time (one round trip per
-  // batch; past the last slice the loads repeat slice 0 and are not added)
-  // and added in slice order
+  // the other slices' partials are requested SB at a time (one round trip
+  // per batch; past the last slice nothing is loaded) and added in slice
+  // order, this slice's own from its registers
   constexpr int SB = GW * S <= 2 ? 8 : 4;
   auto finish_block = [&](int m, unsigned gmask) {
     floatx4 am[GW][S];
@@ -576,14 +579,15 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
       floatx4 buf[SB][GW][S];
 #pragma unroll
       for (int b = 0; b < SB; ++b) {
-        const int sl = sb + b < s ? sb + b : 0;
+        const int sl = sb + b;
 #pragma unroll
         for (int i = 0; i < GW; ++i)
 #pragma unroll
           for (int q = 0; q < S; ++q) {
             const uint32_t off =
                 (uint32_t)((((size_t)sl * 4 * PW + ((wave * GW + i) * S + q) * MT + m) * 64 + lane) * 16);
-            buf[b][i][q] = i < live && ((gmask >> i) & 1u) ? load_l2(rp, off) : floatx4{0.f, 0.f, 0.f, 0.f};
+            buf[b][i][q] = sl < s && sl != ks && i < live && ((gmask >> i) & 1u) ? load_l2(rp, off)
+                                                                                 : floatx4{0.f, 0.f, 0.f, 0.f};
           }
       }
 #pragma unroll
@@ -592,7 +596,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
 #pragma unroll
           for (int i = 0; i < GW; ++i)
 #pragma unroll
-            for (int q = 0; q < S; ++q) am[i][q] += buf[b][i][q];
+            for (int q = 0; q < S; ++q) am[i][q] += sb + b == ks ? acc[i][q][m] : buf[b][i][q];
         }
     }
     EpiIn<KIND, GW> in;
@@ -609,7 +613,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(GemmLaunch g) {
       if (gmask) finish_block(m, gmask);  // uniform: no barriers in these epilogues
     }
   } else {
-    for (int m = ks; m < MT; m += s) finish_block(m, ~0u);
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+      if (m % s == ks) finish_block(m, ~0u);  // uniform in the workgroup
   }
 }
 

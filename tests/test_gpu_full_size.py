@@ -4,19 +4,18 @@ Full width: the 1.4B, 7B, 13B (T in {16, 32, 64, 128}) and 7B-32k workloads
 with their real hidden size, heads, FFN width, vocabulary, cache length and
 tree, i.e. the same kernel launch configurations (tiles, K splits, attention
 splits) that bench.py times -- those depend on the widths, T and L, not on
-the number of layers -- with the decoder cut to one layer.  (Deeper bf16
-networks drift apart from any independent bf16 computation through rounding
-amplification, which is why full depth is checked by properties below.)  The oracle computes sampled nodes one by one: a node's logits depend
-only on its ancestors, so the oracle runs the ancestor closure of the sampled
-nodes as its own tree.
+the number of layers -- with the decoder cut to one layer, every node
+compared (and, where named, sampled nodes: a node's logits depend only on
+its ancestors, so the oracle runs the ancestor closure of the sampled nodes
+as its own tree).  The logits and greedy tokens of the full-depth steps are
+compared with the oracle in test_gpu_full_depth.py.
 
-Full depth: the 32-layer 7B benchmark configuration itself (and the other
-workloads at full depth), checked by properties that hold at any size:
+Full depth, here: the 32-layer 7B benchmark configuration itself (and the
+other workloads at full depth) checked by properties that hold at any size:
 bitwise determinism, sampled nodes bitwise unchanged when every node outside
 their ancestor chains gets other tokens, finite logits with a clean device
-status, and
-acceptance / compaction bit-exact against the oracle's acceptance on the
-GPU's greedy tokens.
+status, and acceptance / compaction bit-exact against the oracle's
+acceptance on the GPU's greedy tokens.
 """
 import numpy as np
 import pytest
