@@ -33,8 +33,9 @@
 //  * a tile's s slices finish in the same kernel: each stores its partial
 //    sums (to L2: all of a tile's workgroups share one XCD), arrives at the
 //    tile's counter (an atomic), waits for the others (bounded spin) and
-//    finishes 1/s of the tile's token blocks, adding the partials in slice
-//    order (deterministic);
+//    finishes its share of the tile (QKV, gate/up: (group, token block)
+//    items dealt in turn; the others: whole token blocks), adding the
+//    partials in slice order (deterministic);
 //  * epilogues: RMSNorm row scale, RoPE + query / key / value stores into the
 //    cache (QKV), residual add + per-tile sum of squares (output / down
 //    projections), SwiGLU (gate/up), logits + per-tile argmax (LM head).
