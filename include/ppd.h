@@ -32,8 +32,9 @@
  * Memory.  Every pointer marked "device" is HIP device memory owned by the
  *   caller and must stay valid until the enqueued work completes.  The
  *   library allocates nothing and keeps no state besides the thread-local
- *   error string and the optional thread-local kernel timer.  Weights, caches and activations of PPD_BF16 models are
- *   bfloat16 (raw 16-bit words); PPD_F32 models use float32 throughout.
+ *   error string and the optional thread-local kernel timer.  Weights and
+ *   caches of PPD_BF16 models are bfloat16 (raw 16-bit words), their
+ *   activations fp32; PPD_F32 models use float32 throughout.
  * Streams.  Device calls enqueue on `stream` (a hipStream_t; NULL = default
  *   stream) and return without waiting.  verify -> accept -> compact must be
  *   enqueued in that order on one stream; no host synchronisation is needed
@@ -256,10 +257,10 @@ ppd_status ppd_accept(int32_t T, const int32_t *parent, const int32_t *ids,
  * device uint32) receives the step's device status word (ppd_device_status
  * bits), the header of the array being cleared at the start of every call.
  * PPD_EWORKSPACE when the step needs more than PPD_STATIC_WS_BYTES
- * (ppd_workspace_bytes(model, T, capacity); a Vicuna-13B-shaped step with a
- * 64-node tree needs about 36 MiB), nothing enqueued.  All calls on one GPU
- * share the array: calls that may overlap on one GPU (unordered streams,
- * several threads) race and must not be made.
+ * (ppd_workspace_bytes(model, T, capacity); a Vicuna-13B-shaped step needs
+ * about 15 MiB with a 64-node tree, 30 MiB with 128), nothing enqueued.  All
+ * calls on one GPU share the array: calls that may overlap on one GPU
+ * (unordered streams, several threads) race and must not be made.
  */
 #define PPD_STATIC_WS_BYTES (64u << 20)
 ppd_status ppd_verify_step_static(const ppd_model *model, const ppd_kv *kv, int32_t L, int32_t T,
