@@ -74,9 +74,10 @@ def _case(name, n_layers):
 
 
 @pytest.mark.parametrize("name,spec", [("1.4b", None), ("7b", None), ("7b", "root"),
+                                       ("7b", "total:48"), ("7b", "total:112"),
                                        ("13b", "total:16"), ("13b", "total:32"),
-                                       ("13b", "total:64"), ("13b", "total:128"),
-                                       ("7b-32k", None)])
+                                       ("13b", "total:64"), ("13b", "total:96"),
+                                       ("13b", "total:128"), ("7b-32k", None)])
 def test_full_width_all_nodes(name, spec):
     """One decoder layer at the workload's full width: every node's logits,
     greedy token and tree keys / values against the oracle."""

@@ -83,7 +83,7 @@ def small_case():
 
 
 @pytest.mark.parametrize("spec", ["total:40", "chain:1", "total:16", "total:17", "total:64",
-                                  "total:100", "total:128"])
+                                  "total:90", "total:100", "total:128"])
 def test_small_bf16_tree_sizes(small_case, spec):
     case = small_case
     tree = tree_for(case, spec=spec)
