@@ -22,10 +22,11 @@
 //  * the groups are dealt to eight workgroup sets b % 8 (each runs on one
 //    XCD: the dispatcher deals workgroups round-robin over the XCDs) and,
 //    within a set, to TX tiles x s K-slices over its 32 workgroups: a
-//    tall tile over a slice of K keeps the activation bytes each compute unit
-//    must read small next to its weight bytes (a compute unit's load path,
-//    not HBM, is the limit when every workgroup re-reads the whole T x K
-//    activation block);
+//    tall tile over a slice of K keeps each workgroup's per-chunk work
+//    (loading and staging the T x 64 activation chunk as two bf16 planes,
+//    two products per fragment, one wave per SIMD) small next to the weight
+//    bytes it streams; a whole-K tile of few groups is bound by that work,
+//    not by HBM;
 //  * the activation chunk (fp32, the same for all of a slice's workgroups,
 //    an L2 hit) is staged per chunk in a double-buffered, XOR-swizzled LDS
 //    slot as the two bf16 parts; norm consumers form RMSNorm's x * gain here
